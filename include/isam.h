@@ -1,0 +1,149 @@
+/*
+ * isam.h -- C ABI of the MI355X (gfx950) library for the dense hot path that
+ * ISA Mapper (Sotoudeh et al., SysML 2019, arXiv 1810.09958) maps deep
+ * learning layers onto: matrix multiplication, the separable depthwise
+ * convolution factored into a depthwise stencil plus a matrix multiplication,
+ * and the GRU recurrence.
+ *
+ * Conventions for every entry point
+ *   - Tensor pointers are DEVICE pointers (hipMalloc'd or torch CUDA tensors)
+ *     unless stated otherwise.  Layouts are row-major; images are NHWC.
+ *   - bf16 tensors hold 16-bit bfloat16 patterns; fp32 accumulation always.
+ *   - The caller owns every buffer, including the workspace.  The library
+ *     allocates no device memory.  Pointers are borrowed until the work
+ *     queued on `stream` has finished.
+ *   - Calls are asynchronous: they validate their arguments on the host,
+ *     enqueue kernels on `stream` (a hipStream_t; NULL = default stream) and
+ *     return.  There is no host synchronisation inside a call.
+ *   - Validation happens before any HIP call.  A non-OK status means nothing
+ *     was launched, except ISAM_ERR_HIP, which reports a failed launch.
+ *     isam_last_error() holds a readable reason for the last non-OK status
+ *     on the calling thread.  No C++ exception crosses this interface.
+ *   - Outputs must not overlap inputs (detected by address range).
+ *   - Each operand's addressed extent must be below 2^31 bytes
+ *     (ISAM_ERR_UNSUPPORTED otherwise).
+ *   - Entry points are thread-safe; the only global state is a cache of
+ *     device properties.
+ */
+#ifndef ISAM_H
+#define ISAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { ISAM_F32 = 0, ISAM_BF16 = 1 } isam_dtype_t;
+
+typedef enum {
+    ISAM_OK = 0,
+    ISAM_ERR_INVALID_ARG = 1, /* bad size, pointer, leading dimension, dtype or aliasing */
+    ISAM_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
+    ISAM_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the *_workspace_size query */
+    ISAM_ERR_HIP = 4          /* a HIP launch failed; isam_last_error() has the HIP message */
+} isam_status_t;
+
+/*
+ * Matrix multiplication, the paper's first listing (Section 2):
+ *   C[i][j] (+)= sum_k a(i,k) * b(k,j)
+ * The listing accumulates into C; accumulate = 1 keeps that form (C += A.B),
+ * accumulate = 0 overwrites (C = A.B).  The K order of the sum is free
+ * (Section 2.1); results are compared with a tolerance, not bit for bit.
+ *
+ *   trans_a = 0: A is [M][K], element a(i,k) = A[i*lda + k], lda >= K
+ *   trans_a = 1: A is [K][M], element a(i,k) = A[k*lda + i], lda >= M
+ *   trans_b = 0: B is [K][N], element b(k,j) = B[k*ldb + j], ldb >= N
+ *   trans_b = 1: B is [N][K], element b(k,j) = B[j*ldb + k], ldb >= K
+ *   C is [M][N] with ldc >= N, dtype c_type (ISAM_F32 or ISAM_BF16; bf16
+ *   outputs are rounded to nearest-even from the fp32 accumulator).
+ *   ab_type is the shared dtype of A and B.
+ * M == 0 or N == 0: no-op.  K == 0: C = 0 (accumulate = 0) or unchanged.
+ * workspace: device buffer of at least isam_gemm_workspace_size(...) bytes,
+ * used for split-K partial sums; with a smaller (or NULL) workspace the call
+ * still succeeds on a plan without split-K.
+ */
+isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                        int ab_type, const void* A, int64_t lda, const void* B, int64_t ldb,
+                        int accumulate, int c_type, void* C, int64_t ldc,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace (bytes) the preferred plan of isam_gemm needs for these sizes; 0 if none. */
+size_t isam_gemm_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                                int ab_type, int c_type);
+
+/*
+ * Separable depthwise convolution, the paper's third listing (Section 2):
+ *   y[b][i][j][k] = sum_{di,dj,q,r} x~[b][s*i+di-pad][s*j+dj-pad][q]
+ *                                   * D[di][dj][q][r] * P[c*q + r][k]
+ * computed in the factored form the mapper exposes by distributing the
+ * pointwise product out of the (di, dj) sum (Section 2.3): first the
+ * depthwise stencil Y[b][i][j][c*q+r] = sum_{di,dj} x~ * D, then the
+ * pointwise matrix product y = Y . P with M = batch*Ho*Wo, K = C_in*c,
+ * N = C_out.  x~ is x with zero padding `pad`.
+ *
+ *   x          [batch][H][W][C_in]                  (in_type)
+ *   dw_filter  [kh][kw][C_in][depth_mult]           (in_type)
+ *   pw_weight  [C_in*depth_mult][C_out]             (in_type)
+ *   y          [batch][Ho][Wo][C_out]               (out_type)
+ *   Ho = (H + 2*pad - kh)/stride + 1, Wo = (W + 2*pad - kw)/stride + 1 (both > 0)
+ * The intermediate Y is held in the workspace in in_type (bf16 Y is rounded
+ * to nearest-even).  batch == 0: no-op.
+ */
+isam_status_t isam_dwsep_conv(int64_t batch, int64_t H, int64_t W, int64_t C_in, int64_t depth_mult,
+                              int64_t kh, int64_t kw, int64_t stride, int64_t pad, int64_t C_out,
+                              int in_type, const void* x, const void* dw_filter, const void* pw_weight,
+                              int out_type, void* y, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+size_t isam_dwsep_conv_workspace_size(int64_t batch, int64_t H, int64_t W, int64_t C_in,
+                                      int64_t depth_mult, int64_t kh, int64_t kw, int64_t stride,
+                                      int64_t pad, int64_t C_out, int in_type, int out_type);
+
+/*
+ * GRU forward over T steps.  GRU cells map onto matrix products plus
+ * element-wise work (Section 6.1); the recurrence is scheduled as a priming
+ * iteration, a recursive iteration with the weights persistent on chip, and a
+ * finish iteration (Section 3.6), with the gate math fused to the products
+ * (Section 6.2.2).  Cell, with gate blocks stacked r, z, n in W and U:
+ *   r   = sigmoid(W_r x_t + U_r h_{t-1} + b_r)
+ *   z   = sigmoid(W_z x_t + U_z h_{t-1} + b_z)
+ *   n   = tanh(W_n x_t + b_n + r * (U_n h_{t-1} + b_hn))
+ *   h_t = (1 - z) * n + z * h_{t-1}
+ *
+ *   x        [T][batch][input_size]      (w_type)
+ *   W        [3*hidden][input_size]      (w_type)
+ *   U        [3*hidden][hidden]          (w_type)
+ *   h0       [batch][hidden] fp32, or NULL for zeros
+ *   bias     [3*hidden] fp32 (b_r, b_z, b_n), or NULL
+ *   bias_hn  [hidden] fp32, or NULL (the PyTorch b_hn form)
+ *   h_seq    [T][batch][hidden] fp32 output, or NULL
+ *   h_T      [batch][hidden] fp32 output, or NULL (at least one of the two)
+ * hidden must be a multiple of 8 (bf16) or 4 (fp32).  The bf16 path rounds
+ * h_{t-1} to bf16 only as the matrix-core operand; the state stays fp32.
+ * T == 0: h_T = h0 (or zeros).  batch == 0: no-op.
+ * The recurrent kernel needs all its workgroups resident at once; if the
+ * device cannot hold them the call returns ISAM_ERR_UNSUPPORTED.
+ */
+isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
+                               int w_type, const void* x, const float* h0, const void* W,
+                               const void* U, const float* bias, const float* bias_hn,
+                               float* h_seq, float* h_T, void* workspace, size_t workspace_bytes,
+                               void* stream);
+
+size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_size,
+                                       int64_t hidden_size, int w_type);
+
+/* Static text for a status code. */
+const char* isam_status_string(int status);
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+const char* isam_last_error(void);
+/* Library version, major*10000 + minor*100 + patch. */
+int isam_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISAM_H */

@@ -1,0 +1,499 @@
+// C-ABI layer: argument validation (pure host code, no HIP call), plan
+// selection, and kernel dispatch.
+//
+// Plan selection is this library's counterpart of the paper's "Approach"
+// interface (Section 4): every tiling, split and rasterisation choice is made
+// in one place (the plan_* functions below) from the problem shape and the
+// device's compute-unit count, and can be overridden for tuning with the
+// environment variable ISAM_GEMM_CONFIG="tile=<0-5>,splits=<n>,group=<n>,xcd=<0|1>".
+// ISAM_LOG=1 prints each chosen plan to stderr.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "../../include/isam.h"
+#include "kernels.hpp"
+
+using namespace isam;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+isam_status_t fail(isam_status_t st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    try {
+        g_last_error = buf;
+    } catch (...) {
+    }
+    return st;
+}
+
+isam_status_t hip_fail(hipError_t e, const char* what) {
+    return fail(ISAM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool log_enabled() {
+    static const bool on = [] {
+        const char* v = getenv("ISAM_LOG");
+        return v && v[0] && v[0] != '0';
+    }();
+    return on;
+}
+
+bool valid_dtype(int t) { return t == ISAM_F32 || t == ISAM_BF16; }
+size_t dsize(int t) { return t == ISAM_BF16 ? 2 : 4; }
+
+constexpr int64_t kMaxExtent = (int64_t(1) << 31) - 1;
+
+bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
+    if (!a || !b || an == 0 || bn == 0) return false;
+    uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + bn && b0 < a0 + an;
+}
+
+// Compute units of the current device, cached.  Falls back to the MI355X
+// count when no device is visible (host-only queries such as workspace sizes).
+int device_cus() {
+    static std::mutex mu;
+    static int cache[64];
+    static bool have[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+        (void)hipGetLastError();
+        return 256;
+    }
+    std::unique_lock<std::mutex> lk(mu, std::defer_lock);
+    try {
+        lk.lock();
+    } catch (...) {
+        return 256;
+    }
+    if (!have[dev]) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) {
+            (void)hipGetLastError();
+            cus = 256;
+        }
+        cache[dev] = cus;
+        have[dev] = true;
+    }
+    return cache[dev];
+}
+
+// ---------------------------------------------------------------------------
+// GEMM plan
+// ---------------------------------------------------------------------------
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus) {
+    GemmPlan p{};
+    p.vec = 1;
+    p.k_splits = 1;
+    p.k_per_split = K;
+    p.group_m = 8;
+    p.xcd_remap = 1;
+    int bm, bn, bk;
+    auto tiles = [&](int t) {
+        tile_dims(t, ab_type, &bm, &bn, &bk);
+        return cdiv(M, bm) * cdiv(N, bn);
+    };
+    if (N <= 32) {
+        p.tile = kTile128x32;
+    } else if (tiles(kTile256x256) >= cus) {
+        p.tile = kTile256x256;
+    } else if (tiles(kTile256x128) >= cus) {
+        p.tile = kTile256x128;
+    } else if (tiles(kTile128x128) >= cus) {
+        p.tile = kTile128x128;
+    } else if (tiles(kTile128x64) >= cus) {
+        p.tile = kTile128x64;
+    } else {
+        p.tile = kTile64x64;
+    }
+    const int64_t nt = tiles(p.tile);
+    // Split K when the tile grid leaves compute units idle and K is deep
+    // enough that every split still runs several K tiles.
+    if (nt < 2 * (int64_t)cus && K >= 8 * bk) {
+        int64_t want = cdiv(2 * (int64_t)cus, nt);
+        int64_t max_by_k = K / (4 * bk);
+        int64_t s = std::max<int64_t>(1, std::min<int64_t>(want, std::min<int64_t>(max_by_k, 16)));
+        if (s > 1) {
+            p.k_per_split = cdiv(cdiv(K, s), bk) * bk;
+            p.k_splits = (int)cdiv(K, p.k_per_split);
+        }
+    }
+    if (p.k_splits <= 1) {
+        p.k_splits = 1;
+        p.k_per_split = K;
+    }
+    // Tuning override.
+    if (const char* env = getenv("ISAM_GEMM_CONFIG")) {
+        int v;
+        const char* s;
+        if ((s = strstr(env, "tile=")) && sscanf(s + 5, "%d", &v) == 1 && v >= 0 && v < kTileCount) p.tile = v;
+        if ((s = strstr(env, "group=")) && sscanf(s + 6, "%d", &v) == 1 && v > 0) p.group_m = v;
+        if ((s = strstr(env, "xcd=")) && sscanf(s + 4, "%d", &v) == 1) p.xcd_remap = v ? 1 : 0;
+        if ((s = strstr(env, "splits=")) && sscanf(s + 7, "%d", &v) == 1 && v >= 1) {
+            tile_dims(p.tile, ab_type, &bm, &bn, &bk);
+            p.k_per_split = std::max<int64_t>(bk, cdiv(cdiv(K, v), bk) * bk);
+            p.k_splits = (int)std::max<int64_t>(1, cdiv(K, p.k_per_split));
+            if (p.k_splits == 1) p.k_per_split = K;
+        }
+    }
+    return p;
+}
+
+size_t gemm_ws_bytes(const GemmPlan& p, int64_t M, int64_t N) {
+    return p.k_splits > 1 ? (size_t)p.k_splits * (size_t)M * (size_t)N * sizeof(float) : 0;
+}
+
+bool vec_ok(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type, const void* A,
+            int64_t lda, const void* B, int64_t ldb) {
+    const int64_t E = ab_type == ISAM_BF16 ? 8 : 4;
+    const int64_t es = (int64_t)dsize(ab_type);
+    if (((uintptr_t)A & 15) || ((uintptr_t)B & 15)) return false;
+    if ((lda * es) % 16 || (ldb * es) % 16) return false;
+    if ((trans_a ? M : K) % E) return false;
+    if ((trans_b ? K : N) % E) return false;
+    return true;
+}
+
+isam_status_t validate_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type,
+                            const void* A, int64_t lda, const void* B, int64_t ldb, int accumulate,
+                            int c_type, const void* C, int64_t ldc, const char* who) {
+    if ((trans_a != 0 && trans_a != 1) || (trans_b != 0 && trans_b != 1))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: trans_a/trans_b must be 0 or 1", who);
+    if (accumulate != 0 && accumulate != 1)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: accumulate must be 0 or 1", who);
+    if (M < 0 || N < 0 || K < 0)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: negative size M=%lld N=%lld K=%lld", who, (long long)M,
+                    (long long)N, (long long)K);
+    if (!valid_dtype(ab_type) || !valid_dtype(c_type))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: dtype must be ISAM_F32 (0) or ISAM_BF16 (1)", who);
+    if (M == 0 || N == 0) return ISAM_OK;
+    if (!C) return fail(ISAM_ERR_INVALID_ARG, "%s: C is NULL", who);
+    if (ldc < N) return fail(ISAM_ERR_INVALID_ARG, "%s: ldc=%lld < N=%lld", who, (long long)ldc, (long long)N);
+    const int64_t c_ext = (M - 1) * ldc + N;
+    if (c_ext * (int64_t)dsize(c_type) > kMaxExtent)
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: C spans more than 2^31 bytes", who);
+    if (K == 0) return ISAM_OK;
+    if (!A || !B) return fail(ISAM_ERR_INVALID_ARG, "%s: A or B is NULL", who);
+    const int64_t need_lda = trans_a ? M : K, need_ldb = trans_b ? K : N;
+    if (lda < need_lda)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: lda=%lld < %lld", who, (long long)lda, (long long)need_lda);
+    if (ldb < need_ldb)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: ldb=%lld < %lld", who, (long long)ldb, (long long)need_ldb);
+    const int64_t es = (int64_t)dsize(ab_type);
+    const int64_t a_ext = trans_a ? (K - 1) * lda + M : (M - 1) * lda + K;
+    const int64_t b_ext = trans_b ? (N - 1) * ldb + K : (K - 1) * ldb + N;
+    if (a_ext * es > kMaxExtent || b_ext * es > kMaxExtent)
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: an operand spans more than 2^31 bytes", who);
+    const size_t cb = (size_t)c_ext * dsize(c_type);
+    if (overlaps(C, cb, A, (size_t)(a_ext * es)) || overlaps(C, cb, B, (size_t)(b_ext * es)))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: C overlaps A or B", who);
+    return ISAM_OK;
+}
+
+isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type,
+                       const void* A, int64_t lda, const void* B, int64_t ldb, int accumulate,
+                       int c_type, void* C, int64_t ldc, const float* bias, void* workspace,
+                       size_t workspace_bytes, hipStream_t stream, const char* who) {
+    GemmPlan p = plan_gemm(M, N, K, ab_type, device_cus());
+    const size_t need = gemm_ws_bytes(p, M, N);
+    if (p.k_splits > 1 && (!workspace || workspace_bytes < need)) {
+        p.k_splits = 1;
+        p.k_per_split = K;
+    }
+    p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
+    if (!p.vec) {
+        // The element-wise loader is instantiated for the small tiles only.
+        if (p.tile != kTile64x64 && p.tile != kTile128x32) p.tile = kTile64x64;
+    }
+    if (log_enabled())
+        fprintf(stderr, "[isam] %s M=%lld N=%lld K=%lld ta=%d tb=%d ab=%d c=%d tile=%d vec=%d splits=%d kps=%lld group=%d xcd=%d\n",
+                who, (long long)M, (long long)N, (long long)K, trans_a, trans_b, ab_type, c_type, p.tile, p.vec,
+                p.k_splits, (long long)p.k_per_split, p.group_m, p.xcd_remap);
+    GemmArgs a{};
+    a.A = A;
+    a.B = B;
+    a.C = C;
+    a.partial = static_cast<float*>(workspace);
+    a.bias = bias;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.lda = lda;
+    a.ldb = ldb;
+    a.ldc = ldc;
+    a.trans_a = trans_a;
+    a.trans_b = trans_b;
+    a.ab_type = ab_type;
+    a.c_type = c_type;
+    a.accumulate = accumulate;
+    hipError_t e = launch_gemm(a, p, stream);
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ISAM_OK;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Exported entry points
+// ---------------------------------------------------------------------------
+extern "C" {
+
+isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type,
+                        const void* A, int64_t lda, const void* B, int64_t ldb, int accumulate,
+                        int c_type, void* C, int64_t ldc, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+    g_last_error.clear();
+    isam_status_t st = validate_gemm(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb, accumulate,
+                                     c_type, C, ldc, "isam_gemm");
+    if (st != ISAM_OK || M == 0 || N == 0) return st;
+    return run_gemm(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb, accumulate, c_type, C, ldc,
+                    nullptr, workspace, workspace_bytes, static_cast<hipStream_t>(stream), "isam_gemm");
+}
+
+size_t isam_gemm_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                                int ab_type, int c_type) {
+    (void)trans_a;
+    (void)trans_b;
+    (void)c_type;
+    if (M <= 0 || N <= 0 || K <= 0 || !valid_dtype(ab_type)) return 0;
+    return gemm_ws_bytes(plan_gemm(M, N, K, ab_type, device_cus()), M, N);
+}
+
+static bool dw_out_dims(int64_t H, int64_t W, int64_t kh, int64_t kw, int64_t stride, int64_t pad,
+                        int64_t* Ho, int64_t* Wo) {
+    if (stride <= 0) return false;
+    *Ho = (H + 2 * pad - kh) / stride + 1;
+    *Wo = (W + 2 * pad - kw) / stride + 1;
+    return H + 2 * pad >= kh && W + 2 * pad >= kw && *Ho > 0 && *Wo > 0;
+}
+
+static size_t dwsep_ws(int64_t batch, int64_t Ho, int64_t Wo, int64_t C_in, int64_t cm,
+                       int64_t C_out, int in_type) {
+    const int64_t M = batch * Ho * Wo, K = C_in * cm;
+    const size_t y = align256((size_t)M * (size_t)K * dsize(in_type));
+    const GemmPlan p = plan_gemm(M, C_out, K, in_type, device_cus());
+    return y + gemm_ws_bytes(p, M, C_out);
+}
+
+size_t isam_dwsep_conv_workspace_size(int64_t batch, int64_t H, int64_t W, int64_t C_in,
+                                      int64_t depth_mult, int64_t kh, int64_t kw, int64_t stride,
+                                      int64_t pad, int64_t C_out, int in_type, int out_type) {
+    (void)out_type;
+    int64_t Ho, Wo;
+    if (batch <= 0 || C_in <= 0 || depth_mult <= 0 || C_out <= 0 || kh <= 0 || kw <= 0 || pad < 0 ||
+        !valid_dtype(in_type) || !dw_out_dims(H, W, kh, kw, stride, pad, &Ho, &Wo))
+        return 0;
+    return dwsep_ws(batch, Ho, Wo, C_in, depth_mult, C_out, in_type);
+}
+
+isam_status_t isam_dwsep_conv(int64_t batch, int64_t H, int64_t W, int64_t C_in, int64_t depth_mult,
+                              int64_t kh, int64_t kw, int64_t stride, int64_t pad, int64_t C_out,
+                              int in_type, const void* x, const void* dw_filter, const void* pw_weight,
+                              int out_type, void* y, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+    g_last_error.clear();
+    const char* who = "isam_dwsep_conv";
+    if (batch < 0 || H <= 0 || W <= 0 || C_in <= 0 || depth_mult <= 0 || kh <= 0 || kw <= 0 ||
+        stride <= 0 || pad < 0 || C_out <= 0)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: sizes must be positive (batch, pad >= 0)", who);
+    if (!valid_dtype(in_type) || !valid_dtype(out_type))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: dtype must be ISAM_F32 (0) or ISAM_BF16 (1)", who);
+    int64_t Ho, Wo;
+    if (!dw_out_dims(H, W, kh, kw, stride, pad, &Ho, &Wo))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: empty output (kernel larger than padded image)", who);
+    if (batch == 0) return ISAM_OK;
+    if (!x || !dw_filter || !pw_weight || !y)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: NULL tensor pointer", who);
+    const size_t es = dsize(in_type);
+    const int64_t Mp = batch * Ho * Wo, Cm = C_in * depth_mult;
+    const int64_t x_el = batch * H * W * C_in, y_el = Mp * C_out, Y_el = Mp * Cm;
+    if ((int64_t)(x_el * es) > kMaxExtent || (int64_t)(Y_el * es) > kMaxExtent ||
+        (int64_t)(y_el * dsize(out_type)) > kMaxExtent)
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: a tensor spans more than 2^31 bytes", who);
+    const size_t yb = (size_t)y_el * dsize(out_type);
+    if (overlaps(y, yb, x, (size_t)x_el * es) ||
+        overlaps(y, yb, dw_filter, (size_t)(kh * kw * Cm) * es) ||
+        overlaps(y, yb, pw_weight, (size_t)(Cm * C_out) * es))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: y overlaps an input", who);
+    const size_t need = dwsep_ws(batch, Ho, Wo, C_in, depth_mult, C_out, in_type);
+    const size_t y_bytes = align256((size_t)Y_el * es);
+    if (!workspace || workspace_bytes < y_bytes)
+        return fail(ISAM_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu required", who, workspace_bytes, need);
+    if (overlaps(workspace, workspace_bytes, y, yb) || overlaps(workspace, workspace_bytes, x, (size_t)x_el * es))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: workspace overlaps a tensor", who);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    DwArgs d{};
+    d.x = x;
+    d.w = dw_filter;
+    d.y = workspace;
+    d.batch = batch;
+    d.H = H;
+    d.W = W;
+    d.C = C_in;
+    d.cm = depth_mult;
+    d.kh = kh;
+    d.kw = kw;
+    d.stride = stride;
+    d.pad = pad;
+    d.Ho = Ho;
+    d.Wo = Wo;
+    d.in_type = in_type;
+    d.y_type = in_type;
+    hipError_t e = launch_depthwise(d, s);
+    if (e != hipSuccess) return hip_fail(e, who);
+    char* gws = static_cast<char*>(workspace) + y_bytes;
+    const size_t gws_bytes = workspace_bytes - y_bytes;
+    return run_gemm(0, 0, Mp, C_out, Cm, in_type, workspace, Cm, pw_weight, C_out, 0, out_type, y, C_out,
+                    nullptr, gws_bytes ? gws : nullptr, gws_bytes, s, who);
+}
+
+size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_size,
+                                       int64_t hidden_size, int w_type) {
+    (void)input_size;
+    if (T < 0 || batch <= 0 || hidden_size <= 0 || !valid_dtype(w_type)) return 0;
+    const size_t gx = align256((size_t)T * (size_t)batch * 3 * (size_t)hidden_size * sizeof(float));
+    const size_t hb = align256(2 * (size_t)batch * (size_t)hidden_size * dsize(w_type));
+    return gx + hb + 256;
+}
+
+}  // extern "C"
+
+extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
+                                          int w_type, const void* x, const float* h0, const void* W,
+                                          const void* U, const float* bias, const float* bias_hn,
+                                          float* h_seq, float* h_T, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+    g_last_error.clear();
+    const char* who = "isam_gru_forward";
+    if (T < 0 || batch < 0 || input_size <= 0 || hidden_size <= 0)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: T, batch >= 0 and input_size, hidden_size > 0 required", who);
+    if (!valid_dtype(w_type)) return fail(ISAM_ERR_INVALID_ARG, "%s: w_type must be 0 or 1", who);
+    if (!h_seq && !h_T) return fail(ISAM_ERR_INVALID_ARG, "%s: h_seq and h_T are both NULL", who);
+    const int64_t H = hidden_size, I = input_size;
+    const int64_t E = w_type == ISAM_BF16 ? 8 : 4;
+    if (H % E) return fail(ISAM_ERR_UNSUPPORTED, "%s: hidden_size must be a multiple of %lld", who, (long long)E);
+    if (batch == 0) return ISAM_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t es = dsize(w_type);
+    const size_t state = (size_t)batch * H * sizeof(float);
+    if (h_seq && h_T && overlaps(h_seq, (size_t)T * state, h_T, state))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: h_seq overlaps h_T", who);
+    if (T == 0) {
+        if (!h_T) return ISAM_OK;
+        if (h0 && overlaps(h0, state, h_T, state)) return fail(ISAM_ERR_INVALID_ARG, "%s: h_T overlaps h0", who);
+        hipError_t e = launch_gru_copy_state(h0, h_T, batch * H, s);
+        return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
+    }
+    if (!x || !W || !U) return fail(ISAM_ERR_INVALID_ARG, "%s: x, W or U is NULL", who);
+    if ((uintptr_t)U & 15) return fail(ISAM_ERR_UNSUPPORTED, "%s: U must be 16-byte aligned", who);
+    const size_t xb = (size_t)T * batch * I * es, wb = (size_t)3 * H * I * es, ub = (size_t)3 * H * H * es;
+    if ((int64_t)xb > kMaxExtent || (int64_t)wb > kMaxExtent || (int64_t)ub > kMaxExtent ||
+        (int64_t)((size_t)T * batch * 3 * H * sizeof(float)) > kMaxExtent)
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: a tensor spans more than 2^31 bytes", who);
+    const void* ins[6] = {x, W, U, h0, bias, bias_hn};
+    const size_t inb[6] = {xb, wb, ub, state, (size_t)3 * H * sizeof(float), (size_t)H * sizeof(float)};
+    for (int i = 0; i < 6; ++i) {
+        if ((h_seq && overlaps(h_seq, (size_t)T * state, ins[i], inb[i])) || (h_T && overlaps(h_T, state, ins[i], inb[i])))
+            return fail(ISAM_ERR_INVALID_ARG, "%s: an output overlaps an input", who);
+    }
+    const size_t need = isam_gru_forward_workspace_size(T, batch, I, H, w_type);
+    if (!workspace || workspace_bytes < need)
+        return fail(ISAM_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu required", who, workspace_bytes, need);
+    if ((h_seq && overlaps(workspace, need, h_seq, (size_t)T * state)) || (h_T && overlaps(workspace, need, h_T, state)))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: workspace overlaps an output", who);
+
+    // Plan: batch groups of up to 16 columns (one 16-wide MFMA tile); hidden
+    // units per workgroup J the smallest power of two that lets every
+    // workgroup stay resident, at most 16 (three gates x 16 = 48 rows).
+    const int BB = (int)std::min<int64_t>(batch, 16);
+    const int64_t n_bg = cdiv(batch, BB);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, who);
+    int cus = device_cus();
+    int lds_max = 0;
+    e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e != hipSuccess) return hip_fail(e, who);
+    int J = 0;
+    for (int cand = 1; cand <= 16; cand *= 2) {
+        if (H % cand) continue;
+        if (cand * BB > 256) break;
+        if (gru_lds_bytes(w_type, H, cand) > (size_t)lds_max) break;
+        if ((H / cand) * n_bg <= cus) { J = cand; break; }
+    }
+    if (!J) return fail(ISAM_ERR_UNSUPPORTED, "%s: no resident tiling for hidden=%lld batch=%lld on %d CUs",
+                        who, (long long)H, (long long)batch, cus);
+    const int n_wg = (int)((H / J) * n_bg);
+    if (log_enabled())
+        fprintf(stderr, "[isam] gru T=%lld B=%lld I=%lld H=%lld w=%d J=%d BB=%d wgs=%d lds=%zu\n", (long long)T,
+                (long long)batch, (long long)I, (long long)H, w_type, J, BB, n_wg, gru_lds_bytes(w_type, H, J));
+
+    char* ws = static_cast<char*>(workspace);
+    float* gx = reinterpret_cast<float*>(ws);
+    const size_t gx_b = align256((size_t)T * batch * 3 * H * sizeof(float));
+    void* hbuf = ws + gx_b;
+    const size_t hb_b = align256(2 * (size_t)batch * H * es);
+    unsigned* sync = reinterpret_cast<unsigned*>(ws + gx_b + hb_b);
+
+    // Input projection for all steps: Gx[T*batch][3H] = x[T*batch][I] . W^T.
+    isam_status_t st = run_gemm(0, 1, T * batch, 3 * H, I, w_type, x, I, W, I, 0, ISAM_F32, gx, 3 * H,
+                                nullptr, nullptr, 0, s, who);
+    if (st != ISAM_OK) return st;
+    GruArgs g{};
+    g.T = T;
+    g.batch = batch;
+    g.I = I;
+    g.H = H;
+    g.w_type = w_type;
+    g.gx = gx;
+    g.h0 = h0;
+    g.U = U;
+    g.bias = bias;
+    g.bias_hn = bias_hn;
+    g.h_seq = h_seq;
+    g.h_T = h_T;
+    g.hbuf = hbuf;
+    g.sync = sync;
+    g.units_per_wg = J;
+    g.batch_per_wg = BB;
+    g.n_wg = n_wg;
+    e = launch_gru_recurrent(g, s);
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ISAM_OK;
+}
+
+extern "C" {
+
+const char* isam_status_string(int status) {
+    switch (status) {
+        case ISAM_OK: return "ISAM_OK";
+        case ISAM_ERR_INVALID_ARG: return "ISAM_ERR_INVALID_ARG: invalid argument";
+        case ISAM_ERR_UNSUPPORTED: return "ISAM_ERR_UNSUPPORTED: unsupported configuration";
+        case ISAM_ERR_WORKSPACE: return "ISAM_ERR_WORKSPACE: workspace missing or too small";
+        case ISAM_ERR_HIP: return "ISAM_ERR_HIP: HIP runtime error";
+        default: return "unknown isam status";
+    }
+}
+
+const char* isam_last_error(void) { return g_last_error.c_str(); }
+
+int isam_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,291 @@
+// MFMA tile kernel for C (+)= op(A) op(B): the dense contraction of the
+// paper's first listing (Section 2), unrolled into compute tiles (Section 3.3),
+// allocated to compute units (Section 3.4) and fed HBM -> LDS -> VGPR
+// (Section 3.5).
+//
+// Design (gfx950):
+//   * A workgroup owns a BM x BN output tile; 4 waves split it 2x2 (or 4x1).
+//   * Both operands are staged in LDS as rows of 128 bytes of K (64 bf16 or
+//     32 fp32), i.e. "K-major" whatever the global layout.  An operand whose
+//     global layout is K-contiguous is copied chunk by chunk; one whose
+//     layout is M/N-contiguous is loaded as E x E blocks and transposed in
+//     registers on the way into LDS.
+//   * 16-byte chunk c of LDS row r sits at chunk c ^ ((r >> 1) & 7) so the
+//     MFMA fragment reads (32 rows x 16 bytes per half wave) spread over all
+//     banks.
+//   * Two LDS stages: the global loads for tile t+1 are issued before the
+//     MFMAs of tile t and written to the other stage after them; one
+//     barrier per K tile.
+//   * Global loads go through buffer resources: a row or K index past the
+//     matrix edge is turned into an out-of-range offset and reads as zero,
+//     so ragged tiles need no branches.
+//   * Rasterisation: tiles are visited in groups of `group_m` tile rows, and
+//     with `xcd_remap` the round-robin dispatch over the 8 XCDs is undone so
+//     that each XCD works on a contiguous run of tiles that share A and B
+//     panels in its L2.
+//   * Split-K (blockIdx.y) writes fp32 partials; a separate kernel reduces
+//     them in split order, so results are deterministic.
+#pragma once
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace isam {
+
+__device__ __forceinline__ uint32_t lds_off(int r, int c) {
+    return (uint32_t)(r * 128 + ((c ^ ((r >> 1) & 7)) << 4));
+}
+
+// Loads one operand tile (ROWS rows of M or N, 128 bytes of K) into
+// registers, then stores it K-major into LDS.
+template <typename T, int ROWS, int NT, bool KC, bool VEC>
+struct TileLoader {
+    static constexpr int E = 16 / (int)sizeof(T);   // elements per 16-byte chunk
+    static constexpr int BK = 128 / (int)sizeof(T); // K depth of a tile
+    static constexpr int UNITS = KC ? ROWS * 8 : (BK / E) * (ROWS / E);
+    static constexpr int NU = (UNITS + NT - 1) / NT;
+    static constexpr int NREG = KC ? NU : NU * E;
+    uint4 r[NREG];
+
+    __device__ __forceinline__ static bool live(int q) { return (UNITS % NT == 0) || q < UNITS; }
+
+    __device__ __forceinline__ static uint4 load_elems(__amdgpu_buffer_rsrc_t rs, int64_t base_el,
+                                                       int64_t step_el, int nvalid) {
+        // E elements at base, base+step, ...; elements >= nvalid read as zero.
+        uint32_t w[4];
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                uint32_t lo = buf_load2(rs, (2 * p < nvalid) ? (uint32_t)((base_el + (2 * p) * step_el) * 2) : kOob);
+                uint32_t hi = buf_load2(rs, (2 * p + 1 < nvalid) ? (uint32_t)((base_el + (2 * p + 1) * step_el) * 2) : kOob);
+                w[p] = (lo & 0xffffu) | (hi << 16);
+            }
+        } else {
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+                w[p] = buf_load4(rs, (p < nvalid) ? (uint32_t)((base_el + p * step_el) * 4) : kOob);
+        }
+        return make_uint4(w[0], w[1], w[2], w[3]);
+    }
+
+    // r0: first row (M or N index) of the tile; k0: first K index;
+    // rows_total / kend: valid extents; ld: leading dimension in elements.
+    __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, int tid, int64_t r0, int64_t k0,
+                                         int64_t rows_total, int64_t kend, int64_t ld) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int q = tid + u * NT;
+            const bool lv = live(q);
+            if constexpr (KC) {
+                const int rr = q >> 3, c = q & 7;
+                const int64_t row = r0 + rr, k = k0 + c * E;
+                const bool ok = lv && row < rows_total && k < kend;
+                if constexpr (VEC) {
+                    r[u] = buf_load16(rs, ok ? (uint32_t)((row * ld + k) * (int64_t)sizeof(T)) : kOob);
+                } else {
+                    int nv = ok ? (int)((kend - k) < E ? (kend - k) : E) : 0;
+                    r[u] = load_elems(rs, row * ld + k, 1, nv);
+                }
+            } else {
+                constexpr int RB = ROWS / E;
+                const int rb = q % RB, kb = q / RB;
+                const int64_t col = r0 + rb * E;
+#pragma unroll
+                for (int i = 0; i < E; ++i) {
+                    const int64_t k = k0 + kb * E + i;
+                    const bool ok = lv && k < kend && col < rows_total;
+                    if constexpr (VEC) {
+                        r[u * E + i] = buf_load16(rs, ok ? (uint32_t)((k * ld + col) * (int64_t)sizeof(T)) : kOob);
+                    } else {
+                        int nv = ok ? (int)((rows_total - col) < E ? (rows_total - col) : E) : 0;
+                        r[u * E + i] = load_elems(rs, k * ld + col, 1, nv);
+                    }
+                }
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(char* lds, int tid) const {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int q = tid + u * NT;
+            if (!live(q)) continue;
+            if constexpr (KC) {
+                *reinterpret_cast<uint4*>(lds + lds_off(q >> 3, q & 7)) = r[u];
+            } else {
+                constexpr int RB = ROWS / E;
+                const int rb = q % RB, kb = q / RB;
+                uint4 t[E];
+                if constexpr (E == 8) transpose8x8_b16(&r[u * E], t);
+                else transpose4x4_b32(&r[u * E], t);
+#pragma unroll
+                for (int j = 0; j < E; ++j)
+                    *reinterpret_cast<uint4*>(lds + lds_off(rb * E + j, kb)) = t[j];
+            }
+        }
+    }
+};
+
+struct TileMapArgs {
+    int tiles_m, tiles_n, group_m, xcd_remap;
+    int64_t k_per_split;
+};
+
+__device__ __forceinline__ void map_tile(const TileMapArgs& t, int& tm, int& tn) {
+    int bid = blockIdx.x;
+    const int G = gridDim.x;
+    if (t.xcd_remap && (G & 7) == 0) bid = (bid & 7) * (G >> 3) + (bid >> 3);
+    const int width = t.group_m * t.tiles_n;
+    const int group = bid / width;
+    const int first_m = group * t.group_m;
+    const int gm = min(t.tiles_m - first_m, t.group_m);
+    const int inner = bid - group * width;
+    tm = first_m + inner % gm;
+    tn = inner / gm;
+}
+
+template <typename T, int BM, int BN, int WM, int WN, bool TA, bool TB, bool VEC>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, TileMapArgs tmap) {
+    constexpr int NT = 64 * WM * WN;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int MI = WTM / 32, NI = WTN / 32;
+    constexpr int BK = 128 / (int)sizeof(T);
+    constexpr int STAGE = (BM + BN) * 128;
+    static_assert(MI >= 1 && NI >= 1, "wave tile must be a multiple of 32x32");
+    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wm = wid / WN, wn = wid % WN;
+    int tm, tn;
+    map_tile(tmap, tm, tn);
+    const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+    const int split = blockIdx.y;
+    const int64_t kbeg = (int64_t)split * tmap.k_per_split;
+    const int64_t kend = min(a.K, kbeg + tmap.k_per_split);
+    const int nk = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
+
+    const int64_t a_ext = TA ? ((a.K - 1) * a.lda + a.M) : ((a.M - 1) * a.lda + a.K);
+    const int64_t b_ext = TB ? ((a.N - 1) * a.ldb + a.K) : ((a.K - 1) * a.ldb + a.N);
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(a_ext * (int64_t)sizeof(T)));
+    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(a.B, (uint32_t)(b_ext * (int64_t)sizeof(T)));
+
+    TileLoader<T, BM, NT, !TA, VEC> la;
+    TileLoader<T, BN, NT, TB, VEC> lb;
+
+    f32x16_t acc[MI][NI];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    if (nk > 0) {
+        la.load(rsA, tid, m0, kbeg, a.M, kend, a.lda);
+        lb.load(rsB, tid, n0, kbeg, a.N, kend, a.ldb);
+        la.store(smem, tid);
+        lb.store(smem + BM * 128, tid);
+        __syncthreads();
+        for (int t = 0; t < nk; ++t) {
+            char* cur = smem + (t & 1) * STAGE;
+            char* nxt = smem + ((t + 1) & 1) * STAGE;
+            const bool more = t + 1 < nk;
+            if (more) {
+                la.load(rsA, tid, m0, kbeg + (int64_t)(t + 1) * BK, a.M, kend, a.lda);
+                lb.load(rsB, tid, n0, kbeg + (int64_t)(t + 1) * BK, a.N, kend, a.ldb);
+            }
+            const char* As = cur;
+            const char* Bs = cur + BM * 128;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                uint4 af[MI], bfr[NI];
+                const int ch = ks * 2 + (lane >> 5);
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+                    af[i] = *reinterpret_cast<const uint4*>(As + lds_off(wm * WTM + i * 32 + (lane & 31), ch));
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+                    bfr[j] = *reinterpret_cast<const uint4*>(Bs + lds_off(wn * WTN + j * 32 + (lane & 31), ch));
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j) {
+                        if constexpr (sizeof(T) == 2) mfma32_bf16(acc[i][j], af[i], bfr[j]);
+                        else mfma32_f32x4(acc[i][j], af[i], bfr[j]);
+                    }
+            }
+            if (more) {
+                la.store(nxt, tid);
+                lb.store(nxt + BM * 128, tid);
+            }
+            __syncthreads();
+        }
+    }
+
+    // Epilogue.  Accumulator element v of lane l: row 8*(v/4) + 4*(l/32) + v%4, column l%32.
+    const bool split_out = gridDim.y > 1;
+    float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+            const int64_t col = n0 + wn * WTN + j * 32 + (lane & 31);
+            if (col >= a.N) continue;
+            const float bv = (!split_out && a.bias) ? a.bias[col] : 0.0f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t row = m0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                if (row >= a.M) continue;
+                float val = acc[i][j][v];
+                if (split_out) {
+                    P[row * a.N + col] = val;
+                } else {
+                    val += bv;
+                    const int64_t idx = row * a.ldc + col;
+                    if (a.c_type == kF32) {
+                        float* C = static_cast<float*>(a.C);
+                        if (a.accumulate) val += C[idx];
+                        C[idx] = val;
+                    } else {
+                        uint16_t* C = static_cast<uint16_t*>(a.C);
+                        if (a.accumulate) val += bf16_to_f32(C[idx]);
+                        C[idx] = (uint16_t)f32_to_bf16(val);
+                    }
+                }
+            }
+        }
+}
+
+// Function table for one element type: [tile][trans_a][trans_b][vec].
+typedef void (*GemmKernelFn)(GemmArgs, TileMapArgs);
+
+template <typename T, int BM, int BN, int WM, int WN>
+struct TileKernels {
+    static GemmKernelFn get(int ta, int tb, int vec) {
+        static const GemmKernelFn tbl[2][2][2] = {
+            {{gemm_tile_kernel<T, BM, BN, WM, WN, false, false, false>,
+              gemm_tile_kernel<T, BM, BN, WM, WN, false, false, true>},
+             {gemm_tile_kernel<T, BM, BN, WM, WN, false, true, false>,
+              gemm_tile_kernel<T, BM, BN, WM, WN, false, true, true>}},
+            {{gemm_tile_kernel<T, BM, BN, WM, WN, true, false, false>,
+              gemm_tile_kernel<T, BM, BN, WM, WN, true, false, true>},
+             {gemm_tile_kernel<T, BM, BN, WM, WN, true, true, false>,
+              gemm_tile_kernel<T, BM, BN, WM, WN, true, true, true>}}};
+        return tbl[ta][tb][vec];
+    }
+};
+
+template <typename T>
+GemmKernelFn gemm_kernel_for(int tile, int ta, int tb, int vec) {
+    switch (tile) {
+        case kTile256x256: return TileKernels<T, 256, 256, 2, 2>::get(ta, tb, vec);
+        case kTile256x128: return TileKernels<T, 256, 128, 2, 2>::get(ta, tb, vec);
+        case kTile128x128: return TileKernels<T, 128, 128, 2, 2>::get(ta, tb, vec);
+        case kTile128x64: return TileKernels<T, 128, 64, 2, 2>::get(ta, tb, vec);
+        case kTile64x64: return TileKernels<T, 64, 64, 2, 2>::get(ta, tb, vec);
+        case kTile128x32: return TileKernels<T, 128, 32, 4, 1>::get(ta, tb, vec);
+        default: return nullptr;
+    }
+}
+
+}  // namespace isam

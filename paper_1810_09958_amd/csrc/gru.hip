@@ -1,0 +1,217 @@
+// GRU recurrence as one persistent kernel.
+//
+// The paper schedules a recurrent loop body three times -- a priming
+// iteration that leaves buffers next to the compute units, a recursive
+// iteration run as often as needed with weights persistent, and a finish
+// iteration that puts the results where the next consumer wants them
+// (Section 3.6) -- and credits its GRU results to fusing the cell's
+// element-wise work with the matrix products and keeping reused data on-chip
+// (Section 6.2.2).  On gfx950 that becomes:
+//   priming   : every workgroup copies its slice of U (the rows of all three
+//               gates for its hidden units) into LDS once;
+//   recursive : per step, a 16x16 MFMA contraction of that U slice with the
+//               bf16 (or fp32) copy of h_{t-1}, split over 4 waves along K
+//               and reduced through LDS, then the r/z/n gate math fused in
+//               the epilogue, then a grid-wide barrier;
+//   finish    : h_T written to its output.
+// The input projection x_t W^T for all t is one GEMM launched before this
+// kernel (it does not depend on h).
+//
+// Cell (gate rows of W and U stacked r, z, n):
+//   r = sigmoid(Gx_r + b_r + (U_r h)),  z = sigmoid(Gx_z + b_z + (U_z h)),
+//   n = tanh(Gx_n + b_n + r * ((U_n h) + b_hn)),  h' = (1 - z) n + z h.
+// The U_n h product is complete before it is scaled by r.
+//
+// All workgroups must be co-resident (cooperative launch); every barrier
+// wait is bounded and raises an error flag instead of spinning forever.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace isam {
+namespace {
+
+constexpr int kWaves = 4;
+// Upper bound on one barrier wait, in ticks of the 100 MHz constant clock.
+constexpr uint64_t kBarrierTimeoutTicks = 200000000ull;  // 2 s
+
+__device__ __forceinline__ int gru_rows(int J) { return ((3 * J + 15) / 16) * 16; }
+
+__device__ __forceinline__ void grid_barrier(unsigned* ctr, unsigned target, unsigned* err) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        atomicAdd(ctr, 1u);
+        const uint64_t start = wall_clock64();
+        // A timed-out wait sets the sticky error flag; every later wait sees
+        // it and returns at once, so the grid always drains.
+        while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target &&
+               __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+            __builtin_amdgcn_s_sleep(1);
+            if (wall_clock64() - start > kBarrierTimeoutTicks) {
+                atomicOr(err, 1u);
+                break;
+            }
+        }
+        __threadfence();
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ float sigmoidf(float v) { return 1.0f / (1.0f + expf(-v)); }
+
+template <typename T>
+__global__ void gru_init_kernel(GruArgs a) {
+    const int64_t n = a.batch * a.H;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const float v = a.h0 ? a.h0[i] : 0.0f;
+        if constexpr (sizeof(T) == 2) static_cast<uint16_t*>(a.hbuf)[i] = (uint16_t)f32_to_bf16(v);
+        else static_cast<float*>(a.hbuf)[i] = v;
+    }
+    if (blockIdx.x == 0 && threadIdx.x < 32) a.sync[threadIdx.x] = 0u;
+}
+
+template <typename T>
+__global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr int E = 16 / (int)sizeof(T);
+    const int J = a.units_per_wg, BB = a.batch_per_wg;
+    const int64_t H = a.H, B = a.batch;
+    const int RT = gru_rows(J), MT = RT / 16;
+    const int row_bytes = (int)(H * (int64_t)sizeof(T)) + 16;
+    const int n_ug = (int)(H / J);
+    const int ug = blockIdx.x % n_ug, bg = blockIdx.x / n_ug;
+    const int64_t j0 = (int64_t)ug * J, b0 = (int64_t)bg * BB;
+    const int nb = (int)min((int64_t)BB, B - b0);
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+
+    char* u_lds = smem;
+    float* red = reinterpret_cast<float*>(smem + RT * row_bytes);  // [kWaves][RT][16]
+
+    // Priming: U rows (g*H + j0 + jj) for local row g*J + jj; padding rows are zero.
+    {
+        const int chunks_per_row = (int)(H / E);
+        const T* U = static_cast<const T*>(a.U);
+        for (int q = tid; q < RT * chunks_per_row; q += 64 * kWaves) {
+            const int lr = q / chunks_per_row, c = q - lr * chunks_per_row;
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (lr < 3 * J) {
+                const int g = lr / J, jj = lr - g * J;
+                v = *reinterpret_cast<const uint4*>(U + (g * H + j0 + jj) * H + (int64_t)c * E);
+            }
+            *reinterpret_cast<uint4*>(u_lds + lr * row_bytes + c * 16) = v;
+        }
+    }
+
+    // Owned outputs: thread p < J * nb handles (jj, n) = (p % J, p / J).
+    const int p = tid;
+    const bool owner = p < J * nb;
+    const int jj = owner ? p % J : 0, nn = owner ? p / J : 0;
+    const int64_t j = j0 + jj, bb = b0 + nn;
+    float h_prev = 0.0f;
+    float bias_r = 0.f, bias_z = 0.f, bias_n = 0.f, bias_hn = 0.f;
+    if (owner) {
+        if (a.h0) h_prev = a.h0[bb * H + j];
+        if (a.bias) { bias_r = a.bias[j]; bias_z = a.bias[H + j]; bias_n = a.bias[2 * H + j]; }
+        if (a.bias_hn) bias_hn = a.bias_hn[j];
+    }
+    __syncthreads();
+
+    const int KG = (int)((H * (int64_t)sizeof(T) + 63) / 64);  // 64-byte K groups
+    const int n_col = lane & 15, quarter = lane >> 4;
+    const bool col_ok = n_col < nb;
+    const int64_t hb_row = b0 + n_col;
+
+    for (int64_t t = 0; t < a.T; ++t) {
+        const T* hcur = static_cast<const T*>(a.hbuf) + (t & 1) * B * H;
+        f32x4_t acc[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) acc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int kg = wid; kg < KG; kg += kWaves) {
+            const int chunk = kg * 4 + quarter;
+            const int64_t k = (int64_t)chunk * E;
+            uint4 hv = make_uint4(0, 0, 0, 0);
+            if (col_ok && k < H) hv = *reinterpret_cast<const uint4*>(hcur + hb_row * H + k);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                if (m >= MT) break;
+                uint4 uv = make_uint4(0, 0, 0, 0);
+                if (k < H) uv = *reinterpret_cast<const uint4*>(u_lds + (m * 16 + n_col) * row_bytes + chunk * 16);
+                if constexpr (sizeof(T) == 2) mfma16_bf16(acc[m], uv, hv);
+                else mfma16_f32x4(acc[m], uv, hv);
+            }
+        }
+        // acc[m] element v of lane l: local row m*16 + 4*(l/16) + v, batch column l%16
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            if (m >= MT) break;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                red[(wid * RT + m * 16 + 4 * quarter + v) * 16 + n_col] = acc[m][v];
+        }
+        __syncthreads();
+        if (owner) {
+            float gh[3];
+#pragma unroll
+            for (int g = 0; g < 3; ++g) {
+                float s = 0.0f;
+#pragma unroll
+                for (int w = 0; w < kWaves; ++w) s += red[(w * RT + g * J + jj) * 16 + nn];
+                gh[g] = s;
+            }
+            const float* gx = a.gx + (t * B + bb) * 3 * H;
+            const float r = sigmoidf(gx[j] + bias_r + gh[0]);
+            const float z = sigmoidf(gx[H + j] + bias_z + gh[1]);
+            const float n = tanhf(gx[2 * H + j] + bias_n + r * (gh[2] + bias_hn));
+            const float h = (1.0f - z) * n + z * h_prev;
+            h_prev = h;
+            if (a.h_seq) a.h_seq[(t * B + bb) * H + j] = h;
+            T* hnext = static_cast<T*>(a.hbuf) + ((t + 1) & 1) * B * H;
+            if constexpr (sizeof(T) == 2) reinterpret_cast<uint16_t*>(hnext)[bb * H + j] = (uint16_t)f32_to_bf16(h);
+            else hnext[bb * H + j] = h;
+        }
+        if (t + 1 < a.T) grid_barrier(a.sync, (unsigned)((t + 1) * gridDim.x), a.sync + 16);
+    }
+    if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
+}
+
+__global__ void copy_state_kernel(const float* h0, float* hT, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        hT[i] = h0 ? h0[i] : 0.0f;
+}
+
+}  // namespace
+
+hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStream_t s) {
+    int blocks = (int)((n + 255) / 256);
+    if (blocks > 1024) blocks = 1024;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(copy_state_kernel, dim3(blocks), dim3(256), 0, s, h0, h_T, n);
+    return hipGetLastError();
+}
+
+size_t gru_lds_bytes(int w_type, int64_t H, int J) {
+    const int RT = ((3 * J + 15) / 16) * 16;
+    const size_t es = w_type == kBF16 ? 2 : 4;
+    return (size_t)RT * (size_t)(H * es + 16) + (size_t)kWaves * RT * 16 * sizeof(float);
+}
+
+hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s) {
+    const size_t lds = gru_lds_bytes(a.w_type, a.H, a.units_per_wg);
+    void* fn = a.w_type == kBF16 ? reinterpret_cast<void*>(gru_recurrent_kernel<bf16_t>)
+                                 : reinterpret_cast<void*>(gru_recurrent_kernel<float>);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    int64_t n = a.batch * a.H;
+    int blocks = (int)((n + 255) / 256);
+    if (blocks > 1024) blocks = 1024;
+    if (a.w_type == kBF16) hipLaunchKernelGGL(gru_init_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(gru_init_kernel<float>, dim3(blocks), dim3(256), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    GruArgs args = a;
+    void* params[] = {&args};
+    return hipLaunchCooperativeKernel(fn, dim3(a.n_wg), dim3(64 * kWaves), params, (unsigned)lds, s);
+}
+
+}  // namespace isam

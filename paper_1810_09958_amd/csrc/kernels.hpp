@@ -1,0 +1,83 @@
+// Internal launch interface between the C-ABI layer (api.cpp) and the HIP
+// kernels.  Nothing here is exported.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace isam {
+
+enum Dtype : int { kF32 = 0, kBF16 = 1 };
+
+// One GEMM launch: C[M][N] (+)= op(A)[M][K] . op(B)[K][N].
+struct GemmArgs {
+    const void* A;
+    const void* B;
+    void* C;
+    float* partial;        // split-K partial sums [k_splits][M][N] fp32 (k_splits > 1)
+    const float* bias;     // optional per-column bias added in the epilogue (fp32, length N)
+    int64_t M, N, K;
+    int64_t lda, ldb, ldc;
+    int trans_a, trans_b;
+    int ab_type;           // kF32 / kBF16
+    int c_type;            // kF32 / kBF16
+    int accumulate;        // C += instead of C =
+};
+
+// Tile configurations of the MFMA tile kernel (see gemm.hip).
+enum TileCfg : int {
+    kTile256x256 = 0,  // 4 waves, 128x128 per wave
+    kTile256x128 = 1,  // 4 waves, 128x64 per wave
+    kTile128x128 = 2,  // 4 waves, 64x64 per wave
+    kTile128x64 = 3,   // 4 waves, 64x32 per wave
+    kTile64x64 = 4,    // 4 waves, 32x32 per wave
+    kTile128x32 = 5,   // 4 waves, 32x32 per wave (tall-skinny)
+    kTileCount
+};
+
+struct GemmPlan {
+    int tile;        // TileCfg
+    int vec;         // 1: 16-byte vector loads (needs alignment); 0: element loads
+    int k_splits;    // >= 1
+    int64_t k_per_split;  // multiple of the tile K depth
+    int group_m;     // tile-row group size of the rasterisation
+    int xcd_remap;   // spread consecutive tiles of one group over one XCD
+};
+
+void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk);
+hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
+
+// Depthwise kh x kw convolution, NHWC.  Y is [batch][Ho][Wo][C*cm] in y_type.
+struct DwArgs {
+    const void* x;
+    const void* w;  // [kh][kw][C][cm]
+    void* y;
+    int64_t batch, H, W, C, cm, kh, kw, stride, pad, Ho, Wo;
+    int in_type, y_type;
+};
+hipError_t launch_depthwise(const DwArgs& a, hipStream_t s);
+
+// GRU recurrence (the input projection is a GemmArgs launch done before).
+struct GruArgs {
+    int64_t T, batch, I, H;
+    int w_type;
+    const float* gx;        // [T*batch][3H] fp32: x W^T (no bias)
+    const float* h0;        // [batch][H] fp32 or null
+    const void* U;          // [3H][H]
+    const float* bias;      // [3H] or null
+    const float* bias_hn;   // [H] or null
+    float* h_seq;           // [T][batch][H] or null
+    float* h_T;             // [batch][H] or null
+    void* hbuf;             // 2 x [batch][H] in w_type: MFMA copy of h_{t-1}
+    unsigned* sync;         // barrier counter + error flag (2 x 64 bytes)
+    int units_per_wg;       // J
+    int batch_per_wg;       // BB
+    int n_wg;
+};
+size_t gru_lds_bytes(int w_type, int64_t H, int J);
+hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s);
+// T == 0: h_T = h0 (or zeros when h0 is null).
+hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStream_t s);
+
+}  // namespace isam

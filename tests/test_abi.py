@@ -1,0 +1,139 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function the header
+declares, and rejects bad arguments during host-side validation (before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1810_09958_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "isam.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE, HIPERR = 0, 1, 2, 3, 4
+F32, BF16 = 0, 1
+FAKE = ctypes.c_void_p(0x10000)      # never dereferenced: validation fails before any launch
+FAKE2 = ctypes.c_void_p(0x20000000)
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(isam_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return _lib.lib()
+
+
+def test_header_declares_expected_entry_points():
+    names = header_functions()
+    for n in ("isam_gemm", "isam_dwsep_conv", "isam_gru_forward", "isam_gemm_workspace_size",
+              "isam_dwsep_conv_workspace_size", "isam_gru_forward_workspace_size",
+              "isam_status_string", "isam_last_error", "isam_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    for n in header_functions():
+        assert hasattr(L, n), f"libisam.so does not export {n}"
+    assert set(header_functions()) == set(_lib.SIGNATURES)
+
+
+def test_binding_has_no_compute_fallback():
+    import paper_1810_09958_amd as P
+    src = open(P.__file__).read() + open(_lib.__file__).read()
+    assert "import oracle" not in src and "from oracle" not in src
+    for op in ("torch.matmul", "torch.mm(", "conv2d", "torch.nn.GRU", ".numpy()"):
+        assert op not in src
+
+
+def test_version_and_status_strings(L):
+    assert L.isam_version() >= 100
+    for s in range(5):
+        assert L.isam_status_string(s).startswith(b"ISAM_")
+    assert b"unknown" in L.isam_status_string(99)
+
+
+def gemm(L, ta=0, tb=0, M=4, N=4, K=4, ab=F32, A=FAKE, lda=4, B=FAKE2, ldb=4, acc=0, ct=F32,
+         C=ctypes.c_void_p(0x40000000), ldc=4, ws=None, wsb=0):
+    return L.isam_gemm(ta, tb, M, N, K, ab, A, lda, B, ldb, acc, ct, C, ldc, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(M=-1), INVALID), (dict(N=-2), INVALID), (dict(K=-3), INVALID),
+    (dict(ta=2), INVALID), (dict(tb=-1), INVALID), (dict(acc=3), INVALID),
+    (dict(ab=7), INVALID), (dict(ct=5), INVALID),
+    (dict(C=None), INVALID), (dict(ldc=3), INVALID),
+    (dict(A=None), INVALID), (dict(B=None), INVALID),
+    (dict(lda=3), INVALID), (dict(ldb=3), INVALID),
+    (dict(ta=1, M=8, lda=4), INVALID), (dict(tb=1, K=8, lda=8, ldb=4), INVALID),
+    (dict(M=1 << 20, K=1 << 12, lda=1 << 12, ldc=4), UNSUPPORTED),
+    (dict(C=FAKE), INVALID),          # C overlaps A
+])
+def test_gemm_validation(L, kw, code):
+    assert gemm(L, **kw) == code
+    assert L.isam_last_error() != b""
+
+
+def test_gemm_empty_is_noop(L):
+    assert gemm(L, M=0, A=None, B=None, C=None) == OK
+    assert gemm(L, N=0, A=None, B=None, C=None) == OK
+
+
+def test_gemm_workspace_queries(L):
+    # A deep-K, skinny-N product is split along K and needs partial-sum space.
+    ws = L.isam_gemm_workspace_size(0, 0, 4096, 32, 4096, BF16, F32)
+    assert ws > 0 and ws % (4096 * 32 * 4) == 0
+    assert L.isam_gemm_workspace_size(0, 0, 8192, 8192, 8192, BF16, BF16) == 0
+    assert L.isam_gemm_workspace_size(0, 0, 0, 8, 8, BF16, BF16) == 0
+
+
+def dw(L, batch=1, H=8, W=8, C=4, cm=1, kh=3, kw=3, s=1, p=1, Co=4, it=F32, x=FAKE,
+       dwf=ctypes.c_void_p(0x30000), pw=ctypes.c_void_p(0x50000), ot=F32,
+       y=ctypes.c_void_p(0x70000000), ws=ctypes.c_void_p(0x90000000), wsb=1 << 30):
+    return L.isam_dwsep_conv(batch, H, W, C, cm, kh, kw, s, p, Co, it, x, dwf, pw, ot, y, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(batch=-1), INVALID), (dict(H=0), INVALID), (dict(C=0), INVALID), (dict(cm=0), INVALID),
+    (dict(kh=0), INVALID), (dict(s=0), INVALID), (dict(p=-1), INVALID), (dict(Co=0), INVALID),
+    (dict(it=3), INVALID), (dict(ot=9), INVALID), (dict(H=2, p=0), INVALID),
+    (dict(x=None), INVALID), (dict(y=None), INVALID), (dict(pw=None), INVALID),
+    (dict(ws=None), WORKSPACE), (dict(wsb=16), WORKSPACE),
+    (dict(y=FAKE), INVALID),
+])
+def test_dwsep_validation(L, kw, code):
+    assert dw(L, **kw) == code
+
+
+def test_dwsep_workspace_query(L):
+    n = L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, BF16, F32)
+    assert n >= 32 * 56 * 56 * 128 * 2
+    assert L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 0, 1, 256, BF16, F32) == 0
+    assert dw(L, batch=0, x=None, y=None) == OK
+
+
+def gru(L, T=4, B=2, I=8, H=8, wt=F32, x=FAKE, h0=None, W=ctypes.c_void_p(0x30000),
+        U=ctypes.c_void_p(0x50000), bias=None, bhn=None, hseq=ctypes.c_void_p(0x70000000),
+        hT=None, ws=ctypes.c_void_p(0x90000000), wsb=1 << 30):
+    return L.isam_gru_forward(T, B, I, H, wt, x, h0, W, U, bias, bhn, hseq, hT, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=-1), INVALID), (dict(B=-1), INVALID), (dict(I=0), INVALID), (dict(H=0), INVALID),
+    (dict(wt=2), INVALID), (dict(hseq=None), INVALID), (dict(x=None), INVALID),
+    (dict(U=None), INVALID), (dict(H=6), UNSUPPORTED), (dict(H=12, wt=BF16), UNSUPPORTED),
+    (dict(ws=None), WORKSPACE), (dict(wsb=64), WORKSPACE),
+    (dict(hseq=FAKE), INVALID),
+])
+def test_gru_validation(L, kw, code):
+    assert gru(L, **kw) == code
+
+
+def test_gru_workspace_query(L):
+    n = L.isam_gru_forward_workspace_size(64, 32, 1024, 1024, BF16)
+    assert n >= 64 * 32 * 3 * 1024 * 4 + 2 * 32 * 1024 * 2
+    assert gru(L, B=0) == OK

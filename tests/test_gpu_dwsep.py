@@ -1,0 +1,69 @@
+"""GPU parity of isam_dwsep_conv against the CPU oracle (the paper's third listing,
+factored into depthwise then pointwise as in Section 2.3)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth import workloads
+from tests._util import TOL_BF16, TOL_F32, bits, norm_err, to_gpu, to_host_f64
+
+pytestmark = pytest.mark.gpu
+
+import paper_1810_09958_amd as isam
+
+
+def _case(b, H, W, C, Co, cm=1, k=3, stride=1, pad=1, dt="f32", ot="f32", seed=0):
+    X = synth.normal(seed, 0, (b, H, W, C))
+    D = synth.uniform(seed, 1, (k, k, C, cm), -1 / 3, 1 / 3)
+    P = synth.uniform(seed, 2, (C * cm, Co), -1 / 11, 1 / 11)
+    if dt == "bf16":
+        X, D, P = bits(X), bits(D), bits(P)
+    y = isam.dwsep_conv(to_gpu(X), to_gpu(D), to_gpu(P), stride=stride, pad=pad,
+                        out_dtype=torch.bfloat16 if ot == "bf16" else torch.float32)
+    torch.cuda.synchronize()
+    Z, S = oracle.dwsep(X, D, P, stride=stride, pad=pad)
+    err = norm_err(to_host_f64(y), Z, S)
+    tol = TOL_F32 if (dt == "f32" and ot == "f32") else TOL_BF16
+    assert err <= tol, f"b={b} H={H} W={W} C={C} Co={Co} cm={cm} k={k} s={stride} p={pad} {dt}->{ot}: {err:.3e}"
+
+
+@pytest.mark.parametrize("dt,ot", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16")])
+def test_small_fast_path(dt, ot):
+    _case(2, 9, 11, 16, 24, dt=dt, ot=ot)
+    _case(3, 17, 5, 64, 40, dt=dt, ot=ot, seed=1)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("cm,k,stride,pad", [(1, 3, 2, 1), (2, 3, 1, 1), (2, 3, 2, 0), (1, 1, 1, 0),
+                                             (1, 5, 1, 2), (3, 3, 1, 0)])
+def test_generic_path(dt, cm, k, stride, pad):
+    _case(2, 10, 9, 8, 12, cm=cm, k=k, stride=stride, pad=pad, dt=dt)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_channels_not_vector_multiple(dt):
+    _case(2, 7, 7, 5, 9, dt=dt)
+    _case(1, 6, 8, 12, 3, dt=dt)
+
+
+def test_one_pixel_image():
+    _case(1, 1, 1, 8, 8, pad=1)
+
+
+@pytest.mark.parametrize("variant", ["f32", "bf16", "bf16_out_bf16"])
+def test_config_full_size_sampled_images(variant):
+    d = workloads.dwsep()
+    if variant == "f32":
+        X, D, P = d["X"], d["D"], d["P"]
+    else:
+        X, D, P = d["X_bf16"], d["D_bf16"], d["P_bf16"]
+    ot = torch.bfloat16 if variant == "bf16_out_bf16" else torch.float32
+    y = isam.dwsep_conv(to_gpu(X), to_gpu(D), to_gpu(P), out_dtype=ot)
+    torch.cuda.synchronize()
+    imgs = [0, 13, 31]   # images are independent: the oracle runs on a subset of the batch
+    Z, S = oracle.dwsep(np.ascontiguousarray(X[imgs]), D, P)
+    got = to_host_f64(y[torch.as_tensor(imgs, device="cuda")])
+    tol = TOL_F32 if variant == "f32" else TOL_BF16
+    assert norm_err(got, Z, S) <= tol

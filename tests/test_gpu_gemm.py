@@ -1,0 +1,156 @@
+"""GPU parity of isam_gemm against the CPU oracle (the paper's first listing)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth import workloads
+from tests._util import TOL_BF16, TOL_F32, bits, norm_err, to_gpu, to_host_f64
+
+pytestmark = pytest.mark.gpu
+
+import paper_1810_09958_amd as isam
+
+
+def _run_case(M, N, K, dt, ct, ta=0, tb=0, accumulate=False, seed=0, pad_ld=0):
+    Am = synth.uniform(seed, 10, (M, K), -1, 1)
+    Bm = synth.uniform(seed, 11, (K, N), -1, 1)
+    A_host = np.ascontiguousarray(Am.T) if ta else Am
+    B_host = np.ascontiguousarray(Bm.T) if tb else Bm
+    if pad_ld:
+        A_host = np.pad(A_host, ((0, 0), (0, pad_ld)), constant_values=7.0)
+        B_host = np.pad(B_host, ((0, 0), (0, pad_ld)), constant_values=-7.0)
+    if dt == "bf16":
+        A_host, B_host = bits(A_host), bits(B_host)
+    A, B = to_gpu(A_host), to_gpu(B_host)
+    if pad_ld:
+        A = A[:, : A.shape[1] - pad_ld]
+        B = B[:, : B.shape[1] - pad_ld]
+    out_dtype = torch.bfloat16 if ct == "bf16" else torch.float32
+    C_in = None
+    if accumulate:
+        c0 = synth.uniform(seed, 12, (M, N), -1, 1)
+        C = to_gpu(bits(c0) if ct == "bf16" else c0)
+        C_in = to_host_f64(C)
+        isam.gemm(A, B, C, trans_a=bool(ta), trans_b=bool(tb), accumulate=True)
+    else:
+        C = isam.gemm(A, B, trans_a=bool(ta), trans_b=bool(tb), out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    lda = A_host.shape[1]
+    ldb = B_host.shape[1]
+    ref, S = oracle.gemm(A_host, B_host, M, N, K, ta, tb, lda=lda, ldb=ldb, C_in=C_in)
+    err = norm_err(to_host_f64(C), ref, S)
+    tol = TOL_F32 if (dt == "f32" and ct == "f32") else TOL_BF16
+    assert err <= tol, f"M={M} N={N} K={K} {dt}->{ct} ta={ta} tb={tb} acc={accumulate}: err {err:.3e}"
+    return err
+
+
+def test_config_fp32_128_cubed():
+    d = workloads.gemm_small_fp32()
+    A, B = to_gpu(d["A"]), to_gpu(d["B"])
+    C = isam.gemm(A, B)
+    torch.cuda.synchronize()
+    ref, S = oracle.gemm(d["A"], d["B"], 128, 128, 128)
+    assert norm_err(to_host_f64(C), ref, S) <= TOL_F32
+
+
+SIZES = [1, 7, 31, 64, 65, 129]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_shape_sweep_layouts(dt, ta, tb):
+    for M in SIZES:
+        for N in (1, 33, 64, 200):
+            for K in (1, 31, 64, 129):
+                _run_case(M, N, K, dt, "f32" if dt == "f32" else "bf16", ta, tb, seed=M * 7 + N + K)
+
+
+@pytest.mark.parametrize("dt,ct", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16"), ("f32", "bf16")])
+@pytest.mark.parametrize("shape", [(256, 256, 256), (300, 520, 192), (1000, 96, 1000), (520, 700, 64),
+                                   (64, 4096, 72), (2048, 40, 2048)])
+def test_tiles_and_outputs(dt, ct, shape):
+    M, N, K = shape
+    _run_case(M, N, K, dt, ct)
+
+
+@pytest.mark.parametrize("dt,ct", [("f32", "f32"), ("bf16", "bf16")])
+def test_accumulate(dt, ct):
+    _run_case(129, 65, 257, dt, ct, accumulate=True)
+    _run_case(1024, 32, 2048, dt, ct, accumulate=True)   # split-K path with accumulate
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_leading_dimension_padding(dt):
+    _run_case(100, 72, 136, dt, "f32", pad_ld=8)
+    _run_case(100, 72, 136, dt, "f32", ta=1, tb=1, pad_ld=8)
+
+
+def test_k_zero():
+    A = torch.empty((5, 0), device="cuda", dtype=torch.float32)
+    B = torch.empty((0, 6), device="cuda", dtype=torch.float32)
+    C = isam.gemm(A, B)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(C).item() == 0
+    C2 = torch.full((5, 6), 3.0, device="cuda")
+    isam.gemm(A, B, C2, accumulate=True)
+    torch.cuda.synchronize()
+    assert torch.all(C2 == 3.0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_guard_bands_untouched(dt):
+    M, N, K, ldc = 130, 70, 96, 80
+    A_h = synth.uniform(1, 0, (M, K), -1, 1)
+    B_h = synth.uniform(1, 1, (K, N), -1, 1)
+    if dt == "bf16":
+        A_h, B_h = bits(A_h), bits(B_h)
+    A, B = to_gpu(A_h), to_gpu(B_h)
+    buf = torch.full((M * ldc + 4096,), -12345.0, device="cuda")
+    C = buf[2048: 2048 + M * ldc].view(M, ldc)[:, :N]
+    isam.gemm(A, B, C)
+    torch.cuda.synchronize()
+    h = buf.cpu().numpy()
+    assert np.all(h[:2048] == -12345.0) and np.all(h[2048 + M * ldc:] == -12345.0)
+    body = h[2048: 2048 + M * ldc].reshape(M, ldc)
+    assert np.all(body[:, N:] == -12345.0)
+    ref, S = oracle.gemm(A_h, B_h, M, N, K)
+    assert norm_err(body[:, :N].astype(np.float64), ref, S) <= (TOL_F32 if dt == "f32" else TOL_BF16)
+
+
+def test_deterministic_run_twice():
+    for (M, N, K) in [(512, 512, 512), (4096, 32, 4096)]:
+        A = to_gpu(bits(synth.uniform(2, 0, (M, K), -1, 1)))
+        B = to_gpu(bits(synth.uniform(2, 1, (K, N), -1, 1)))
+        c1 = isam.gemm(A, B)
+        c2 = isam.gemm(A, B)
+        torch.cuda.synchronize()
+        assert torch.equal(c1, c2)
+
+
+@pytest.mark.parametrize("variant", ["bf16", "f32"])
+def test_config_skinny_full(variant):
+    d = workloads.skinny()
+    A_h = d["A_bf16"] if variant == "bf16" else d["A"]
+    B_h = d["B_bf16"] if variant == "bf16" else d["B"]
+    C = isam.gemm(to_gpu(A_h), to_gpu(B_h))
+    torch.cuda.synchronize()
+    ref, S = oracle.gemm(A_h, B_h, 4096, 32, 4096)
+    err = norm_err(to_host_f64(C), ref, S)
+    assert err <= (TOL_BF16 if variant == "bf16" else TOL_F32), err
+
+
+@pytest.mark.parametrize("which", ["square", "rect"])
+@pytest.mark.parametrize("ct", ["bf16", "f32"])
+def test_config_large_bf16_sampled_rows(which, ct):
+    d = workloads.gemm_square_bf16() if which == "square" else workloads.gemm_rect_bf16()
+    A_h, B_h = d["A_bf16"], d["B_bf16"]
+    M, K = A_h.shape
+    N = B_h.shape[1]
+    C = isam.gemm(to_gpu(A_h), to_gpu(B_h), out_dtype=torch.bfloat16 if ct == "bf16" else torch.float32)
+    torch.cuda.synchronize()
+    rows = workloads.rows_sample(M, 48)
+    ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), B_h, len(rows), N, K)
+    got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
+    assert norm_err(got, ref, S) <= TOL_BF16

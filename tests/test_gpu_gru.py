@@ -1,0 +1,115 @@
+"""GPU parity of isam_gru_forward against the CPU oracle (GRU cells as matmul + element-wise
+work, Section 6.1; recurrence as priming / recursive / finish iterations, Section 3.6).
+The GRU output is a convex blend of tanh values and h0, so |h| <= max(1, |h0|); the check is
+the maximum absolute difference, with the same 1e-2 (bf16 weights) / 1e-5 (fp32) split."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth import workloads
+from tests._util import TOL_BF16, TOL_F32, bits, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+import paper_1810_09958_amd as isam
+
+
+def _inputs(T, B, I, H, seed=0, scale=1 / 32, with_h0=False, with_bhn=False):
+    x = synth.normal(seed, 3, (T, B, I))
+    W = synth.uniform(seed, 0, (3 * H, I), -scale, scale)
+    U = synth.uniform(seed, 1, (3 * H, H), -scale, scale)
+    b = synth.normal(seed, 2, (3 * H,), scale=0.1)
+    h0 = synth.normal(seed, 4, (B, H), scale=0.5) if with_h0 else None
+    bhn = synth.normal(seed, 5, (H,), scale=0.1) if with_bhn else None
+    return x, W, U, b, h0, bhn
+
+
+def _run(T, B, I, H, dt="bf16", seed=0, with_h0=False, with_bhn=False, scale=1 / 32):
+    x, W, U, b, h0, bhn = _inputs(T, B, I, H, seed, scale, with_h0, with_bhn)
+    if dt == "bf16":
+        x, W, U = bits(x), bits(W), bits(U)
+    hs, hT = isam.gru_forward(to_gpu(x), to_gpu(W), to_gpu(U), bias=to_gpu(b),
+                              bias_hn=None if bhn is None else to_gpu(bhn),
+                              h0=None if h0 is None else to_gpu(h0))
+    torch.cuda.synchronize()
+    ref = oracle.gru(x, W, U, b, bhn, h0)
+    hs = hs.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(hs))
+    err = float(np.max(np.abs(hs - ref)))
+    tol = TOL_BF16 if dt == "bf16" else TOL_F32
+    assert err <= tol, f"T={T} B={B} I={I} H={H} {dt} h0={with_h0} bhn={with_bhn}: {err:.3e}"
+    assert np.array_equal(hT.cpu().numpy(), hs[-1].astype(np.float32))
+    return err
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("T", [1, 2, 3, 9])
+def test_small_steps(dt, T):
+    _run(T, 4, 40, 64, dt, seed=T, with_h0=True, with_bhn=True, scale=1 / 4)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("B,H", [(1, 128), (16, 256), (17, 64), (33, 96), (5, 1024)])
+def test_shapes(dt, B, H):
+    _run(5, B, 72, H, dt, seed=B + H, with_h0=(B % 2 == 1), scale=1 / 8)
+
+
+def test_h0_null_equals_zeros():
+    T, B, I, H = 4, 8, 64, 128
+    x, W, U, b, _, _ = _inputs(T, B, I, H)
+    args = [to_gpu(bits(a)) for a in (x, W, U)]
+    hs1, _ = isam.gru_forward(*args, bias=to_gpu(b))
+    hs2, _ = isam.gru_forward(*args, bias=to_gpu(b), h0=torch.zeros(B, H, device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.equal(hs1, hs2)
+
+
+def test_time_split_chains_through_h_T():
+    # Priming + recursive + finish over T steps == two calls chained through h_T.
+    T, B, I, H = 6, 4, 64, 128
+    x, W, U, b, _, _ = _inputs(T, B, I, H, seed=9)
+    xg, Wg, Ug = (to_gpu(a) for a in (x, W, U))
+    hs_full, _ = isam.gru_forward(xg, Wg, Ug, bias=to_gpu(b))
+    hs1, hT1 = isam.gru_forward(xg[:2].contiguous(), Wg, Ug, bias=to_gpu(b))
+    hs2, _ = isam.gru_forward(xg[2:].contiguous(), Wg, Ug, bias=to_gpu(b), h0=hT1)
+    torch.cuda.synchronize()
+    assert torch.max(torch.abs(torch.cat([hs1, hs2]) - hs_full)).item() <= 1e-6
+
+
+def test_t_zero_copies_h0():
+    B, H = 3, 64
+    h0 = torch.randn(B, H, device="cuda")
+    x = torch.empty((0, B, 16), device="cuda")
+    W = torch.zeros(3 * H, 16, device="cuda")
+    U = torch.zeros(3 * H, H, device="cuda")
+    _, hT = isam.gru_forward(x, W, U, h0=h0, return_sequence=False)
+    torch.cuda.synchronize()
+    assert torch.equal(hT, h0)
+
+
+def test_deterministic_run_twice():
+    T, B, I, H = 8, 32, 256, 256
+    x, W, U, b, _, _ = _inputs(T, B, I, H)
+    args = [to_gpu(bits(a)) for a in (x, W, U)]
+    a1, _ = isam.gru_forward(*args, bias=to_gpu(b))
+    a2, _ = isam.gru_forward(*args, bias=to_gpu(b))
+    torch.cuda.synchronize()
+    assert torch.equal(a1, a2)
+
+
+@pytest.mark.parametrize("variant", ["bf16", "f32"])
+def test_config_full_size_sampled_sequences(variant):
+    d = workloads.gru()
+    if variant == "bf16":
+        x, W, U = d["x_bf16"], d["W_bf16"], d["U_bf16"]
+    else:
+        x, W, U = d["x"], d["W"], d["U"]
+    hs, hT = isam.gru_forward(to_gpu(x), to_gpu(W), to_gpu(U), bias=to_gpu(d["bias"]))
+    torch.cuda.synchronize()
+    seqs = [0, 17, 31]   # batch entries are independent sequences
+    ref = oracle.gru(np.ascontiguousarray(x[:, seqs]), W, U, d["bias"], None, None)
+    got = hs[:, seqs].cpu().numpy().astype(np.float64)
+    err = float(np.max(np.abs(got - ref)))
+    assert err <= (TOL_BF16 if variant == "bf16" else TOL_F32), err
