@@ -1,0 +1,283 @@
+"""Benchmark of the whole hot path on one MI355X.
+
+A step runs every part of the path once, on seeded synthetic inputs already resident in
+HBM:
+  * bf16 GEMM 8192 x 8192 x 8192, bf16 and fp32 outputs
+  * bf16 GEMM M=8192 N=1024 K=16384, bf16 and fp32 outputs
+  * skinny GEMM 4096 x 32 x 4096, bf16 and fp32 inputs (fp32 out)
+  * GRU forward T=64, batch 32, input = hidden = 1024, bf16 weights
+  * separable depthwise conv 32 x 56 x 56 x 128 -> 256, bf16 (fp32 out) and fp32
+  * fp32 GEMM 128^3
+Each part is bracketed by HIP events on the stream the library launches on (torch's current
+stream), so the per-part times are device times.  `value` is the GEMM throughput of the
+large bf16 GEMMs (total FLOP / total time); GRU timesteps/s, separable-conv GB/s and the
+rest are reported under "components".  `roofline` covers the dominant kernel (the square
+bf16 GEMM, bf16 output); `cpu_baseline` times the CPU oracle on a bounded sample.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "GEMM TFLOP/s (% of MFMA peak); GRU timesteps/sec; dwsep conv GB/s"
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", default="", help="comma list of component names to run (profiling)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: this library has no multi-GPU path "
+              "(the kernels are timed on one GPU's share of the work).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1810_09958_amd as isam
+    from synth import workloads
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def gpu(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    t_setup = time.time()
+    only = set(s for s in args.only.split(",") if s)
+    comps = []   # (name, callable, info dict)
+
+    def want(name):
+        return not only or name in only
+
+    # -- large bf16 GEMMs -------------------------------------------------------------
+    sq = workloads.gemm_square_bf16()
+    Aq, Bq = gpu(sq["A_bf16"]), gpu(sq["B_bf16"])
+    del sq
+    Cq16 = torch.empty((8192, 8192), device=dev, dtype=torch.bfloat16)
+    Cq32 = torch.empty((8192, 8192), device=dev, dtype=torch.float32)
+    rc = workloads.gemm_rect_bf16()
+    Ar, Br = gpu(rc["A_bf16"]), gpu(rc["B_bf16"])
+    del rc
+    Cr16 = torch.empty((8192, 1024), device=dev, dtype=torch.bfloat16)
+    Cr32 = torch.empty((8192, 1024), device=dev, dtype=torch.float32)
+    f_sq = 2.0 * 8192 ** 3
+    f_rc = 2.0 * 8192 * 1024 * 16384
+
+    def gemm_bytes(M, N, K, cbytes):
+        return 2 * (M * K + K * N) + cbytes * M * N
+
+    for name, A, B, C, fl, M, N, K in [
+        ("gemm_8192x8192x8192_bf16_out_bf16", Aq, Bq, Cq16, f_sq, 8192, 8192, 8192),
+        ("gemm_8192x8192x8192_bf16_out_f32", Aq, Bq, Cq32, f_sq, 8192, 8192, 8192),
+        ("gemm_8192x1024x16384_bf16_out_bf16", Ar, Br, Cr16, f_rc, 8192, 1024, 16384),
+        ("gemm_8192x1024x16384_bf16_out_f32", Ar, Br, Cr32, f_rc, 8192, 1024, 16384),
+    ]:
+        ws = torch.empty(max(1, isam.gemm_workspace_size(M, N, K, 1, 1 if C.dtype == torch.bfloat16 else 0)),
+                         device=dev, dtype=torch.uint8)
+        if want(name):
+            comps.append((name, (lambda A=A, B=B, C=C, ws=ws: isam.gemm(A, B, C, workspace=ws)),
+                          {"kind": "gemm_bf16", "flop": fl,
+                           "bytes": gemm_bytes(M, N, K, C.element_size())}))
+
+    # -- skinny GEMM ------------------------------------------------------------------
+    sk = workloads.skinny()
+    for name, A_h, B_h, es in [("skinny_4096x32x4096_bf16", sk["A_bf16"], sk["B_bf16"], 2),
+                               ("skinny_4096x32x4096_f32", sk["A"], sk["B"], 4)]:
+        A, B = gpu(A_h), gpu(B_h)
+        C = torch.empty((4096, 32), device=dev, dtype=torch.float32)
+        ws = torch.empty(max(1, isam.gemm_workspace_size(4096, 32, 4096, 1 if es == 2 else 0, 0)),
+                         device=dev, dtype=torch.uint8)
+        if want(name):
+            comps.append((name, (lambda A=A, B=B, C=C, ws=ws: isam.gemm(A, B, C, workspace=ws)),
+                          {"kind": "skinny", "flop": 2.0 * 4096 * 32 * 4096,
+                           "bytes": es * (4096 * 4096 + 4096 * 32) + 4 * 4096 * 32}))
+    del sk
+
+    # -- GRU --------------------------------------------------------------------------
+    g = workloads.gru()
+    T, Bt, I, H = 64, 32, 1024, 1024
+    gx, gW, gU, gb = gpu(g["x_bf16"]), gpu(g["W_bf16"]), gpu(g["U_bf16"]), gpu(g["bias"])
+    g_hseq = torch.empty((T, Bt, H), device=dev)
+    g_hT = torch.empty((Bt, H), device=dev)
+    g_ws = torch.empty(isam.gru_forward_workspace_size(T, Bt, I, H, 1), device=dev, dtype=torch.uint8)
+    del g
+    if want("gru_T64_B32_H1024_bf16"):
+        comps.append(("gru_T64_B32_H1024_bf16",
+                      lambda: isam.gru_forward(gx, gW, gU, bias=gb, h_seq=g_hseq, h_T=g_hT, workspace=g_ws),
+                      {"kind": "gru", "steps": T,
+                       "flop": 2.0 * T * Bt * 3 * H * (I + H),
+                       "bytes": 2 * (3 * H * I + 3 * H * H + T * Bt * I) + 4 * T * Bt * H}))
+
+    # -- separable depthwise conv -------------------------------------------------------
+    d = workloads.dwsep()
+    for name, X_h, D_h, P_h, es in [("dwsep_32x56x56x128_256_bf16_out_f32", d["X_bf16"], d["D_bf16"], d["P_bf16"], 2),
+                                    ("dwsep_32x56x56x128_256_f32", d["X"], d["D"], d["P"], 4)]:
+        X, Dw, P = gpu(X_h), gpu(D_h), gpu(P_h)
+        y = torch.empty((32, 56, 56, 256), device=dev, dtype=torch.float32)
+        it = 1 if es == 2 else 0
+        ws = torch.empty(isam.dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, it, 0),
+                         device=dev, dtype=torch.uint8)
+        if want(name):
+            comps.append((name, (lambda X=X, Dw=Dw, P=P, y=y, ws=ws: isam.dwsep_conv(X, Dw, P, out=y, workspace=ws)),
+                          {"kind": "dwsep", "flop": 2.0 * 100352 * (9 * 128 + 128 * 256),
+                           # fused minimum: X read once, y written once (+ the small filters)
+                           "bytes": es * (32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + 4 * 100352 * 256}))
+    del d
+
+    # -- small fp32 GEMM ------------------------------------------------------------------
+    s1 = workloads.gemm_small_fp32()
+    A1, B1 = gpu(s1["A"]), gpu(s1["B"])
+    C1 = torch.empty((128, 128), device=dev)
+    if want("gemm_128x128x128_f32"):
+        comps.append(("gemm_128x128x128_f32", lambda: isam.gemm(A1, B1, C1),
+                      {"kind": "gemm_f32", "flop": 2.0 * 128 ** 3, "bytes": 3 * 4 * 128 * 128}))
+    torch.cuda.synchronize()
+    t_setup = time.time() - t_setup
+
+    stream = torch.cuda.current_stream()
+
+    def run_step(evs=None):
+        for i, (_, fn, _) in enumerate(comps):
+            if evs is not None:
+                evs[i][0].record(stream)
+            fn()
+            if evs is not None:
+                evs[i][1].record(stream)
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    events = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+               for _ in comps] for _ in range(K)]
+    t0 = time.perf_counter()
+    for k in range(K):
+        run_step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    results = {}
+    for i, (name, _, info) in enumerate(comps):
+        ms = [events[k][i][0].elapsed_time(events[k][i][1]) for k in range(K)]
+        avg = float(np.mean(ms))
+        r = {"us_avg": round(avg * 1e3, 2), "us_median": round(float(np.median(ms)) * 1e3, 2),
+             "us_p10": round(float(np.percentile(ms, 10)) * 1e3, 2),
+             "us_p90": round(float(np.percentile(ms, 90)) * 1e3, 2)}
+        s = avg * 1e-3
+        tfl = info["flop"] / s / 1e12
+        gbs = info["bytes"] / s / 1e9
+        r["TFLOP/s"] = round(tfl, 2)
+        r["GB/s"] = round(gbs, 1)
+        if info["kind"] == "gemm_bf16":
+            r["frac_bf16_peak"] = round(tfl / PEAK_BF16_TFLOPS, 4)
+        elif info["kind"] == "gemm_f32":
+            r["frac_f32_peak"] = round(tfl / PEAK_F32_TFLOPS, 6)
+        elif info["kind"] in ("skinny", "dwsep"):
+            r["frac_hbm_peak"] = round(gbs / PEAK_HBM_GBPS, 4)
+        if info["kind"] == "gru":
+            r["timesteps_per_s"] = round(info["steps"] / s, 1)
+            r["us_per_timestep"] = round(avg * 1e3 / info["steps"], 3)
+        results[name] = r
+
+    gemm_names = [n for n, _, i in comps if i["kind"] == "gemm_bf16"]
+    if gemm_names:
+        tot_flop = sum(i["flop"] for n, _, i in comps if i["kind"] == "gemm_bf16")
+        tot_s = sum(results[n]["us_avg"] for n in gemm_names) * 1e-6
+        value = tot_flop / tot_s / 1e12
+    else:
+        value = None
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2) if value is not None else None,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / K, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "hot path: bf16 GEMM 8192^3 + 8192x1024x16384 (bf16/fp32 out), skinny 4096x32x4096, "
+                        "GRU T64 B32 I1024 H1024, dwsep 32x56x56x128->256, fp32 GEMM 128^3",
+            "value_is": "large bf16 GEMM throughput (total FLOP / total device time of those launches)",
+            "parallelism": "single GPU",
+        },
+    }
+    if value is not None:
+        out["frac_of_bf16_peak"] = round(value / PEAK_BF16_TFLOPS, 4)
+    dom = "gemm_8192x8192x8192_bf16_out_bf16"
+    if dom in results:
+        ach = results[dom]["TFLOP/s"]
+        out["roofline"] = {"kernel": "gemm_tile_kernel<bf16, 256x256> (8192^3, bf16 out)",
+                           "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                           "traffic": None}
+    if "gru_T64_B32_H1024_bf16" in results:
+        out["gru_timesteps_per_s"] = results["gru_T64_B32_H1024_bf16"]["timesteps_per_s"]
+    if "dwsep_32x56x56x128_256_bf16_out_f32" in results:
+        out["dwsep_GBps"] = results["dwsep_32x56x56x128_256_bf16_out_f32"]["GB/s"]
+    out["components"] = results
+    out["setup_s"] = round(t_setup, 1)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline():
+    """The CPU oracle (fp64, as used for parity) on a bounded sample of the square GEMM:
+    R full rows of C = A.B with K = 8192, timed on this host's cores."""
+    import oracle
+    from synth import workloads
+
+    sq = workloads.gemm_square_bf16()
+    A, B = sq["A_bf16"], sq["B_bf16"]
+    threads = oracle.max_threads()
+    rows = 8
+    t = time.perf_counter()
+    oracle.gemm(np.ascontiguousarray(A[:rows]), B, rows, 8192, 8192, with_norm=False)
+    dt = time.perf_counter() - t
+    # scale the sample to about 10 s of work
+    rows2 = int(min(8192, max(rows, rows * 10.0 / max(dt, 1e-3))))
+    rows2 = max(threads, (rows2 // threads) * threads)
+    t = time.perf_counter()
+    oracle.gemm(np.ascontiguousarray(A[:rows2]), B, rows2, 8192, 8192, with_norm=False)
+    dt2 = time.perf_counter() - t
+    fl = 2.0 * rows2 * 8192 * 8192
+    return {"value": round(fl / dt2 / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{rows2} rows of the 8192^3 bf16 GEMM (fp64 naive loops), {dt2:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

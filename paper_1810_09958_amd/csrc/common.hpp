@@ -5,7 +5,29 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace isam {
+
+// Compile-time loop: f(std::integral_constant<int, I>{}) for I = 0 .. N-1, so
+// register-array indices stay constants (no dynamic indexing into scratch).
+template <int I, int N>
+struct StaticFor {
+    template <typename F>
+    __device__ __forceinline__ static void run(F&& f) {
+        f(std::integral_constant<int, I>{});
+        StaticFor<I + 1, N>::run(f);
+    }
+};
+template <int N>
+struct StaticFor<N, N> {
+    template <typename F>
+    __device__ __forceinline__ static void run(F&&) {}
+};
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    StaticFor<0, N>::run(f);
+}
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;

@@ -173,12 +173,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, Til
     TileLoader<T, BN, NT, TB, VEC> lb;
 
     f32x16_t acc[MI][NI];
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) { acc[i][j][decltype(v)::value] = 0.0f; });
+        });
+    });
 
     if (nk > 0) {
         la.load(rsA, tid, m0, kbeg, a.M, kend, a.lda);
@@ -196,24 +195,22 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, Til
             }
             const char* As = cur;
             const char* Bs = cur + BM * 128;
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
+            static_for<4>([&](auto ks) {
                 uint4 af[MI], bfr[NI];
                 const int ch = ks * 2 + (lane >> 5);
-#pragma unroll
-                for (int i = 0; i < MI; ++i)
+                static_for<MI>([&](auto i) {
                     af[i] = *reinterpret_cast<const uint4*>(As + lds_off(wm * WTM + i * 32 + (lane & 31), ch));
-#pragma unroll
-                for (int j = 0; j < NI; ++j)
+                });
+                static_for<NI>([&](auto j) {
                     bfr[j] = *reinterpret_cast<const uint4*>(Bs + lds_off(wn * WTN + j * 32 + (lane & 31), ch));
-#pragma unroll
-                for (int i = 0; i < MI; ++i)
-#pragma unroll
-                    for (int j = 0; j < NI; ++j) {
+                });
+                static_for<MI>([&](auto i) {
+                    static_for<NI>([&](auto j) {
                         if constexpr (sizeof(T) == 2) mfma32_bf16(acc[i][j], af[i], bfr[j]);
                         else mfma32_f32x4(acc[i][j], af[i], bfr[j]);
-                    }
-            }
+                    });
+                });
+            });
             if (more) {
                 la.store(nxt, tid);
                 lb.store(nxt + BM * 128, tid);
@@ -222,38 +219,78 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, Til
         }
     }
 
-    // Epilogue.  Accumulator element v of lane l: row 8*(v/4) + 4*(l/32) + v%4, column l%32.
+    // Epilogue, one 32-row slab of the wave tile at a time: the accumulators
+    // (element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32 of a
+    // 32x32 block) go to a per-wave LDS buffer, then each lane reads 4
+    // consecutive columns back and writes them with one vector store.
     const bool split_out = gridDim.y > 1;
+    constexpr int EPI_LD = WTN * 4 + 16;  // bytes per staged row (padding spreads banks)
+    static_assert(4 * 32 * EPI_LD <= 2 * STAGE, "epilogue staging must fit in LDS");
+    char* epi = smem + wid * 32 * EPI_LD;
     float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-            const int64_t col = n0 + wn * WTN + j * 32 + (lane & 31);
-            if (col >= a.N) continue;
-            const float bv = (!split_out && a.bias) ? a.bias[col] : 0.0f;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t row = m0 + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                if (row >= a.M) continue;
-                float val = acc[i][j][v];
-                if (split_out) {
-                    P[row * a.N + col] = val;
+    const int64_t ldo = split_out ? a.N : a.ldc;
+    const int osz = split_out ? 4 : (a.c_type == kF32 ? 4 : 2);
+    char* obase = split_out ? reinterpret_cast<char*>(P) : static_cast<char*>(a.C);
+    const bool vec_out = ((reinterpret_cast<uintptr_t>(obase) & 15) == 0) && ((ldo * osz) % 16 == 0);
+    constexpr int Q = WTN / 4;  // float4 groups per staged row
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) {
+                constexpr int vv = decltype(v)::value;
+                const int r = 8 * (vv >> 2) + 4 * (lane >> 5) + (vv & 3);
+                *reinterpret_cast<float*>(epi + r * EPI_LD + (j * 32 + (lane & 31)) * 4) = acc[i][j][vv];
+            });
+        });
+        __syncthreads();
+        const int64_t row0 = m0 + wm * WTM + i * 32;
+        const int64_t col0 = n0 + wn * WTN;
+        for (int q = lane; q < 32 * Q; q += 64) {
+            const int r = q / Q, c4 = q - r * Q;
+            const int64_t row = row0 + r, col = col0 + c4 * 4;
+            if (row >= a.M || col >= a.N) continue;
+            float4 v4 = *reinterpret_cast<const float4*>(epi + r * EPI_LD + c4 * 16);
+            float vals[4] = {v4.x, v4.y, v4.z, v4.w};
+            const int nv = (int)((a.N - col) < 4 ? (a.N - col) : 4);
+            if (!split_out && a.bias) {
+                for (int e = 0; e < nv; ++e) vals[e] += a.bias[col + e];
+            }
+            const int64_t idx = row * ldo + col;
+            if (split_out || a.c_type == kF32) {
+                float* C = reinterpret_cast<float*>(obase);
+                if (nv == 4 && vec_out) {
+                    if (!split_out && a.accumulate) {
+                        float4 c = *reinterpret_cast<const float4*>(C + idx);
+                        vals[0] += c.x; vals[1] += c.y; vals[2] += c.z; vals[3] += c.w;
+                    }
+                    *reinterpret_cast<float4*>(C + idx) = make_float4(vals[0], vals[1], vals[2], vals[3]);
                 } else {
-                    val += bv;
-                    const int64_t idx = row * a.ldc + col;
-                    if (a.c_type == kF32) {
-                        float* C = static_cast<float*>(a.C);
-                        if (a.accumulate) val += C[idx];
-                        C[idx] = val;
-                    } else {
-                        uint16_t* C = static_cast<uint16_t*>(a.C);
-                        if (a.accumulate) val += bf16_to_f32(C[idx]);
-                        C[idx] = (uint16_t)f32_to_bf16(val);
+                    for (int e = 0; e < nv; ++e) {
+                        float val = vals[e];
+                        if (!split_out && a.accumulate) val += C[idx + e];
+                        C[idx + e] = val;
+                    }
+                }
+            } else {
+                uint16_t* C = reinterpret_cast<uint16_t*>(obase);
+                if (nv == 4 && ((reinterpret_cast<uintptr_t>(C + idx) & 7) == 0)) {
+                    if (a.accumulate) {
+                        uint2 c = *reinterpret_cast<const uint2*>(C + idx);
+                        vals[0] += bf16lo(c.x); vals[1] += bf16hi(c.x);
+                        vals[2] += bf16lo(c.y); vals[3] += bf16hi(c.y);
+                    }
+                    *reinterpret_cast<uint2*>(C + idx) =
+                        make_uint2(pack_bf16x2(vals[0], vals[1]), pack_bf16x2(vals[2], vals[3]));
+                } else {
+                    for (int e = 0; e < nv; ++e) {
+                        float val = vals[e];
+                        if (a.accumulate) val += bf16_to_f32(C[idx + e]);
+                        C[idx + e] = (uint16_t)f32_to_bf16(val);
                     }
                 }
             }
         }
+        __syncthreads();
+    });
 }
 
 // Function table for one element type: [tile][trans_a][trans_b][vec].
