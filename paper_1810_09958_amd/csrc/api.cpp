@@ -5,7 +5,7 @@
 // interface (Section 4): every tiling, split and rasterisation choice is made
 // in one place (the plan_* functions below) from the problem shape and the
 // device's compute-unit count, and can be overridden for tuning with the
-// environment variable ISAM_GEMM_CONFIG="tile=<0-5>,splits=<n>,group=<n>,xcd=<0|1>".
+// environment variable ISAM_GEMM_CONFIG="tile=<0-5>,splits=<n>,group=<n>,xcd=<0|1>,dma=<0|1>".
 // ISAM_LOG=1 prints each chosen plan to stderr.
 #include <hip/hip_runtime.h>
 
@@ -103,6 +103,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus) {
     p.k_per_split = K;
     p.group_m = 8;
     p.xcd_remap = 1;
+    p.dma = 1;
     int bm, bn, bk;
     auto tiles = [&](int t) {
         tile_dims(t, ab_type, &bm, &bn, &bk);
@@ -144,6 +145,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus) {
         if ((s = strstr(env, "tile=")) && sscanf(s + 5, "%d", &v) == 1 && v >= 0 && v < kTileCount) p.tile = v;
         if ((s = strstr(env, "group=")) && sscanf(s + 6, "%d", &v) == 1 && v > 0) p.group_m = v;
         if ((s = strstr(env, "xcd=")) && sscanf(s + 4, "%d", &v) == 1) p.xcd_remap = v ? 1 : 0;
+        if ((s = strstr(env, "dma=")) && sscanf(s + 4, "%d", &v) == 1) p.dma = v ? 1 : 0;
         if ((s = strstr(env, "splits=")) && sscanf(s + 7, "%d", &v) == 1 && v >= 1) {
             tile_dims(p.tile, ab_type, &bm, &bn, &bk);
             p.k_per_split = std::max<int64_t>(bk, cdiv(cdiv(K, v), bk) * bk);
@@ -221,9 +223,9 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         if (p.tile != kTile64x64 && p.tile != kTile128x32) p.tile = kTile64x64;
     }
     if (log_enabled())
-        fprintf(stderr, "[isam] %s M=%lld N=%lld K=%lld ta=%d tb=%d ab=%d c=%d tile=%d vec=%d splits=%d kps=%lld group=%d xcd=%d\n",
+        fprintf(stderr, "[isam] %s M=%lld N=%lld K=%lld ta=%d tb=%d ab=%d c=%d tile=%d vec=%d splits=%d kps=%lld group=%d xcd=%d dma=%d\n",
                 who, (long long)M, (long long)N, (long long)K, trans_a, trans_b, ab_type, c_type, p.tile, p.vec,
-                p.k_splits, (long long)p.k_per_split, p.group_m, p.xcd_remap);
+                p.k_splits, (long long)p.k_per_split, p.group_m, p.xcd_remap, p.dma);
     GemmArgs a{};
     a.A = A;
     a.B = B;

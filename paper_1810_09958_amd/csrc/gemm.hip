@@ -6,6 +6,7 @@ namespace isam {
 
 GemmKernelFn gemm_kernel_bf16(int tile, int ta, int tb, int vec);
 GemmKernelFn gemm_kernel_f32(int tile, int ta, int tb, int vec);
+GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk) {
     static const int dims[kTileCount][2] = {{256, 256}, {256, 128}, {128, 128},
@@ -42,8 +43,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int spli
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     int bm, bn, bk;
     tile_dims(p.tile, a.ab_type, &bm, &bn, &bk);
-    GemmKernelFn fn = a.ab_type == kBF16 ? gemm_kernel_bf16(p.tile, a.trans_a, a.trans_b, p.vec)
-                                         : gemm_kernel_f32(p.tile, a.trans_a, a.trans_b, p.vec);
+    GemmKernelFn fn = nullptr;
+    if (p.dma && a.ab_type == kBF16 && !a.trans_a && p.vec) fn = gemm_dma_kernel_for(p.tile, a.trans_b);
+    if (!fn)
+        fn = a.ab_type == kBF16 ? gemm_kernel_bf16(p.tile, a.trans_a, a.trans_b, p.vec)
+                                : gemm_kernel_f32(p.tile, a.trans_a, a.trans_b, p.vec);
     if (!fn) return hipErrorInvalidValue;
     TileMapArgs t;
     t.tiles_m = (int)((a.M + bm - 1) / bm);

@@ -1,0 +1,16 @@
+// Instantiations of the direct-to-LDS bf16 GEMM kernel (A K-contiguous;
+// B K-contiguous or N-contiguous).
+#include "gemm_dma.hpp"
+
+namespace isam {
+
+GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b) {
+    switch (tile) {
+        case kTile256x256: return trans_b ? gemm_dma_kernel<256, 256, true> : gemm_dma_kernel<256, 256, false>;
+        case kTile256x128: return trans_b ? gemm_dma_kernel<256, 128, true> : gemm_dma_kernel<256, 128, false>;
+        case kTile128x128: return trans_b ? gemm_dma_kernel<128, 128, true> : gemm_dma_kernel<128, 128, false>;
+        default: return nullptr;
+    }
+}
+
+}  // namespace isam

@@ -1,0 +1,291 @@
+// bf16 MFMA GEMM fed by direct global->LDS loads (gfx950).
+//
+// Same contraction as the register-staged tile kernel (the paper's first
+// listing), with the HBM -> LDS -> VGPR path of Section 3.5 rebuilt around
+// the CDNA4 data movers:
+//   * buffer_load ... lds (16 bytes per lane) copies A and B tiles straight
+//     into LDS: no staging registers, no ds_write instructions, and copies
+//     for three K tiles ahead are in flight while the MFMAs of the current
+//     tile run (4-stage LDS ring, K depth 32 per stage);
+//   * a copy instruction writes 64 consecutive 16-byte LDS units, so the
+//     bank swizzle is applied by choosing which global chunk each lane
+//     fetches; out-of-range chunks are fetched at an offset past the buffer
+//     end and arrive as zeros;
+//   * A (K-contiguous) is read with ds_read_b128.  B is read with
+//     ds_read_b128 when K-contiguous, and with ds_read_b64_tr_b16 when
+//     N-contiguous: within each 16-lane group that instruction hands lane j
+//     element j%4 of the 8-byte pieces addressed by lanes j/4 + 4e
+//     (e = 0..3), so pieces taken from four consecutive K rows arrive as
+//     four consecutive K values of one column -- the MFMA B operand -- with
+//     no transpose pass.
+// LDS layouts (one stage, bf16):
+//   A / K-contiguous B: row r (64 bytes = 32 K values), logical 16-byte chunk
+//     c at physical chunk c ^ (((r >> 1) ^ (r >> 3)) & 3);
+//   N-contiguous B: K row k (BN*2 bytes), logical 32-byte block b at physical
+//     block b ^ (k & 3).
+// Both make every 8-lane (b128) or 16-lane (b64) read phase hit distinct
+// banks of the 32-bank LDS.
+#pragma once
+
+#include "common.hpp"
+#include "gemm_impl.hpp"
+
+namespace isam {
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+
+__device__ __forceinline__ uint32_t dma_a_off(int r, int c) {
+    return (uint32_t)(r * 64 + ((c ^ (((r >> 1) ^ (r >> 3)) & 3)) << 4));
+}
+
+// The copies are issued with inline assembly so that the compiler, which
+// cannot tell which LDS bytes an in-flight copy will write, does not drain
+// every outstanding copy before each LDS read and barrier.  Completion is
+// tracked explicitly: vm_wait<N>() returns once at most N of this wave's
+// copies are still in flight (they complete in issue order), and
+// block_sync() is a plain workgroup barrier without a memory fence.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, uint32_t lds_addr, uint32_t voff) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(lds_addr), "v"(voff), "s"(rs)
+        : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+__device__ __forceinline__ void block_sync() {
+    asm volatile("" : : : "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" : : : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+template <int BM, int BN, bool TB>
+__global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
+    constexpr int WM = 2, WN = 2, STAGES = 4, BK = 32;
+    constexpr int WTM = BM / WM, WTN = BN / WN, MI = WTM / 32, NI = WTN / 32;
+    constexpr int A_BYTES = BM * 64, B_BYTES = BN * 64, STAGE = A_BYTES + B_BYTES;
+    constexpr int A_INSTR = A_BYTES / 1024 / 4, B_INSTR = B_BYTES / 1024 / 4;  // per wave per tile
+    constexpr int PER_TILE = A_INSTR + B_INSTR;
+    static_assert(A_INSTR >= 1 && B_INSTR >= 1, "tile too small for 4 waves of copies");
+    static_assert(2 * PER_TILE < 64, "vmcnt range");
+    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wm = wid / WN, wn = wid % WN;
+    int tm, tn;
+    map_tile(tmap, tm, tn);
+    const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+    const int split = blockIdx.y;
+    const int64_t kbeg = (int64_t)split * tmap.k_per_split;
+    const int64_t kend = min(a.K, kbeg + tmap.k_per_split);
+    const int nk = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
+
+    const int64_t a_ext = (a.M - 1) * a.lda + a.K;
+    const int64_t b_ext = TB ? ((a.N - 1) * a.ldb + a.K) : ((a.K - 1) * a.ldb + a.N);
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(a_ext * 2));
+    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(a.B, (uint32_t)(b_ext * 2));
+
+    // Per-lane global byte offsets of this wave's copies, relative to tile
+    // origin (row m0 / n0, K index 0 of the tile); -1 marks a chunk outside
+    // the M / N range.  The K position is added per tile.
+    int64_t a_row_off[A_INSTR];
+    int a_k[A_INSTR];
+#pragma unroll
+    for (int q = 0; q < A_INSTR; ++q) {
+        const int unit = (wid * A_INSTR + q) * 64 + lane;  // 16-byte LDS unit within the A region
+        const int r = unit >> 2, pc = unit & 3;
+        const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
+        a_k[q] = c * 8;
+        a_row_off[q] = (m0 + r < a.M) ? (m0 + r) * a.lda : -1;
+    }
+    int64_t b_off[B_INSTR];
+    int b_k[B_INSTR];
+#pragma unroll
+    for (int q = 0; q < B_INSTR; ++q) {
+        const int unit = (wid * B_INSTR + q) * 64 + lane;
+        if constexpr (TB) {
+            const int r = unit >> 2, pc = unit & 3;
+            const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
+            b_k[q] = c * 8;
+            b_off[q] = (n0 + r < a.N) ? (n0 + r) * a.ldb : -1;
+        } else {
+            constexpr int UPR = BN / 8;  // 16-byte units per K row
+            const int k = unit / UPR, u = unit % UPR;
+            const int b = (u >> 1) ^ (k & 3);
+            const int64_t n = n0 + b * 16 + (u & 1) * 8;
+            b_k[q] = k;
+            b_off[q] = (n < a.N) ? n : -1;
+        }
+    }
+
+    auto issue = [&](int tile) {
+        const int stage = tile % STAGES;
+        const int64_t k0 = kbeg + (int64_t)tile * BK;
+        char* sa = smem + stage * STAGE;
+        char* sb = sa + A_BYTES;
+#pragma unroll
+        for (int q = 0; q < A_INSTR; ++q) {
+            const int64_t k = k0 + a_k[q];
+            const uint32_t off = (a_row_off[q] >= 0 && k < kend) ? (uint32_t)((a_row_off[q] + k) * 2) : kOob;
+            dma16(rsA, __builtin_amdgcn_readfirstlane(lds_addr_of(sa + (wid * A_INSTR + q) * 1024)), off);
+        }
+#pragma unroll
+        for (int q = 0; q < B_INSTR; ++q) {
+            uint32_t off;
+            if constexpr (TB) {
+                const int64_t k = k0 + b_k[q];
+                off = (b_off[q] >= 0 && k < kend) ? (uint32_t)((b_off[q] + k) * 2) : kOob;
+            } else {
+                const int64_t k = k0 + b_k[q];
+                off = (b_off[q] >= 0 && k < kend) ? (uint32_t)((k * a.ldb + b_off[q]) * 2) : kOob;
+            }
+            dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(sb + (wid * B_INSTR + q) * 1024)), off);
+        }
+    };
+
+    f32x16_t acc[MI][NI];
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) { acc[i][j][decltype(v)::value] = 0.0f; });
+        });
+    });
+
+    auto compute = [&](int stage) {
+        const char* sa = smem + stage * STAGE;
+        const char* sb = sa + A_BYTES;
+        static_for<2>([&](auto ks) {
+            uint4 af[MI], bfr[NI];
+            const int ch = ks * 2 + (lane >> 5);
+            static_for<MI>([&](auto i) {
+                const int r = wm * WTM + i * 32 + (lane & 31);
+                af[i] = *reinterpret_cast<const uint4*>(sa + dma_a_off(r, ch));
+            });
+            if constexpr (TB) {
+                static_for<NI>([&](auto j) {
+                    const int r = wn * WTN + j * 32 + (lane & 31);
+                    bfr[j] = *reinterpret_cast<const uint4*>(sb + dma_a_off(r, ch));
+                });
+            } else {
+                const int g = lane >> 4, li = lane & 15;
+                static_for<NI>([&](auto j) {
+                    const int n = wn * WTN + j * 32 + (g & 1) * 16 + 4 * (li & 3);
+                    uint32_t w[4];
+                    static_for<2>([&](auto rr) {
+                        const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
+                        const int b = (n >> 4) ^ (k & 3);
+                        const char* p = sb + k * (BN * 2) + b * 32 + (n & 15) * 2;
+                        v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p);
+                        const uint2 u = __builtin_bit_cast(uint2, v);
+                        w[rr * 2 + 0] = u.x;
+                        w[rr * 2 + 1] = u.y;
+                    });
+                    bfr[j] = make_uint4(w[0], w[1], w[2], w[3]);
+                });
+            }
+            static_for<MI>([&](auto i) {
+                static_for<NI>([&](auto j) { mfma32_bf16(acc[i][j], af[i], bfr[j]); });
+            });
+        });
+    };
+
+    if (nk > 0) {
+        issue(0);
+        if (nk > 1) issue(1);
+        if (nk > 2) issue(2);
+        for (int t = 0; t < nk; ++t) {
+            const int pending = min(nk - 1 - t, STAGES - 2);  // tiles issued after t
+            if (pending >= 2) vm_wait<2 * PER_TILE>();
+            else if (pending == 1) vm_wait<PER_TILE>();
+            else vm_wait<0>();
+            block_sync();
+            if (t + STAGES - 1 < nk) issue(t + STAGES - 1);
+            compute(t % STAGES);
+        }
+    }
+    __syncthreads();
+
+    // Epilogue: identical to the register-staged kernel's (LDS-staged vector stores).
+    const bool split_out = gridDim.y > 1;
+    constexpr int EPI_LD = WTN * 4 + 16;
+    static_assert(4 * 32 * EPI_LD <= STAGES * STAGE, "epilogue staging must fit in LDS");
+    char* epi = smem + wid * 32 * EPI_LD;
+    float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
+    const int64_t ldo = split_out ? a.N : a.ldc;
+    const int osz = split_out ? 4 : (a.c_type == kF32 ? 4 : 2);
+    char* obase = split_out ? reinterpret_cast<char*>(P) : static_cast<char*>(a.C);
+    const bool vec_out = ((reinterpret_cast<uintptr_t>(obase) & 15) == 0) && ((ldo * osz) % 16 == 0);
+    constexpr int Q = WTN / 4;
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) {
+                constexpr int vv = decltype(v)::value;
+                const int r = 8 * (vv >> 2) + 4 * (lane >> 5) + (vv & 3);
+                *reinterpret_cast<float*>(epi + r * EPI_LD + (j * 32 + (lane & 31)) * 4) = acc[i][j][vv];
+            });
+        });
+        __syncthreads();
+        const int64_t row0 = m0 + wm * WTM + i * 32;
+        const int64_t col0 = n0 + wn * WTN;
+        for (int q = lane; q < 32 * Q; q += 64) {
+            const int r = q / Q, c4 = q - r * Q;
+            const int64_t row = row0 + r, col = col0 + c4 * 4;
+            if (row >= a.M || col >= a.N) continue;
+            float4 v4 = *reinterpret_cast<const float4*>(epi + r * EPI_LD + c4 * 16);
+            float vals[4] = {v4.x, v4.y, v4.z, v4.w};
+            const int nv = (int)((a.N - col) < 4 ? (a.N - col) : 4);
+            if (!split_out && a.bias) {
+                for (int e = 0; e < nv; ++e) vals[e] += a.bias[col + e];
+            }
+            const int64_t idx = row * ldo + col;
+            if (split_out || a.c_type == kF32) {
+                float* C = reinterpret_cast<float*>(obase);
+                if (nv == 4 && vec_out) {
+                    if (!split_out && a.accumulate) {
+                        float4 c = *reinterpret_cast<const float4*>(C + idx);
+                        vals[0] += c.x; vals[1] += c.y; vals[2] += c.z; vals[3] += c.w;
+                    }
+                    *reinterpret_cast<float4*>(C + idx) = make_float4(vals[0], vals[1], vals[2], vals[3]);
+                } else {
+                    for (int e = 0; e < nv; ++e) {
+                        float val = vals[e];
+                        if (!split_out && a.accumulate) val += C[idx + e];
+                        C[idx + e] = val;
+                    }
+                }
+            } else {
+                uint16_t* C = reinterpret_cast<uint16_t*>(obase);
+                if (nv == 4 && ((reinterpret_cast<uintptr_t>(C + idx) & 7) == 0)) {
+                    if (a.accumulate) {
+                        uint2 c = *reinterpret_cast<const uint2*>(C + idx);
+                        vals[0] += bf16lo(c.x); vals[1] += bf16hi(c.x);
+                        vals[2] += bf16lo(c.y); vals[3] += bf16hi(c.y);
+                    }
+                    *reinterpret_cast<uint2*>(C + idx) =
+                        make_uint2(pack_bf16x2(vals[0], vals[1]), pack_bf16x2(vals[2], vals[3]));
+                } else {
+                    for (int e = 0; e < nv; ++e) {
+                        float val = vals[e];
+                        if (a.accumulate) val += bf16_to_f32(C[idx + e]);
+                        C[idx + e] = (uint16_t)f32_to_bf16(val);
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    });
+}
+
+}  // namespace isam

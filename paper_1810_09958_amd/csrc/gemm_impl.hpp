@@ -10,9 +10,12 @@
 //     global layout is K-contiguous is copied chunk by chunk; one whose
 //     layout is M/N-contiguous is loaded as E x E blocks and transposed in
 //     registers on the way into LDS.
-//   * 16-byte chunk c of LDS row r sits at chunk c ^ ((r >> 1) & 7) so the
-//     MFMA fragment reads (32 rows x 16 bytes per half wave) spread over all
-//     banks.
+//   * 16-byte chunk c of LDS row r sits at chunk c ^ ((r ^ (r >> 3)) & 7):
+//     the fragment reads (consecutive rows, one chunk) and the transposed
+//     stores (rows 8 apart, one chunk) both land on distinct bank groups for
+//     every 8- and 16-lane phase; the transposed stores also alternate the
+//     order of their E rows between lane halves so each phase covers both
+//     128-byte halves of a 256-byte bank line.
 //   * Two LDS stages: the global loads for tile t+1 are issued before the
 //     MFMAs of tile t and written to the other stage after them; one
 //     barrier per K tile.
@@ -33,7 +36,7 @@
 namespace isam {
 
 __device__ __forceinline__ uint32_t lds_off(int r, int c) {
-    return (uint32_t)(r * 128 + ((c ^ ((r >> 1) & 7)) << 4));
+    return (uint32_t)(r * 128 + ((c ^ ((r ^ (r >> 3)) & 7)) << 4));
 }
 
 // Loads one operand tile (ROWS rows of M or N, 128 bytes of K) into
@@ -118,9 +121,17 @@ struct TileLoader {
                 uint4 t[E];
                 if constexpr (E == 8) transpose8x8_b16(&r[u * E], t);
                 else transpose4x4_b32(&r[u * E], t);
-#pragma unroll
-                for (int j = 0; j < E; ++j)
-                    *reinterpret_cast<uint4*>(lds + lds_off(rb * E + j, kb)) = t[j];
+                const int flip = (rb >> 3) & 1;
+                const uint32_t m = 0u - (uint32_t)flip;  // all ones when flipped
+                static_for<E>([&](auto jc) {
+                    constexpr int j = decltype(jc)::value;
+                    // v = flip ? t[j ^ 1] : t[j], as bit operations so the
+                    // register array is never indexed by a run-time value
+                    const uint4 a0 = t[j], a1 = t[j ^ 1];
+                    const uint4 v = make_uint4(a0.x ^ ((a0.x ^ a1.x) & m), a0.y ^ ((a0.y ^ a1.y) & m),
+                                               a0.z ^ ((a0.z ^ a1.z) & m), a0.w ^ ((a0.w ^ a1.w) & m));
+                    *reinterpret_cast<uint4*>(lds + lds_off(rb * E + (j ^ flip), kb)) = v;
+                });
             }
         }
     }
@@ -169,8 +180,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, Til
     const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(a_ext * (int64_t)sizeof(T)));
     const __amdgpu_buffer_rsrc_t rsB = make_rsrc(a.B, (uint32_t)(b_ext * (int64_t)sizeof(T)));
 
-    TileLoader<T, BM, NT, !TA, VEC> la;
-    TileLoader<T, BN, NT, TB, VEC> lb;
+    TileLoader<T, BM, NT, !TA, VEC> la0;
+    TileLoader<T, BN, NT, TB, VEC> lb0;
 
     f32x16_t acc[MI][NI];
     static_for<MI>([&](auto i) {
@@ -179,42 +190,45 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, Til
         });
     });
 
-    if (nk > 0) {
-        la.load(rsA, tid, m0, kbeg, a.M, kend, a.lda);
-        lb.load(rsB, tid, n0, kbeg, a.N, kend, a.ldb);
-        la.store(smem, tid);
-        lb.store(smem + BM * 128, tid);
-        __syncthreads();
-        for (int t = 0; t < nk; ++t) {
-            char* cur = smem + (t & 1) * STAGE;
-            char* nxt = smem + ((t + 1) & 1) * STAGE;
-            const bool more = t + 1 < nk;
-            if (more) {
-                la.load(rsA, tid, m0, kbeg + (int64_t)(t + 1) * BK, a.M, kend, a.lda);
-                lb.load(rsB, tid, n0, kbeg + (int64_t)(t + 1) * BK, a.N, kend, a.ldb);
-            }
-            const char* As = cur;
-            const char* Bs = cur + BM * 128;
-            static_for<4>([&](auto ks) {
-                uint4 af[MI], bfr[NI];
-                const int ch = ks * 2 + (lane >> 5);
-                static_for<MI>([&](auto i) {
-                    af[i] = *reinterpret_cast<const uint4*>(As + lds_off(wm * WTM + i * 32 + (lane & 31), ch));
-                });
+    auto gload = [&](auto& la, auto& lb, int tile) {
+        const int64_t k0 = kbeg + (int64_t)tile * BK;
+        la.load(rsA, tid, m0, k0, a.M, kend, a.lda);
+        lb.load(rsB, tid, n0, k0, a.N, kend, a.ldb);
+    };
+    auto lstore = [&](const auto& la, const auto& lb, int stage) {
+        la.store(smem + stage * STAGE, tid);
+        lb.store(smem + stage * STAGE + BM * 128, tid);
+    };
+    auto compute = [&](int stage) {
+        const char* As = smem + stage * STAGE;
+        const char* Bs = As + BM * 128;
+        static_for<4>([&](auto ks) {
+            uint4 af[MI], bfr[NI];
+            const int ch = ks * 2 + (lane >> 5);
+            static_for<MI>([&](auto i) {
+                af[i] = *reinterpret_cast<const uint4*>(As + lds_off(wm * WTM + i * 32 + (lane & 31), ch));
+            });
+            static_for<NI>([&](auto j) {
+                bfr[j] = *reinterpret_cast<const uint4*>(Bs + lds_off(wn * WTN + j * 32 + (lane & 31), ch));
+            });
+            static_for<MI>([&](auto i) {
                 static_for<NI>([&](auto j) {
-                    bfr[j] = *reinterpret_cast<const uint4*>(Bs + lds_off(wn * WTN + j * 32 + (lane & 31), ch));
-                });
-                static_for<MI>([&](auto i) {
-                    static_for<NI>([&](auto j) {
-                        if constexpr (sizeof(T) == 2) mfma32_bf16(acc[i][j], af[i], bfr[j]);
-                        else mfma32_f32x4(acc[i][j], af[i], bfr[j]);
-                    });
+                    if constexpr (sizeof(T) == 2) mfma32_bf16(acc[i][j], af[i], bfr[j]);
+                    else mfma32_f32x4(acc[i][j], af[i], bfr[j]);
                 });
             });
-            if (more) {
-                la.store(nxt, tid);
-                lb.store(nxt + BM * 128, tid);
-            }
+        });
+    };
+
+    if (nk > 0) {
+        gload(la0, lb0, 0);
+        lstore(la0, lb0, 0);
+        __syncthreads();
+        for (int t = 0; t < nk; ++t) {
+            const bool more = t + 1 < nk;
+            if (more) gload(la0, lb0, t + 1);
+            compute(t & 1);
+            if (more) lstore(la0, lb0, (t + 1) & 1);
             __syncthreads();
         }
     }

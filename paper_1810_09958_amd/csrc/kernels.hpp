@@ -43,6 +43,7 @@ struct GemmPlan {
     int64_t k_per_split;  // multiple of the tile K depth
     int group_m;     // tile-row group size of the rasterisation
     int xcd_remap;   // spread consecutive tiles of one group over one XCD
+    int dma;         // 1: direct-to-LDS kernel where it applies (bf16, A K-contiguous, vec)
 };
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk);
