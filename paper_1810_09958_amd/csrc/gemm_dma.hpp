@@ -5,8 +5,9 @@
 // the CDNA4 data movers:
 //   * buffer_load ... lds (16 bytes per lane) copies A and B tiles straight
 //     into LDS: no staging registers, no ds_write instructions, and copies
-//     for three K tiles ahead are in flight while the MFMAs of the current
-//     tile run (4-stage LDS ring, K depth 32 per stage);
+//     for up to three K tiles ahead are in flight while the MFMAs of the
+//     current tile run (4-stage LDS ring, K depth 32 per stage), and LDS
+//     fragment reads run one K step ahead of the MFMAs;
 //   * a copy instruction writes 64 consecutive 16-byte LDS units, so the
 //     bank swizzle is applied by choosing which global chunk each lane
 //     fetches; out-of-range chunks are fetched at an offset past the buffer
@@ -163,56 +164,128 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a, TileMapArgs t
         });
     });
 
-    auto compute = [&](int stage) {
+    // Fragments of one 16-deep K step: MI A blocks and NI B blocks (32x32 each).
+    struct Frag {
+        uint4 a[MI], b[NI];
+    };
+    constexpr int B_READS = TB ? 1 : 2;               // LDS reads per B block
+    constexpr int N_READS = MI + NI * B_READS;        // LDS reads per fragment set
+    // Issue read number `idx` of fragment set f (stage, K step ks).
+    auto read_part = [&](Frag& f, int stage, int ks, auto idx_c) {
+        constexpr int idx = decltype(idx_c)::value;
         const char* sa = smem + stage * STAGE;
         const char* sb = sa + A_BYTES;
-        static_for<2>([&](auto ks) {
-            uint4 af[MI], bfr[NI];
-            const int ch = ks * 2 + (lane >> 5);
-            static_for<MI>([&](auto i) {
-                const int r = wm * WTM + i * 32 + (lane & 31);
-                af[i] = *reinterpret_cast<const uint4*>(sa + dma_a_off(r, ch));
-            });
-            if constexpr (TB) {
-                static_for<NI>([&](auto j) {
-                    const int r = wn * WTN + j * 32 + (lane & 31);
-                    bfr[j] = *reinterpret_cast<const uint4*>(sb + dma_a_off(r, ch));
-                });
-            } else {
-                const int g = lane >> 4, li = lane & 15;
-                static_for<NI>([&](auto j) {
-                    const int n = wn * WTN + j * 32 + (g & 1) * 16 + 4 * (li & 3);
-                    uint32_t w[4];
-                    static_for<2>([&](auto rr) {
-                        const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
-                        const int b = (n >> 4) ^ (k & 3);
-                        const char* p = sb + k * (BN * 2) + b * 32 + (n & 15) * 2;
-                        v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p);
-                        const uint2 u = __builtin_bit_cast(uint2, v);
-                        w[rr * 2 + 0] = u.x;
-                        w[rr * 2 + 1] = u.y;
-                    });
-                    bfr[j] = make_uint4(w[0], w[1], w[2], w[3]);
-                });
-            }
-            static_for<MI>([&](auto i) {
-                static_for<NI>([&](auto j) { mfma32_bf16(acc[i][j], af[i], bfr[j]); });
-            });
+        const int ch = ks * 2 + (lane >> 5);
+        if constexpr (idx < MI) {
+            const int r = wm * WTM + idx * 32 + (lane & 31);
+            f.a[idx] = *reinterpret_cast<const uint4*>(sa + dma_a_off(r, ch));
+        } else if constexpr (TB) {
+            constexpr int j = idx - MI;
+            const int r = wn * WTN + j * 32 + (lane & 31);
+            f.b[j] = *reinterpret_cast<const uint4*>(sb + dma_a_off(r, ch));
+        } else {
+            constexpr int j = (idx - MI) / 2, rr = (idx - MI) % 2;
+            const int g = lane >> 4, li = lane & 15;
+            const int n = wn * WTN + j * 32 + (g & 1) * 16 + 4 * (li & 3);
+            const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
+            const int b = (n >> 4) ^ (k & 3);
+            const char* p = sb + k * (BN * 2) + b * 32 + (n & 15) * 2;
+            v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p);
+            const uint2 u = __builtin_bit_cast(uint2, v);
+            if constexpr (rr == 0) { f.b[j].x = u.x; f.b[j].y = u.y; }
+            else { f.b[j].z = u.x; f.b[j].w = u.y; }
+        }
+    };
+    auto read_all = [&](Frag& f, int stage, int ks) {
+        static_for<N_READS>([&](auto idx) { read_part(f, stage, ks, idx); });
+    };
+    // Copies of one K tile, one instruction at a time (A first, then B).
+    auto issue_part = [&](int tile, auto q_c) {
+        constexpr int q = decltype(q_c)::value;
+        const int stage = tile % STAGES;
+        const int64_t k0 = kbeg + (int64_t)tile * BK;
+        char* sa = smem + stage * STAGE;
+        char* sb = sa + A_BYTES;
+        if constexpr (q < A_INSTR) {
+            const int64_t k = k0 + a_k[q];
+            const uint32_t off = (a_row_off[q] >= 0 && k < kend) ? (uint32_t)((a_row_off[q] + k) * 2) : kOob;
+            dma16(rsA, __builtin_amdgcn_readfirstlane(lds_addr_of(sa + (wid * A_INSTR + q) * 1024)), off);
+        } else {
+            constexpr int qb = q - A_INSTR;
+            const int64_t k = k0 + b_k[qb];
+            uint32_t off;
+            if constexpr (TB) off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((b_off[qb] + k) * 2) : kOob;
+            else off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((k * a.ldb + b_off[qb]) * 2) : kOob;
+            dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(sb + (wid * B_INSTR + qb) * 1024)), off);
+        }
+    };
+    // MI*NI MFMAs of fragment set f; after MFMA number k the side operation
+    // side(k) is issued, so loads and copies go out while the matrix core is
+    // busy instead of between MFMA groups.  sched_barrier pins the order.
+    auto mfma_with = [&](const Frag& f, auto&& side) {
+        static_for<MI * NI>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            mfma32_bf16(acc[k / NI][k % NI], f.a[k / NI], f.b[k % NI]);
+            side(kc);
+            __builtin_amdgcn_sched_barrier(0);
         });
     };
 
+    // Per K tile t (stage t % 4):
+    //   MFMAs ks=0 of t   + reads of ks=1 of t
+    //   wait for tile t+1's copies, barrier
+    //   MFMAs ks=1 of t   + reads of ks=0 of t+1, copies of tile t+3 (into
+    //                       the stage tile t-1 used)
     if (nk > 0) {
-        issue(0);
-        if (nk > 1) issue(1);
-        if (nk > 2) issue(2);
+        static_for<3>([&](auto pc) {
+            constexpr int p = decltype(pc)::value;
+            if (p < nk) static_for<PER_TILE>([&](auto q) { issue_part(p, q); });
+        });
+        if (nk > 2) vm_wait<2 * PER_TILE>();
+        else if (nk > 1) vm_wait<PER_TILE>();
+        else vm_wait<0>();
+        block_sync();
+        Frag f0, f1;
+        read_all(f0, 0, 0);
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): nothing pending at the loop head
         for (int t = 0; t < nk; ++t) {
-            const int pending = min(nk - 1 - t, STAGES - 2);  // tiles issued after t
-            if (pending >= 2) vm_wait<2 * PER_TILE>();
-            else if (pending == 1) vm_wait<PER_TILE>();
-            else vm_wait<0>();
-            block_sync();
-            if (t + STAGES - 1 < nk) issue(t + STAGES - 1);
-            compute(t % STAGES);
+            const int st = t % STAGES;
+            __builtin_amdgcn_sched_barrier(0);
+            mfma_with(f0, [&](auto kc) {
+                constexpr int k = decltype(kc)::value;
+                constexpr int S = MI * NI;
+                constexpr int lo = (k * N_READS + S - 1) / S, hi = ((k + 1) * N_READS + S - 1) / S;
+                static_for<hi - lo>([&](auto d) {
+                    read_part(f1, st, 1, std::integral_constant<int, lo + decltype(d)::value>{});
+                });
+            });
+            const bool more = t + 1 < nk;
+            if (more) {
+                if (t + 2 < nk) vm_wait<PER_TILE>();  // tiles issued after t+1: only t+2
+                else vm_wait<0>();
+                block_sync();
+            }
+            const bool next_copy = t + 3 < nk;
+            const int nst = (t + 1) % STAGES;
+            // Reads of ks=0 of t+1 are unconditional (after the last tile they
+            // read an idle stage and are unused) so every path reaching the
+            // MFMAs has the same LDS requests in flight.
+            mfma_with(f1, [&](auto kc) {
+                // N_READS reads then PER_TILE copies, spread evenly over the
+                // MI*NI MFMA slots (slot k issues ops [k*NOPS/S, (k+1)*NOPS/S)).
+                constexpr int k = decltype(kc)::value;
+                constexpr int S = MI * NI, NOPS = N_READS + PER_TILE;
+                constexpr int lo = (k * NOPS + S - 1) / S, hi = ((k + 1) * NOPS + S - 1) / S;
+                static_for<hi - lo>([&](auto d) {
+                    constexpr int o = lo + decltype(d)::value;
+                    if constexpr (o < N_READS) read_part(f0, nst, 0, std::integral_constant<int, o>{});
+                    else if (next_copy) issue_part(t + 3, std::integral_constant<int, o - N_READS>{});
+                });
+            });
+            // The next K step's fragments were requested during these MFMAs;
+            // waiting here tells the compiler nothing is pending at the loop
+            // head, which keeps it from draining reads it does not need.
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
         }
     }
     __syncthreads();
