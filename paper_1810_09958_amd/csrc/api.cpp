@@ -372,7 +372,7 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
     if (T < 0 || batch <= 0 || hidden_size <= 0 || !valid_dtype(w_type)) return 0;
     const size_t gx = align256((size_t)T * (size_t)batch * 3 * (size_t)hidden_size * sizeof(float));
     const size_t hb = align256(2 * (size_t)batch * (size_t)hidden_size * dsize(w_type));
-    return gx + hb + 256;
+    return gx + hb + 4096;
 }
 
 }  // extern "C"
@@ -442,7 +442,15 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     }
     if (!J) return fail(ISAM_ERR_UNSUPPORTED, "%s: no resident tiling for hidden=%lld batch=%lld on %d CUs",
                         who, (long long)H, (long long)batch, cus);
+    if (const char* env = getenv("ISAM_GRU_J")) {  // tuning override, ignored when it does not fit
+        const int v = atoi(env);
+        if (v >= 1 && v <= 16 && H % v == 0 && v * BB <= 256 && (H / v) * n_bg <= cus &&
+            gru_lds_bytes(w_type, H, v) <= (size_t)lds_max)
+            J = v;
+    }
     const int n_wg = (int)((H / J) * n_bg);
+    if (n_wg > 992)  // the barrier area holds 62 group counters of 16 workgroups
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: %d workgroups exceed the barrier area", who, n_wg);
     if (log_enabled())
         fprintf(stderr, "[isam] gru T=%lld B=%lld I=%lld H=%lld w=%d J=%d BB=%d wgs=%d lds=%zu\n", (long long)T,
                 (long long)batch, (long long)I, (long long)H, w_type, J, BB, n_wg, gru_lds_bytes(w_type, H, J));

@@ -31,28 +31,51 @@ namespace isam {
 namespace {
 
 constexpr int kWaves = 4;
+constexpr int kSyncWords = 1024;  // barrier area: 4 KiB of the workspace
 // Upper bound on one barrier wait, in ticks of the 100 MHz constant clock.
 constexpr uint64_t kBarrierTimeoutTicks = 200000000ull;  // 2 s
 
 __device__ __forceinline__ int gru_rows(int J) { return ((3 * J + 15) / 16) * 16; }
 
-__device__ __forceinline__ void grid_barrier(unsigned* ctr, unsigned target, unsigned* err) {
+// Cross-workgroup exchange of h and the step barrier.
+//
+// h_{t-1} travels between workgroups (and XCDs, whose L2 caches are not
+// coherent with each other) through device-scope (sc1) buffer stores and
+// loads: stores write through to the device coherence point and loads are
+// served from it, so no L2 write-back or invalidation is needed per step.
+// __syncthreads() waits for each thread's stores to complete (vmcnt(0))
+// before the workgroup signals arrival.
+//
+// The barrier is two-level to limit serialised atomics on one address:
+// workgroups arrive on a counter of their group of kGroup, the last arrival
+// of a group bumps the global counter, and every workgroup polls the global
+// counter.  All counters are monotonic over the steps of one launch (zeroed
+// by the init kernel).  Each wait is bounded in time; a timeout sets the
+// sticky error word, after which every wait returns at once.
+constexpr int kGroup = 16;
+constexpr int kSyncGlobal = 0, kSyncError = 16, kSyncGroups = 32;  // word offsets, 64-byte apart
+constexpr int kCpolDevice = 16;                                    // sc1: device-scope coherence
+
+__device__ __forceinline__ void grid_barrier(unsigned* sync, int64_t step) {
     __syncthreads();
     if (threadIdx.x == 0) {
-        __threadfence();
-        atomicAdd(ctr, 1u);
+        const int G = gridDim.x, g = blockIdx.x / kGroup;
+        const int n_groups = (G + kGroup - 1) / kGroup;
+        const unsigned gsize = (unsigned)min(kGroup, G - g * kGroup);
+        const unsigned old = __hip_atomic_fetch_add(sync + kSyncGroups + 16 * g, 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        if (old + 1 == (unsigned)(step + 1) * gsize)
+            __hip_atomic_fetch_add(sync + kSyncGlobal, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned target = (unsigned)(step + 1) * (unsigned)n_groups;
         const uint64_t start = wall_clock64();
-        // A timed-out wait sets the sticky error flag; every later wait sees
-        // it and returns at once, so the grid always drains.
-        while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target &&
-               __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
-            __builtin_amdgcn_s_sleep(1);
+        while (__hip_atomic_load(sync + kSyncGlobal, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target &&
+               __hip_atomic_load(sync + kSyncError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+            __builtin_amdgcn_s_sleep(2);
             if (wall_clock64() - start > kBarrierTimeoutTicks) {
-                atomicOr(err, 1u);
+                __hip_atomic_fetch_or(sync + kSyncError, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 break;
             }
         }
-        __threadfence();
     }
     __syncthreads();
 }
@@ -68,7 +91,8 @@ __global__ void gru_init_kernel(GruArgs a) {
         if constexpr (sizeof(T) == 2) static_cast<uint16_t*>(a.hbuf)[i] = (uint16_t)f32_to_bf16(v);
         else static_cast<float*>(a.hbuf)[i] = v;
     }
-    if (blockIdx.x == 0 && threadIdx.x < 32) a.sync[threadIdx.x] = 0u;
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < kSyncWords; i += blockDim.x) a.sync[i] = 0u;
 }
 
 template <typename T>
@@ -118,27 +142,57 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
     __syncthreads();
 
     const int KG = (int)((H * (int64_t)sizeof(T) + 63) / 64);  // 64-byte K groups
+    // Wave w owns the contiguous K groups [kg_lo, kg_hi).
+    const int kg_lo = (KG * wid) / kWaves, kg_hi = (KG * (wid + 1)) / kWaves;
     const int n_col = lane & 15, quarter = lane >> 4;
     const bool col_ok = n_col < nb;
     const int64_t hb_row = b0 + n_col;
 
+    // Input-projection values of the owned (b, j) for the next step, fetched
+    // one step ahead so their latency hides behind the barrier.
+    float gx_r = 0.f, gx_z = 0.f, gx_n = 0.f;
+    auto fetch_gx = [&](int64_t t) {
+        if (owner && t < a.T) {
+            const float* gx = a.gx + (t * B + bb) * 3 * H;
+            gx_r = gx[j];
+            gx_z = gx[H + j];
+            gx_n = gx[2 * H + j];
+        }
+    };
+    fetch_gx(0);
+
+    constexpr int kBatch = 8;  // h chunks requested together per lane
+    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)(2 * B * H * (int64_t)sizeof(T)));
     for (int64_t t = 0; t < a.T; ++t) {
-        const T* hcur = static_cast<const T*>(a.hbuf) + (t & 1) * B * H;
+        const int64_t hcur_off = (t & 1) * B * H;  // element offset of h_{t-1} in hbuf
         f32x4_t acc[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) acc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int kg = wid; kg < KG; kg += kWaves) {
-            const int chunk = kg * 4 + quarter;
-            const int64_t k = (int64_t)chunk * E;
-            uint4 hv = make_uint4(0, 0, 0, 0);
-            if (col_ok && k < H) hv = *reinterpret_cast<const uint4*>(hcur + hb_row * H + k);
+        for (int kg0 = kg_lo; kg0 < kg_hi; kg0 += kBatch) {
+            // Issue every h load of the batch before the first MFMA needs one.
+            uint4 hv[kBatch];
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                if (m >= MT) break;
-                uint4 uv = make_uint4(0, 0, 0, 0);
-                if (k < H) uv = *reinterpret_cast<const uint4*>(u_lds + (m * 16 + n_col) * row_bytes + chunk * 16);
-                if constexpr (sizeof(T) == 2) mfma16_bf16(acc[m], uv, hv);
-                else mfma16_f32x4(acc[m], uv, hv);
+            for (int u = 0; u < kBatch; ++u) {
+                const int kg = kg0 + u;
+                const int64_t k = (int64_t)(kg * 4 + quarter) * E;
+                const bool ok = kg < kg_hi && col_ok && k < H;
+                const uint32_t off = ok ? (uint32_t)((hcur_off + hb_row * H + k) * (int64_t)sizeof(T)) : kOob;
+                hv[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs_h, (int)off, 0, kCpolDevice));
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int kg = kg0 + u;
+                if (kg >= kg_hi) break;
+                const int chunk = kg * 4 + quarter;
+                const int64_t k = (int64_t)chunk * E;
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    if (m >= MT) break;
+                    uint4 uv = make_uint4(0, 0, 0, 0);
+                    if (k < H) uv = *reinterpret_cast<const uint4*>(u_lds + (m * 16 + n_col) * row_bytes + chunk * 16);
+                    if constexpr (sizeof(T) == 2) mfma16_bf16(acc[m], uv, hv[u]);
+                    else mfma16_f32x4(acc[m], uv, hv[u]);
+                }
             }
         }
         // acc[m] element v of lane l: local row m*16 + 4*(l/16) + v, batch column l%16
@@ -159,18 +213,20 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
                 for (int w = 0; w < kWaves; ++w) s += red[(w * RT + g * J + jj) * 16 + nn];
                 gh[g] = s;
             }
-            const float* gx = a.gx + (t * B + bb) * 3 * H;
-            const float r = sigmoidf(gx[j] + bias_r + gh[0]);
-            const float z = sigmoidf(gx[H + j] + bias_z + gh[1]);
-            const float n = tanhf(gx[2 * H + j] + bias_n + r * (gh[2] + bias_hn));
+            const float r = sigmoidf(gx_r + bias_r + gh[0]);
+            const float z = sigmoidf(gx_z + bias_z + gh[1]);
+            const float n = tanhf(gx_n + bias_n + r * (gh[2] + bias_hn));
             const float h = (1.0f - z) * n + z * h_prev;
             h_prev = h;
             if (a.h_seq) a.h_seq[(t * B + bb) * H + j] = h;
-            T* hnext = static_cast<T*>(a.hbuf) + ((t + 1) & 1) * B * H;
-            if constexpr (sizeof(T) == 2) reinterpret_cast<uint16_t*>(hnext)[bb * H + j] = (uint16_t)f32_to_bf16(h);
-            else hnext[bb * H + j] = h;
+            const int64_t hn = ((t + 1) & 1) * B * H + bb * H + j;
+            if constexpr (sizeof(T) == 2)
+                __builtin_amdgcn_raw_buffer_store_b16((unsigned short)f32_to_bf16(h), rs_h, (int)(hn * 2), 0, kCpolDevice);
+            else
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), rs_h, (int)(hn * 4), 0, kCpolDevice);
         }
-        if (t + 1 < a.T) grid_barrier(a.sync, (unsigned)((t + 1) * gridDim.x), a.sync + 16);
+        fetch_gx(t + 1);
+        if (t + 1 < a.T) grid_barrier(a.sync, t);
     }
     if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
 }

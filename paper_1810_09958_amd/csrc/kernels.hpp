@@ -71,7 +71,7 @@ struct GruArgs {
     float* h_seq;           // [T][batch][H] or null
     float* h_T;             // [batch][H] or null
     void* hbuf;             // 2 x [batch][H] in w_type: MFMA copy of h_{t-1}
-    unsigned* sync;         // barrier counter + error flag (2 x 64 bytes)
+    unsigned* sync;         // barrier counters and error word (4 KiB, zeroed by the launch)
     int units_per_wg;       // J
     int batch_per_wg;       // BB
     int n_wg;
