@@ -372,7 +372,7 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
     if (T < 0 || batch <= 0 || hidden_size <= 0 || !valid_dtype(w_type)) return 0;
     const size_t gx = align256((size_t)T * (size_t)batch * 3 * (size_t)hidden_size * sizeof(float));
     const size_t hb = align256(2 * (size_t)batch * (size_t)hidden_size * dsize(w_type));
-    return gx + hb + 4096;
+    return gx + hb + kGruSyncBytes;
 }
 
 }  // extern "C"
@@ -433,24 +433,36 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     int lds_max = 0;
     e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (e != hipSuccess) return hip_fail(e, who);
+    // Units per workgroup: the smallest power of two whose grid fits one
+    // workgroup per CU (measured faster than packing two per CU); if none
+    // does, the smallest that fits at the occupancy limit.  Batch groups
+    // have separate barriers.
     int J = 0;
-    for (int cand = 1; cand <= 16; cand *= 2) {
-        if (H % cand) continue;
-        if (cand * BB > 256) break;
-        if (gru_lds_bytes(w_type, H, cand) > (size_t)lds_max) break;
-        if ((H / cand) * n_bg <= cus) { J = cand; break; }
+    int n_wg = 0;
+    for (int pass = 0; pass < 2 && !J; ++pass) {
+        for (int cand = 1; cand <= 16; cand *= 2) {
+            if (H % cand) continue;
+            if (cand * BB > 256) break;
+            const size_t lds = gru_lds_bytes(w_type, H, cand);
+            if (lds > (size_t)lds_max) break;
+            const int64_t wgs = (H / cand) * n_bg;
+            const int per_cu = pass == 0 ? 1 : gru_blocks_per_cu(w_type, lds);
+            if (wgs <= (int64_t)cus * per_cu && H / cand <= 31 * 16) { J = cand; n_wg = (int)wgs; break; }
+        }
     }
     if (!J) return fail(ISAM_ERR_UNSUPPORTED, "%s: no resident tiling for hidden=%lld batch=%lld on %d CUs",
                         who, (long long)H, (long long)batch, cus);
     if (const char* env = getenv("ISAM_GRU_J")) {  // tuning override, ignored when it does not fit
         const int v = atoi(env);
-        if (v >= 1 && v <= 16 && H % v == 0 && v * BB <= 256 && (H / v) * n_bg <= cus &&
-            gru_lds_bytes(w_type, H, v) <= (size_t)lds_max)
+        const size_t lds = (v >= 1 && v <= 16) ? gru_lds_bytes(w_type, H, v) : 0;
+        if (v >= 1 && v <= 16 && H % v == 0 && v * BB <= 256 && lds <= (size_t)lds_max &&
+            (H / v) * n_bg <= (int64_t)cus * std::min(2, gru_blocks_per_cu(w_type, lds)) && H / v <= 31 * 16) {
             J = v;
+            n_wg = (int)((H / v) * n_bg);
+        }
     }
-    const int n_wg = (int)((H / J) * n_bg);
-    if (n_wg > 992)  // the barrier area holds 62 group counters of 16 workgroups
-        return fail(ISAM_ERR_UNSUPPORTED, "%s: %d workgroups exceed the barrier area", who, n_wg);
+    if (n_bg > kGruSyncBytes / 4 / 512 - 1)  // one 512-word domain per batch group after the error word's
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: batch %lld needs too many barrier domains", who, (long long)batch);
     if (log_enabled())
         fprintf(stderr, "[isam] gru T=%lld B=%lld I=%lld H=%lld w=%d J=%d BB=%d wgs=%d lds=%zu\n", (long long)T,
                 (long long)batch, (long long)I, (long long)H, w_type, J, BB, n_wg, gru_lds_bytes(w_type, H, J));

@@ -31,7 +31,7 @@ namespace isam {
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kSyncWords = 1024;  // barrier area: 4 KiB of the workspace
+constexpr int kSyncWords = kGruSyncBytes / 4;
 // Upper bound on one barrier wait, in ticks of the 100 MHz constant clock.
 constexpr uint64_t kBarrierTimeoutTicks = 200000000ull;  // 2 s
 
@@ -48,27 +48,31 @@ __device__ __forceinline__ int gru_rows(int J) { return ((3 * J + 15) / 16) * 16
 //
 // The barrier is two-level to limit serialised atomics on one address:
 // workgroups arrive on a counter of their group of kGroup, the last arrival
-// of a group bumps the global counter, and every workgroup polls the global
+// of a group bumps the domain counter, and every workgroup polls the domain
 // counter.  All counters are monotonic over the steps of one launch (zeroed
 // by the init kernel).  Each wait is bounded in time; a timeout sets the
 // sticky error word, after which every wait returns at once.
 constexpr int kGroup = 16;
-constexpr int kSyncGlobal = 0, kSyncError = 16, kSyncGroups = 32;  // word offsets, 64-byte apart
-constexpr int kCpolDevice = 16;                                    // sc1: device-scope coherence
+constexpr int kSyncError = 0;           // word offsets; counters sit 64 bytes apart
+constexpr int kSyncDomainWords = 512;   // per batch group: global counter + group counters
+constexpr int kCpolDevice = 16;         // sc1: device-scope coherence
 
-__device__ __forceinline__ void grid_barrier(unsigned* sync, int64_t step) {
+// Workgroups of one batch group form a barrier domain: batch groups are
+// independent sequences, so they never wait for each other.
+__device__ __forceinline__ void grid_barrier(unsigned* sync, int64_t step, int domain, int member, int n_members) {
     __syncthreads();
     if (threadIdx.x == 0) {
-        const int G = gridDim.x, g = blockIdx.x / kGroup;
-        const int n_groups = (G + kGroup - 1) / kGroup;
-        const unsigned gsize = (unsigned)min(kGroup, G - g * kGroup);
-        const unsigned old = __hip_atomic_fetch_add(sync + kSyncGroups + 16 * g, 1u, __ATOMIC_RELAXED,
+        unsigned* dom = sync + kSyncDomainWords * (1 + domain);
+        const int g = member / kGroup;
+        const int n_groups = (n_members + kGroup - 1) / kGroup;
+        const unsigned gsize = (unsigned)min(kGroup, n_members - g * kGroup);
+        const unsigned old = __hip_atomic_fetch_add(dom + 16 * (1 + g), 1u, __ATOMIC_RELAXED,
                                                     __HIP_MEMORY_SCOPE_AGENT);
         if (old + 1 == (unsigned)(step + 1) * gsize)
-            __hip_atomic_fetch_add(sync + kSyncGlobal, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(dom, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const unsigned target = (unsigned)(step + 1) * (unsigned)n_groups;
         const uint64_t start = wall_clock64();
-        while (__hip_atomic_load(sync + kSyncGlobal, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target &&
+        while (__hip_atomic_load(dom, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target &&
                __hip_atomic_load(sync + kSyncError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
             __builtin_amdgcn_s_sleep(2);
             if (wall_clock64() - start > kBarrierTimeoutTicks) {
@@ -226,7 +230,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), rs_h, (int)(hn * 4), 0, kCpolDevice);
         }
         fetch_gx(t + 1);
-        if (t + 1 < a.T) grid_barrier(a.sync, t);
+        if (t + 1 < a.T) grid_barrier(a.sync, t, bg, ug, n_ug);
     }
     if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
 }
@@ -237,6 +241,18 @@ __global__ void copy_state_kernel(const float* h0, float* hT, int64_t n) {
 }
 
 }  // namespace
+
+int gru_blocks_per_cu(int w_type, size_t lds) {
+    int n = 0;
+    const void* fn = w_type == kBF16 ? reinterpret_cast<const void*>(gru_recurrent_kernel<bf16_t>)
+                                     : reinterpret_cast<const void*>(gru_recurrent_kernel<float>);
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, 64 * kWaves, lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return 1;
+    }
+    return n > 0 ? n : 1;
+}
 
 hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStream_t s) {
     int blocks = (int)((n + 255) / 256);

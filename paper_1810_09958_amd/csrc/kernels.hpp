@@ -71,12 +71,15 @@ struct GruArgs {
     float* h_seq;           // [T][batch][H] or null
     float* h_T;             // [batch][H] or null
     void* hbuf;             // 2 x [batch][H] in w_type: MFMA copy of h_{t-1}
-    unsigned* sync;         // barrier counters and error word (4 KiB, zeroed by the launch)
+    unsigned* sync;         // barrier counters and error word (kGruSyncBytes, zeroed by the launch)
     int units_per_wg;       // J
     int batch_per_wg;       // BB
     int n_wg;
 };
 size_t gru_lds_bytes(int w_type, int64_t H, int J);
+// Resident workgroups of the recurrent kernel per compute unit at this LDS size.
+int gru_blocks_per_cu(int w_type, size_t lds);
+constexpr int kGruSyncBytes = 32768;  // barrier area at the end of the GRU workspace
 hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s);
 // T == 0: h_T = h0 (or zeros when h0 is null).
 hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStream_t s);
