@@ -96,7 +96,7 @@ int device_cus() {
 // ---------------------------------------------------------------------------
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus) {
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool allow_skinny = true) {
     GemmPlan p{};
     p.vec = 1;
     p.k_splits = 1;
@@ -109,6 +109,17 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus) {
         tile_dims(t, ab_type, &bm, &bn, &bk);
         return cdiv(M, bm) * cdiv(N, bn);
     };
+    // N <= 32 with A and B in NN layout streams A through the skinny kernel
+    // (layout and alignment are checked at dispatch; the tile kernel is the
+    // fallback).
+    if (allow_skinny && N <= 32 && K > 0 && N % (ab_type == kBF16 ? 8 : 4) == 0 &&
+        !(getenv("ISAM_GEMM_CONFIG") && strstr(getenv("ISAM_GEMM_CONFIG"), "skinny=0"))) {
+        p.skinny = 1;
+        p.tile = kTile128x32;
+        p.k_per_split = skinny_k_slice(ab_type);
+        p.k_splits = (int)cdiv(K, p.k_per_split);
+        return p;
+    }
     if (N <= 32) {
         p.tile = kTile128x32;
     } else if (tiles(kTile256x256) >= cus) {
@@ -212,12 +223,17 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
                        int c_type, void* C, int64_t ldc, const float* bias, void* workspace,
                        size_t workspace_bytes, hipStream_t stream, const char* who) {
     GemmPlan p = plan_gemm(M, N, K, ab_type, device_cus());
-    const size_t need = gemm_ws_bytes(p, M, N);
-    if (p.k_splits > 1 && (!workspace || workspace_bytes < need)) {
+    p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
+    if (p.skinny && (!p.vec || trans_a || trans_b || K == 0)) {
+        p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
+        p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
+    }
+    if (p.k_splits > 1 && (!workspace || workspace_bytes < gemm_ws_bytes(p, M, N))) {
+        if (p.skinny) p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
         p.k_splits = 1;
         p.k_per_split = K;
+        p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     }
-    p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     if (!p.vec) {
         // The element-wise loader is instantiated for the small tiles only.
         if (p.tile != kTile64x64 && p.tile != kTile128x32) p.tile = kTile64x64;

@@ -41,6 +41,15 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int spli
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+    if (p.skinny) {
+        hipError_t e = launch_skinny(a, p.k_splits, s);
+        if (e != hipSuccess || p.k_splits <= 1) return e;
+        const int64_t total = a.M * a.N;
+        int64_t blocks = (total + 255) / 256;
+        if (blocks > 4096) blocks = 4096;
+        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, p.k_splits);
+        return hipGetLastError();
+    }
     int bm, bn, bk;
     tile_dims(p.tile, a.ab_type, &bm, &bn, &bk);
     GemmKernelFn fn = nullptr;

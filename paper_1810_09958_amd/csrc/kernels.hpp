@@ -44,7 +44,11 @@ struct GemmPlan {
     int group_m;     // tile-row group size of the rasterisation
     int xcd_remap;   // spread consecutive tiles of one group over one XCD
     int dma;         // 1: direct-to-LDS kernel where it applies (bf16, A K-contiguous, vec)
+    int skinny;      // 1: streaming kernel for N <= 32 (k_splits = K slices of skinny_k_slice)
 };
+int64_t skinny_k_slice(int ab_type);
+int skinny_rows_per_wg(int ab_type);
+hipError_t launch_skinny(const GemmArgs& a, int splits, hipStream_t s);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk);
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s);

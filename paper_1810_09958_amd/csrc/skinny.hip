@@ -1,0 +1,223 @@
+// Skinny GEMM, C[M][N] = A[M][K] . B[K][N] with N <= 32: the RNN-batch form of
+// the paper's first listing (GRU-shaped products, Section 6.2.2).  The
+// product is bound by streaming A from HBM once, so the kernel is built
+// around that stream:
+//   * A never touches LDS: each lane loads 64 contiguous bytes of one row per
+//     K group straight into registers in MFMA operand order, and every load
+//     of a wave is issued before its first MFMA (16 x 16 bytes per lane in
+//     flight);
+//   * B's K slice for the workgroup (zero-padded to 32 columns) is copied to
+//     LDS with buffer_load ... lds and read as MFMA B fragments: bf16 with
+//     ds_read_b64_tr_b16 (N-contiguous rows give K-contiguous fragments), fp32
+//     with ds_read_b32;
+//   * 8 waves split the workgroup's K slice; their 32-row partial tiles are
+//     summed through LDS in wave order, and K slices of different
+//     workgroups (split-K) are summed by a separate pass in slice order, so
+//     results are deterministic.
+// Lane l of a wave handles row (l % 32) and K half g = l / 32.  Within a K
+// group of 2*CK values (CK = 32 bf16 or 16 fp32) half g owns
+// [g*CK, g*CK + CK); MFMA number s of the group takes the s-th 16-byte piece
+// (bf16, 8 K values) or, for fp32, piece s/4 element s%4 -- A and B use the
+// same assignment.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace isam {
+namespace {
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+
+constexpr int kSkWaves = 8;
+
+__device__ __forceinline__ void sk_dma16(__amdgpu_buffer_rsrc_t rs, uint32_t lds_addr, uint32_t voff) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(lds_addr), "v"(voff), "s"(rs)
+        : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t sk_lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// bf16 B rows are 64 bytes (two 32-byte blocks); block b of K row k sits at
+// block b ^ ((k >> 1) & 1) so a transpose read of 4 consecutive rows hits 4
+// different bank groups.
+__device__ __forceinline__ uint32_t sk_b16_off(int k, int col) {
+    return (uint32_t)(k * 64 + ((((col >> 4) ^ ((k >> 1) & 1))) << 5) + (col & 15) * 2);
+}
+
+template <typename T, int RT, int KC>
+__global__ __launch_bounds__(64 * kSkWaves) void skinny_kernel(GemmArgs a) {
+    constexpr bool BF = sizeof(T) == 2;
+    constexpr int E = 16 / (int)sizeof(T);    // elements per 16 bytes
+    constexpr int CK = 64 / (int)sizeof(T);   // K values per lane per group
+    constexpr int GK = 2 * CK;                // K values per group
+    constexpr int KW = KC / kSkWaves;         // K values per wave
+    constexpr int NG = KW / GK;               // groups per wave
+    constexpr int ROWB = 32 * (int)sizeof(T); // bytes of one padded B row in LDS
+    constexpr int B_BYTES = KC * ROWB;
+    static_assert(NG >= 1 && KW % GK == 0, "K slice must split into whole groups");
+    static_assert(B_BYTES % (1024 * kSkWaves) == 0, "B slice copy must split evenly");
+    __shared__ __attribute__((aligned(1024))) char smem[B_BYTES];
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int g = lane >> 5, r = lane & 31;
+    const int64_t m0 = (int64_t)blockIdx.x * (32 * RT);
+    const int split = blockIdx.y;
+    const int64_t ks0 = (int64_t)split * KC;  // first K of this workgroup
+
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(((a.M - 1) * a.lda + a.K) * (int64_t)sizeof(T)));
+    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(a.B, (uint32_t)(((a.K - 1) * a.ldb + a.N) * (int64_t)sizeof(T)));
+
+    // 1. Copy B[ks0 .. ks0+KC)[0 .. 32) into LDS (columns >= N and rows >= K read as zero).
+    {
+        constexpr int UNITS_PER_ROW = ROWB / 16;
+        constexpr int INSTR = B_BYTES / 1024 / kSkWaves;
+#pragma unroll
+        for (int q = 0; q < INSTR; ++q) {
+            const int unit = (wid * INSTR + q) * 64 + lane;
+            const int k = unit / UNITS_PER_ROW, pu = unit % UNITS_PER_ROW;
+            int col;
+            if constexpr (BF) {
+                const int pb = pu >> 1;  // physical 32-byte block
+                col = ((pb ^ ((k >> 1) & 1)) << 4) + (pu & 1) * 8;
+            } else {
+                col = pu * 4;
+            }
+            const int64_t kk = ks0 + k;
+            const uint32_t off = (kk < a.K && col < a.N) ? (uint32_t)((kk * a.ldb + col) * (int64_t)sizeof(T)) : kOob;
+            sk_dma16(rsB, __builtin_amdgcn_readfirstlane(sk_lds_addr(smem + (wid * INSTR + q) * 1024)), off);
+        }
+    }
+
+    // 2. Issue every A load of this wave: RT row tiles x NG groups x 4 pieces.
+    uint4 av[RT][NG][4];
+    const int64_t kw0 = ks0 + (int64_t)wid * KW;
+#pragma unroll
+    for (int t = 0; t < RT; ++t) {
+        const int64_t row = m0 + t * 32 + r;
+#pragma unroll
+        for (int q = 0; q < NG; ++q)
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const int64_t k = kw0 + q * GK + g * CK + p * E;
+                const uint32_t off = (row < a.M && k < a.K) ? (uint32_t)((row * a.lda + k) * (int64_t)sizeof(T)) : kOob;
+                av[t][q][p] = buf_load16(rsA, off);
+            }
+    }
+
+    // 3. Wait for this wave's copies (issued before the A loads) and for
+    //    everyone's, then run the MFMAs.
+    {
+        constexpr int N_A = RT * NG * 4;
+        static_assert(N_A < 64, "vmcnt range");
+        asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N_A) : "memory");
+    }
+    // Barrier without a memory fence: the A loads stay in flight (the
+    // compiler waits for each before its first MFMA use).
+    asm volatile("" : : : "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" : : : "memory");
+
+    f32x16_t acc[RT];
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[t][v] = 0.0f;
+
+    const int kl0 = wid * KW;  // wave's first K row inside the LDS slice
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+        if constexpr (BF) {
+            // 4 MFMAs per group; B fragment of MFMA s = K rows kb+s*8 .. +8 of column (lane % 32)
+            const int gq = lane >> 4, li = lane & 15;
+            const int col = (gq & 1) * 16 + 4 * (li & 3);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const int kb = kl0 + q * GK + (gq >> 1) * CK + s * 8;
+                uint32_t w[4];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int k = kb + h * 4 + (li >> 2);
+                    v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(smem + sk_b16_off(k, col)));
+                    const uint2 u = __builtin_bit_cast(uint2, v);
+                    w[2 * h] = u.x;
+                    w[2 * h + 1] = u.y;
+                }
+                const uint4 bfrag = make_uint4(w[0], w[1], w[2], w[3]);
+#pragma unroll
+                for (int t = 0; t < RT; ++t) mfma32_bf16(acc[t], av[t][q][s], bfrag);
+            }
+        } else {
+            // 16 MFMAs per group; MFMA (p, e) takes K = kb + p*4 + e, one value per lane
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int k = kl0 + q * GK + g * CK + p * 4 + e;
+                    const float bv = *reinterpret_cast<const float*>(smem + k * ROWB + r * 4);
+#pragma unroll
+                    for (int t = 0; t < RT; ++t) {
+                        const uint4 x = av[t][q][p];
+                        const uint32_t xe = e == 0 ? x.x : e == 1 ? x.y : e == 2 ? x.z : x.w;
+                        acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(xe), bv, acc[t], 0, 0, 0);
+                    }
+                }
+        }
+    }
+
+    // 4. Sum the 8 waves' tiles through LDS (B slice no longer needed).
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(smem);  // [wave][RT*32][32]
+#pragma unroll
+    for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int row = t * 32 + 8 * (v >> 2) + 4 * g + (v & 3);
+            red[(wid * RT * 32 + row) * 32 + r] = acc[t][v];
+        }
+    __syncthreads();
+    const bool split_out = gridDim.y > 1;
+    for (int o = tid; o < RT * 32 * 32; o += 64 * kSkWaves) {
+        const int row = o >> 5, col = o & 31;
+        float sum = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kSkWaves; ++w) sum += red[(w * RT * 32 + row) * 32 + col];
+        const int64_t gr = m0 + row;
+        if (gr >= a.M || col >= a.N) continue;
+        if (split_out) {
+            a.partial[((int64_t)split * a.M + gr) * a.N + col] = sum;
+        } else {
+            const int64_t idx = gr * a.ldc + col;
+            if (a.bias) sum += a.bias[col];
+            if (a.c_type == kF32) {
+                float* C = static_cast<float*>(a.C);
+                C[idx] = a.accumulate ? C[idx] + sum : sum;
+            } else {
+                uint16_t* C = static_cast<uint16_t*>(a.C);
+                C[idx] = (uint16_t)f32_to_bf16(a.accumulate ? bf16_to_f32(C[idx]) + sum : sum);
+            }
+        }
+    }
+}
+
+}  // namespace
+
+// K depth of one workgroup's slice (the split-K unit) for the skinny kernel.
+int64_t skinny_k_slice(int ab_type) { return ab_type == kBF16 ? 2048 : 1024; }
+int skinny_rows_per_wg(int ab_type) { return ab_type == kBF16 ? 32 : 64; }
+
+hipError_t launch_skinny(const GemmArgs& a, int splits, hipStream_t s) {
+    const int R = skinny_rows_per_wg(a.ab_type);
+    const dim3 grid((unsigned)((a.M + R - 1) / R), (unsigned)splits), block(64 * kSkWaves);
+    if (a.ab_type == kBF16) hipLaunchKernelGGL((skinny_kernel<bf16_t, 1, 2048>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((skinny_kernel<float, 2, 1024>), grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace isam

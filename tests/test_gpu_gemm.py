@@ -154,3 +154,19 @@ def test_config_large_bf16_sampled_rows(which, ct):
     ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), B_h, len(rows), N, K)
     got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
     assert norm_err(got, ref, S) <= TOL_BF16
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("N", [8, 16, 24, 32])
+def test_skinny_shapes(dt, N):
+    # streaming kernel for N <= 32: ragged M, K covering partial and multiple K slices
+    for M, K in [(1, 8), (33, 1000), (100, 2048), (4097, 4104), (257, 6000)]:
+        _run_case(M, N, K, dt, "f32", seed=M + K + N)
+    _run_case(300, N, 3000, dt, "bf16", seed=N)
+
+
+def test_skinny_accumulate_and_fallback_layouts():
+    _run_case(513, 32, 5000, "bf16", "f32", accumulate=True)
+    _run_case(513, 32, 5000, "f32", "f32", accumulate=True)
+    _run_case(300, 32, 2048, "bf16", "f32", ta=1)      # transposed A: tile kernel
+    _run_case(300, 16, 2048, "bf16", "f32", tb=1)      # transposed B: tile kernel
