@@ -67,3 +67,12 @@ def test_config_full_size_sampled_images(variant):
     got = to_host_f64(y[torch.as_tensor(imgs, device="cuda")])
     tol = TOL_F32 if variant == "f32" else TOL_BF16
     assert norm_err(got, Z, S) <= tol
+
+
+@pytest.mark.parametrize("ot", ["f32", "bf16"])
+@pytest.mark.parametrize("C,Co", [(64, 8), (64, 40), (128, 256), (128, 96)])
+def test_fused_path_shapes(ot, C, Co):
+    # bf16 3x3 stride-1 pad-1 shapes taken by the fused depthwise+pointwise kernel:
+    # widths for 4, 2 and 1 rows per tile, heights not a multiple of the rows per tile
+    for (b, H, W) in [(2, 5, 7), (1, 9, 32), (2, 7, 56), (1, 3, 64), (1, 5, 100)]:
+        _case(b, H, W, C, Co, dt="bf16", ot=ot, seed=H * W + C)
