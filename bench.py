@@ -43,11 +43,48 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", default="", help="comma list of component names to run (profiling)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="time plain device copies / fills of known size (HBM reference, counter scaling)")
     return ap.parse_args()
+
+
+def copy_calibration():
+    """Plain torch copies and fills of 256 MiB and 1 GiB: the achieved HBM rate of trivial
+    streaming kernels on this device, and the reference the FETCH_SIZE / WRITE_SIZE counters
+    are scaled by (each copy reads and writes exactly its size)."""
+    import torch
+    dev = torch.device("cuda:0")
+    out = {}
+    for mib in (256, 1024):
+        n = mib * (1 << 20) // 4
+        a = torch.ones(n, device=dev)
+        b = torch.empty(n, device=dev)
+        for _ in range(3):
+            b.copy_(a)
+            b.fill_(2.0)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        R = 10
+        e[0].record()
+        for _ in range(R):
+            b.copy_(a)
+        e[1].record()
+        for _ in range(R):
+            b.fill_(3.0)
+        e[2].record()
+        torch.cuda.synchronize()
+        tc = e[0].elapsed_time(e[1]) / R * 1e-3
+        tf = e[1].elapsed_time(e[2]) / R * 1e-3
+        out[f"copy_{mib}MiB"] = {"us": round(tc * 1e6, 1), "GB/s": round(2 * n * 4 / tc / 1e9, 1)}
+        out[f"fill_{mib}MiB"] = {"us": round(tf * 1e6, 1), "GB/s": round(n * 4 / tf / 1e9, 1)}
+    print(json.dumps({"copy_calibration": out}), flush=True)
 
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: this library has no multi-GPU path "
               "(the kernels are timed on one GPU's share of the work).", file=sys.stderr)

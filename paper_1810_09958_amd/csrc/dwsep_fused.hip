@@ -11,8 +11,8 @@
 //      into LDS with buffer_load ... lds;
 //   2. computes the depthwise result for its pixels in fp32 from LDS (each
 //      thread owns one channel vector of one column and reuses the vertical
-//      window in registers), rounds it to bf16 and stores it as the A tile
-//      [128][C] in LDS;
+//      window in registers; taps are paired for v_dot2_f32_bf16), rounds it
+//      to bf16 and stores it as the A tile [128][C] in LDS;
 //   3. runs the [128 x C] . [C x 256] product on MFMA (A with ds_read_b128,
 //      P with ds_read_b64_tr_b16) and writes the output tile.
 // Supported: bf16 input, 3x3, stride 1, pad 1, depth multiplier 1,
@@ -28,6 +28,7 @@ namespace {
 
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kFBM = 128;     // MFMA rows per workgroup
 constexpr int kFBN = 256;     // output channels per workgroup (padded)
@@ -54,185 +55,264 @@ __device__ __forceinline__ uint32_t f_p_off(int k, int n) {
     return (uint32_t)(k * kPRow + ((((n >> 4) ^ (k & 3))) << 5) + (n & 15) * 2);
 }
 
+template <int N>
+__device__ __forceinline__ void f_vm_wait() {
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+__device__ __forceinline__ void f_vm_wait_rt(int n) {
+    switch (n) {
+        case 0: f_vm_wait<0>(); break;
+        case 1: f_vm_wait<1>(); break;
+        case 2: f_vm_wait<2>(); break;
+        case 3: f_vm_wait<3>(); break;
+        default: f_vm_wait<4>(); break;
+    }
+}
+__device__ __forceinline__ void f_barrier() {
+    asm volatile("" : : : "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" : : : "memory");
+}
+
+constexpr int kFWaves = 8;
+constexpr int kARegion = 32768;        // A tile (<= 128 x 128 bf16), also 8 x 4 KiB store staging
+constexpr int kXBuf = 32768;           // bytes of one input half-tile buffer
+constexpr int kXInstr = kXBuf / 1024 / kFWaves;  // copies per wave per half (4)
+
+// Persistent form: one workgroup per CU walks its tiles (tile = R output rows
+// of one image).  LDS: P [C][256] (copied once) | A [128][C] | two buffers of
+// one channel half of the input tile.  Per tile, all 8 waves in lockstep:
+//   depthwise of channel half 0 -> A     (half 1 of this tile is landing)
+//   wait, barrier; copy half 0 of the next tile
+//   depthwise of channel half 1 -> A
+//   barrier; copy half 1 of the next tile
+//   MFMA [128 x C] . [C x 256]           (next tile's copies land meanwhile)
+//   wait for next half 0, barrier; store this tile from the accumulators
 template <int R, typename TO>
-__global__ __launch_bounds__(256) void dwsep_fused_kernel(DwArgs d, const void* pw, void* out, int64_t C_out,
-                                                          int out_type) {
+__global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, const void* pw, void* out,
+                                                                   int64_t C_out) {
     extern __shared__ __attribute__((aligned(1024))) char smem[];
     const int C = (int)d.C, W = (int)d.W, H = (int)d.H;
-    const int CV = C / 8;                       // 16-byte channel vectors per pixel
-    const int pix_bytes = C * 2;
-    const int xrow_bytes = W * pix_bytes;
-    const int xt_bytes = (R + 2) * xrow_bytes;
-    char* sP = smem;                                  // [C][256] bf16
-    char* sX = smem + C * kPRow;                      // [R+2][W][C] bf16
-    char* sA = sX + ((xt_bytes + 1023) & ~1023);      // [128][C] bf16
+    const int CH = C / 2;                 // channels per half
+    const int UH = CH / 8;                // 16-byte units per pixel per half
+    const int half_bytes = (R + 2) * W * CH * 2;
+    char* sP = smem;                                   // [C][256] bf16
+    char* sA = smem + C * kPRow;                       // [128][C] bf16
+    char* sX0 = sA + kARegion;                         // two [R+2][W][CH] bf16 buffers
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-
-    // Tile: image b, output rows i0 .. i0+R-1.  Consecutive tiles of one
-    // image go to one XCD (dispatch is round robin over the 8 XCDs), so the
-    // halo rows two tiles share are reused from that XCD's L2.
-    int bid = blockIdx.x;
-    const int G = gridDim.x;
-    if ((G & 7) == 0) bid = (bid & 7) * (G >> 3) + (bid >> 3);
+    const int a_row_bytes = C * 2;
     const int tiles_per_img = (H + R - 1) / R;
-    const int b = bid / tiles_per_img, i0 = (bid % tiles_per_img) * R;
+    const int n_tiles = (int)d.batch * tiles_per_img;
 
-    // 1. Copies: P, then the input rows i0-1 .. i0+R.
     const __amdgpu_buffer_rsrc_t rsP = make_rsrc(pw, (uint32_t)(C * C_out * 2));
     const __amdgpu_buffer_rsrc_t rsX = make_rsrc(d.x, (uint32_t)(d.batch * (int64_t)H * W * C * 2));
+
+    // Copy channel half h of tile `tile`'s input rows into buffer h.
+    auto copy_half = [&](int tile, int h) {
+        const int b = tile / tiles_per_img, i0 = (tile % tiles_per_img) * R;
+        char* dst = sX0 + h * kXBuf;
+#pragma unroll
+        for (int qq = 0; qq < kXInstr; ++qq) {
+            const int q = wid * kXInstr + qq;
+            const int unit = q * 64 + lane;              // 16-byte unit of the half tile
+            const int pix = unit / UH, u = unit % UH;    // pixel index within the (R+2) x W rows
+            const int rr = pix / W, x = pix % W;
+            const int ir = i0 - 1 + rr;
+            const bool ok = tile < n_tiles && rr < R + 2 && ir >= 0 && ir < H;
+            const uint32_t off = ok ? (uint32_t)(((((int64_t)b * H + ir) * W + x) * C + h * CH + u * 8) * 2) : kOob;
+            f_dma16(rsX, __builtin_amdgcn_readfirstlane(f_lds_addr(dst + q * 1024)), off);
+        }
+    };
+
+    // Prologue: P once, both halves of the first tile.
     {
-        const int p_instr = C * kPRow / 1024;  // C/2 copies of 1 KiB
-        for (int q = wid; q < p_instr; q += 4) {
-            const int unit = q * 64 + lane;        // 16-byte unit of the P region
+        const int p_instr = C * kPRow / 1024;
+        for (int q = wid; q < p_instr; q += kFWaves) {
+            const int unit = q * 64 + lane;
             const int k = unit / (kPRow / 16), pu = unit % (kPRow / 16);
             const int n = (((pu >> 1) ^ (k & 3)) << 4) + (pu & 1) * 8;
             const uint32_t off = (n < C_out) ? (uint32_t)((k * C_out + n) * 2) : kOob;
             f_dma16(rsP, __builtin_amdgcn_readfirstlane(f_lds_addr(sP + q * 1024)), off);
         }
-        const int x_instr = (xt_bytes + 1023) / 1024;
-        const int64_t row0 = (int64_t)b * H + i0 - 1;  // global image row of tile row 0
-        for (int q = wid; q < x_instr; q += 4) {
-            const int o = q * 1024 + lane * 16;
-            const int tr = o / xrow_bytes;
-            const int64_t ir = i0 - 1 + tr;
-            const bool ok = o < xt_bytes && ir >= 0 && ir < H;
-            const uint32_t off = ok ? (uint32_t)((row0 * xrow_bytes) + o) : kOob;
-            f_dma16(rsX, __builtin_amdgcn_readfirstlane(f_lds_addr(sX + q * 1024)), off);
-        }
     }
+    int tile = blockIdx.x;
+    copy_half(tile, 0);
+    copy_half(tile, 1);
+    f_vm_wait<0>();
+    f_barrier();
 
-    // Depthwise filter of this thread's channel vector, fp32 (taps di*3+dj).
-    const int cv = tid % CV;
-    const int jstep = 256 / CV;
-    float wv[9][8];
-    {
-        const uint16_t* wp = static_cast<const uint16_t*>(d.w);
+    // Depthwise of one channel half into the A tile: item = (column j, unit u).
+    const uint16_t* wp = static_cast<const uint16_t*>(d.w);
+    auto depthwise_half = [&](int h) {
+        const char* xs = sX0 + h * kXBuf;
+        for (int item = tid; item < W * UH; item += 64 * kFWaves) {
+            const int j = item / UH, u = item % UH;
+            const int cv = h * UH + u;                   // channel vector within C
+            // Taps (di, 0) and (di, 1) of channel c are paired as bf16x2 for
+            // v_dot2_f32_bf16; tap (di, 2) is applied with an fp32 FMA.  The
+            // input pairs of each row are built once and shared by the output
+            // rows that use it.
+            uint32_t w01[3][8];
+            float w2[3][8];
 #pragma unroll
-        for (int tap = 0; tap < 9; ++tap) {
-            const uint4 v = *reinterpret_cast<const uint4*>(wp + tap * C + cv * 8);
-            wv[tap][0] = bf16lo(v.x); wv[tap][1] = bf16hi(v.x); wv[tap][2] = bf16lo(v.y); wv[tap][3] = bf16hi(v.y);
-            wv[tap][4] = bf16lo(v.z); wv[tap][5] = bf16hi(v.z); wv[tap][6] = bf16lo(v.w); wv[tap][7] = bf16hi(v.w);
-        }
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // every copy of this wave has landed
-    __syncthreads();
-
-    // 2. Depthwise into the A tile.  Rows R*W .. 127 of the tile are zero.
-    const int a_row_bytes = C * 2;
-    // every (column, channel vector) pair has exactly one owner thread
-    for (int j = tid / CV; tid < CV * jstep && j < W; j += jstep) {
-        float col[R + 2][3][8];
+            for (int di = 0; di < 3; ++di) {
+                const uint4 t0 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 0) * C + cv * 8);
+                const uint4 t1 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 1) * C + cv * 8);
+                const uint4 t2 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 2) * C + cv * 8);
+                const uint32_t a0[4] = {t0.x, t0.y, t0.z, t0.w}, a1[4] = {t1.x, t1.y, t1.z, t1.w},
+                               a2[4] = {t2.x, t2.y, t2.z, t2.w};
 #pragma unroll
-        for (int rr = 0; rr < R + 2; ++rr)
-#pragma unroll
-            for (int dj = 0; dj < 3; ++dj) {
-                const int x = j + dj - 1;
-                if (x >= 0 && x < W) {
-                    const uint4 v = *reinterpret_cast<const uint4*>(sX + rr * xrow_bytes + x * pix_bytes + cv * 16);
-                    col[rr][dj][0] = bf16lo(v.x); col[rr][dj][1] = bf16hi(v.x);
-                    col[rr][dj][2] = bf16lo(v.y); col[rr][dj][3] = bf16hi(v.y);
-                    col[rr][dj][4] = bf16lo(v.z); col[rr][dj][5] = bf16hi(v.z);
-                    col[rr][dj][6] = bf16lo(v.w); col[rr][dj][7] = bf16hi(v.w);
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) col[rr][dj][e] = 0.0f;
+                for (int q = 0; q < 4; ++q) {
+                    w01[di][2 * q] = (a0[q] & 0xffffu) | (a1[q] << 16);
+                    w01[di][2 * q + 1] = (a0[q] >> 16) | (a1[q] & 0xffff0000u);
+                    w2[di][2 * q] = bf16lo(a2[q]);
+                    w2[di][2 * q + 1] = bf16hi(a2[q]);
                 }
             }
+            uint32_t pr[3][8];  // sliding window of rows: (x=j-1, x=j) pairs per channel
+            float sg[3][8];     // x=j+1 values per channel
+            auto load_row = [&](int rr, int slot) {
+                uint4 v[3];
 #pragma unroll
-        for (int rl = 0; rl < R; ++rl) {
-            float acc[8];
+                for (int dj = 0; dj < 3; ++dj) {
+                    const int x = j + dj - 1;
+                    v[dj] = (x >= 0 && x < W) ? *reinterpret_cast<const uint4*>(xs + ((rr * W + x) * UH + u) * 16)
+                                              : make_uint4(0, 0, 0, 0);
+                }
+                const uint32_t b0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, b1[4] = {v[1].x, v[1].y, v[1].z, v[1].w},
+                               b2[4] = {v[2].x, v[2].y, v[2].z, v[2].w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+                for (int q = 0; q < 4; ++q) {
+                    pr[slot][2 * q] = (b0[q] & 0xffffu) | (b1[q] << 16);
+                    pr[slot][2 * q + 1] = (b0[q] >> 16) | (b1[q] & 0xffff0000u);
+                    sg[slot][2 * q] = bf16lo(b2[q]);
+                    sg[slot][2 * q + 1] = bf16hi(b2[q]);
+                }
+            };
+            load_row(0, 0);
+            load_row(1, 1);
 #pragma unroll
-            for (int di = 0; di < 3; ++di)
+            for (int rl = 0; rl < R; ++rl) {
+                load_row(rl + 2, (rl + 2) % 3);
+                float acc[8];
 #pragma unroll
-                for (int dj = 0; dj < 3; ++dj)
+                for (int c = 0; c < 8; ++c) {
+                    float a = 0.0f;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) acc[e] = fmaf(col[rl + di][dj][e], wv[di * 3 + dj][e], acc[e]);
-            const int px = rl * W + j;
-            // rows past the image bottom are computed from zero input and never stored
-            *reinterpret_cast<uint4*>(sA + f_a_off(px, cv, a_row_bytes)) =
-                make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
-                           pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
-        }
-    }
-    for (int q = R * W * CV + tid; q < kFBM * CV; q += 256)
-        *reinterpret_cast<uint4*>(sA + f_a_off(q / CV, q % CV, a_row_bytes)) = make_uint4(0, 0, 0, 0);
-    __syncthreads();
-
-    // 3. MFMA: waves 2x2 over the 128 x 256 tile, 64 x 128 each.
-    constexpr int MI = 2, NI = 4;
-    const int wm = wid >> 1, wn = wid & 1;
-    f32x16_t acc[MI][NI];
-    static_for<MI>([&](auto i) {
-        static_for<NI>([&](auto jj) {
-            static_for<16>([&](auto v) { acc[i][jj][decltype(v)::value] = 0.0f; });
-        });
-    });
-    const int g = lane >> 4, li = lane & 15;
-    for (int ks = 0; ks < C / 16; ++ks) {
-        uint4 af[MI], bfr[NI];
-        const int ch = ks * 2 + (lane >> 5);
-        static_for<MI>([&](auto i) {
-            af[i] = *reinterpret_cast<const uint4*>(sA + f_a_off(wm * 64 + i * 32 + (lane & 31), ch, a_row_bytes));
-        });
-        static_for<NI>([&](auto jj) {
-            const int n = wn * 128 + jj * 32 + (g & 1) * 16 + 4 * (li & 3);
-            uint32_t w[4];
-            static_for<2>([&](auto rr) {
-                const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
-                v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(sP + f_p_off(k, n)));
-                const uint2 u = __builtin_bit_cast(uint2, v);
-                w[rr * 2] = u.x;
-                w[rr * 2 + 1] = u.y;
-            });
-            bfr[jj] = make_uint4(w[0], w[1], w[2], w[3]);
-        });
-        static_for<MI>([&](auto i) {
-            static_for<NI>([&](auto jj) { mfma32_bf16(acc[i][jj], af[i], bfr[jj]); });
-        });
-    }
-    __syncthreads();
-
-    // 4. Epilogue through LDS (the X and A regions are free now): output rows
-    //    are the tile's pixels, contiguous in NHWC.
-    constexpr int WTN = 128;
-    constexpr int EPI_LD = WTN * 4 + 16;
-    char* epi = sX + wid * 32 * EPI_LD;
-    const int valid_rows = min(R, H - i0) * W;
-    const int64_t m0 = ((int64_t)b * H + i0) * W;
-    constexpr int Q = WTN / 4;
-    static_for<MI>([&](auto i) {
-        static_for<NI>([&](auto jj) {
-            static_for<16>([&](auto v) {
-                constexpr int vv = decltype(v)::value;
-                const int r = 8 * (vv >> 2) + 4 * (lane >> 5) + (vv & 3);
-                *reinterpret_cast<float*>(epi + r * EPI_LD + (jj * 32 + (lane & 31)) * 4) = acc[i][jj][vv];
-            });
-        });
-        __syncthreads();
-        for (int q = lane; q < 32 * Q; q += 64) {
-            const int r = q / Q, c4 = q - r * Q;
-            const int prow = wm * 64 + i * 32 + r;
-            const int64_t col = wn * WTN + c4 * 4;
-            if (prow >= valid_rows || col >= C_out) continue;
-            const float4 v4 = *reinterpret_cast<const float4*>(epi + r * EPI_LD + c4 * 16);
-            const int64_t idx = (m0 + prow) * C_out + col;  // C_out % 8 == 0: whole float4 in range
-            if constexpr (sizeof(TO) == 4) {
-                *reinterpret_cast<float4*>(static_cast<float*>(out) + idx) = v4;
-            } else {
-                *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + idx) =
-                    make_uint2(pack_bf16x2(v4.x, v4.y), pack_bf16x2(v4.z, v4.w));
+                    for (int di = 0; di < 3; ++di) {
+                        const int slot = (rl + di) % 3;
+                        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pr[slot][c]),
+                                                            __builtin_bit_cast(bf16x2_t, w01[di][c]), a, false);
+                        a = fmaf(sg[slot][c], w2[di][c], a);
+                    }
+                    acc[c] = a;
+                }
+                const int px = rl * W + j;
+                *reinterpret_cast<uint4*>(sA + f_a_off(px, cv, a_row_bytes)) =
+                    make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+                               pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
             }
         }
-        __syncthreads();
-    });
+    };
+    // Rows R*W .. 127 of the A tile stay zero for every tile.
+    for (int q = R * W * (C / 8) + tid; q < kFBM * (C / 8); q += 64 * kFWaves)
+        *reinterpret_cast<uint4*>(sA + f_a_off(q / (C / 8), q % (C / 8), a_row_bytes)) = make_uint4(0, 0, 0, 0);
+
+    constexpr int MI = 2, NI = 2;  // wave tile 64 x 64; waves 2 (M) x 4 (N)
+    const int wm = wid >> 2, wn = wid & 3;
+    const int g = lane >> 4, li = lane & 15;
+
+    for (; tile < n_tiles; tile += gridDim.x) {
+        const int next = tile + (int)gridDim.x;
+        depthwise_half(0);
+        f_vm_wait<0>();            // half 1 of this tile (and earlier stores) done
+        f_barrier();
+        copy_half(next, 0);
+        depthwise_half(1);
+        f_barrier();               // A complete, buffer 1 free
+        copy_half(next, 1);
+
+        f32x16_t acc[MI][NI];
+        static_for<MI>([&](auto i) {
+            static_for<NI>([&](auto jj) {
+                static_for<16>([&](auto v) { acc[i][jj][decltype(v)::value] = 0.0f; });
+            });
+        });
+        for (int ks = 0; ks < C / 16; ++ks) {
+            uint4 af[MI], bfr[NI];
+            const int ch = ks * 2 + (lane >> 5);
+            static_for<MI>([&](auto i) {
+                af[i] = *reinterpret_cast<const uint4*>(sA + f_a_off(wm * 64 + i * 32 + (lane & 31), ch, a_row_bytes));
+            });
+            static_for<NI>([&](auto jj) {
+                const int n = wn * 64 + jj * 32 + (g & 1) * 16 + 4 * (li & 3);
+                uint32_t w[4];
+                static_for<2>([&](auto rr) {
+                    const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
+                    v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(sP + f_p_off(k, n)));
+                    const uint2 uu = __builtin_bit_cast(uint2, v);
+                    w[rr * 2] = uu.x;
+                    w[rr * 2 + 1] = uu.y;
+                });
+                bfr[jj] = make_uint4(w[0], w[1], w[2], w[3]);
+            });
+            static_for<MI>([&](auto i) {
+                static_for<NI>([&](auto jj) { mfma32_bf16(acc[i][jj], af[i], bfr[jj]); });
+            });
+        }
+        // Next tile's half 0 (issued before this wave's half-1 copies) must
+        // have landed before the next depthwise; loads complete in order.
+        f_vm_wait<kXInstr>();
+        f_barrier();
+
+        // Store this tile through LDS: the A tile is consumed, so each wave
+        // stages 16-row x 64-column fp32 slabs of its block in its own 4 KiB
+        // of the A region and writes them back as 16-byte row segments
+        // (rows are the tile's pixels, contiguous in NHWC).
+        const int b = tile / tiles_per_img, i0 = (tile % tiles_per_img) * R;
+        const int valid_rows = min(R, H - i0) * W;
+        const int64_t m0 = ((int64_t)b * H + i0) * W;
+        float* stage = reinterpret_cast<float*>(sA + wid * 4096);  // [16][64] fp32
+        static_for<MI>([&](auto i) {
+            static_for<2>([&](auto hh) {
+                // rows 16*hh .. 16*hh+15 of the 32-row block i: accumulator elements 8*hh .. 8*hh+7
+                static_for<NI>([&](auto jj) {
+                    static_for<8>([&](auto vc) {
+                        constexpr int vv = 8 * decltype(hh)::value + decltype(vc)::value;
+                        const int r = 8 * ((vv >> 2) & 1) + 4 * (lane >> 5) + (vv & 3);
+                        stage[r * 64 + jj * 32 + (lane & 31)] = acc[i][jj][vv];
+                    });
+                });
+                __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the wave's slab is in LDS
+                __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int q = lane + 64 * k;
+                    const int r = q >> 4, c4 = q & 15;
+                    const int prow = wm * 64 + i * 32 + hh * 16 + r;
+                    const int64_t col = wn * 64 + c4 * 4;
+                    const float4 v4 = *reinterpret_cast<const float4*>(stage + r * 64 + c4 * 4);
+                    if (prow < valid_rows && col < C_out) {
+                        const int64_t idx = (m0 + prow) * C_out + col;
+                        if constexpr (sizeof(TO) == 4)
+                            *reinterpret_cast<float4*>(static_cast<float*>(out) + idx) = v4;
+                        else
+                            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + idx) =
+                                make_uint2(pack_bf16x2(v4.x, v4.y), pack_bf16x2(v4.z, v4.w));
+                    }
+                }
+                __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the slab is overwritten
+                __builtin_amdgcn_wave_barrier();
+            });
+        });
+        f_barrier();  // every wave is done with the A region before the next depthwise
+    }
+    f_vm_wait<0>();
 }
 
 template <int R>
 size_t fused_lds(const DwArgs& d) {
-    const size_t xt = (size_t)(R + 2) * d.W * d.C * 2;
-    return (size_t)d.C * kPRow + ((xt + 1023) & ~(size_t)1023) + (size_t)kFBM * d.C * 2;
+    return (size_t)d.C * kPRow + (size_t)kARegion + 2 * (size_t)kXBuf;
 }
 
 }  // namespace
@@ -244,33 +324,32 @@ int dwsep_fused_rows(const DwArgs& d, int64_t C_out, int lds_max) {
     if (d.C % 64 || d.C > 128 || C_out % 8 || C_out > kFBN) return 0;
     if (d.batch * d.H * d.W * d.C * 2 > (int64_t(1) << 31) - 1) return 0;
     if ((reinterpret_cast<uintptr_t>(d.x) & 15) || (reinterpret_cast<uintptr_t>(d.w) & 15)) return 0;
-    const int r = d.W <= 32 ? 4 : d.W <= 64 ? 2 : d.W <= 128 ? 1 : 0;
+    const int r = d.W <= 32 ? 4 : d.W <= 64 ? 2 : 0;
     if (!r) return 0;
-    const size_t lds = r == 4 ? fused_lds<4>(d) : r == 2 ? fused_lds<2>(d) : fused_lds<1>(d);
-    // epilogue staging (4 waves x 32 rows) reuses the X and A regions
-    const size_t epi = 4 * 32 * (128 * 4 + 16);
-    const size_t xa = lds - (size_t)d.C * kPRow;
-    if (lds > (size_t)lds_max || epi > xa) return 0;
+    // one channel half of the R+2 input rows must fit one copy buffer
+    if ((int64_t)(r + 2) * d.W * (d.C / 2) * 2 > kXBuf) return 0;
+    const size_t lds = r == 4 ? fused_lds<4>(d) : fused_lds<2>(d);
+    if (lds > (size_t)lds_max) return 0;
     return r;
 }
 
 hipError_t launch_dwsep_fused(const DwArgs& d, const void* pw, void* out, int64_t C_out, int out_type, int R,
-                              hipStream_t s) {
-    const size_t lds = R == 4 ? fused_lds<4>(d) : R == 2 ? fused_lds<2>(d) : fused_lds<1>(d);
+                              int cus, hipStream_t s) {
+    const size_t lds = R == 4 ? fused_lds<4>(d) : fused_lds<2>(d);
     const int tiles = (int)(d.batch * ((d.H + R - 1) / R));
+    const int grid = tiles < cus ? tiles : cus;
     void* fn = nullptr;
-#define ISAM_FUSED_FN(RR)                                                                        \
-    fn = out_type == kF32 ? reinterpret_cast<void*>(dwsep_fused_kernel<RR, float>)               \
-                          : reinterpret_cast<void*>(dwsep_fused_kernel<RR, uint16_t>)
-    if (R == 4) ISAM_FUSED_FN(4);
-    else if (R == 2) ISAM_FUSED_FN(2);
-    else ISAM_FUSED_FN(1);
-#undef ISAM_FUSED_FN
+    if (R == 4)
+        fn = out_type == kF32 ? reinterpret_cast<void*>(dwsep_fused_kernel<4, float>)
+                              : reinterpret_cast<void*>(dwsep_fused_kernel<4, uint16_t>);
+    else
+        fn = out_type == kF32 ? reinterpret_cast<void*>(dwsep_fused_kernel<2, float>)
+                              : reinterpret_cast<void*>(dwsep_fused_kernel<2, uint16_t>);
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     DwArgs dd = d;
-    void* args[] = {&dd, const_cast<void**>(&pw), &out, &C_out, &out_type};
-    return hipLaunchKernel(fn, dim3(tiles), dim3(256), args, lds, s);
+    void* args[] = {&dd, const_cast<void**>(&pw), &out, &C_out};
+    return hipLaunchKernel(fn, dim3(grid), dim3(64 * kFWaves), args, lds, s);
 }
 
 }  // namespace isam

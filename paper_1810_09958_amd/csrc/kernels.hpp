@@ -65,7 +65,7 @@ hipError_t launch_depthwise(const DwArgs& a, hipStream_t s);
 // Fused depthwise + pointwise (bf16 input): rows per tile, 0 if not applicable.
 int dwsep_fused_rows(const DwArgs& d, int64_t C_out, int lds_max);
 hipError_t launch_dwsep_fused(const DwArgs& d, const void* pw, void* out, int64_t C_out, int out_type, int R,
-                              hipStream_t s);
+                              int cus, hipStream_t s);
 
 // GRU recurrence (the input projection is a GemmArgs launch done before).
 struct GruArgs {
