@@ -104,6 +104,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     p.group_m = 8;
     p.xcd_remap = 1;
     p.dma = 1;
+    p.dma_waves = 4;  // set to 8 below for 256x256 tiles (two waves per SIMD measured faster)
     int bm, bn, bk;
     auto tiles = [&](int t) {
         tile_dims(t, ab_type, &bm, &bn, &bk);
@@ -133,6 +134,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     } else {
         p.tile = kTile64x64;
     }
+    if (p.tile == kTile256x256) p.dma_waves = 8;
     const int64_t nt = tiles(p.tile);
     // Split K when the tile grid leaves compute units idle and K is deep
     // enough that every split still runs several K tiles.
@@ -157,6 +159,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
         if ((s = strstr(env, "group=")) && sscanf(s + 6, "%d", &v) == 1 && v > 0) p.group_m = v;
         if ((s = strstr(env, "xcd=")) && sscanf(s + 4, "%d", &v) == 1) p.xcd_remap = v ? 1 : 0;
         if ((s = strstr(env, "dma=")) && sscanf(s + 4, "%d", &v) == 1) p.dma = v ? 1 : 0;
+        if ((s = strstr(env, "dmaw=")) && sscanf(s + 5, "%d", &v) == 1) p.dma_waves = v == 8 ? 8 : 4;
         if ((s = strstr(env, "splits=")) && sscanf(s + 7, "%d", &v) == 1 && v >= 1) {
             tile_dims(p.tile, ab_type, &bm, &bn, &bk);
             p.k_per_split = std::max<int64_t>(bk, cdiv(cdiv(K, v), bk) * bk);

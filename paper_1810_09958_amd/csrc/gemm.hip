@@ -6,7 +6,7 @@ namespace isam {
 
 GemmKernelFn gemm_kernel_bf16(int tile, int ta, int tb, int vec);
 GemmKernelFn gemm_kernel_f32(int tile, int ta, int tb, int vec);
-GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b);
+GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk) {
     static const int dims[kTileCount][2] = {{256, 256}, {256, 128}, {128, 128},
@@ -53,7 +53,12 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     int bm, bn, bk;
     tile_dims(p.tile, a.ab_type, &bm, &bn, &bk);
     GemmKernelFn fn = nullptr;
-    if (p.dma && a.ab_type == kBF16 && !a.trans_a && p.vec) fn = gemm_dma_kernel_for(p.tile, a.trans_b);
+    int threads = 256;
+    if (p.dma && a.ab_type == kBF16 && !a.trans_a && p.vec) {
+        fn = gemm_dma_kernel_for(p.tile, a.trans_b, p.dma_waves);
+        if (fn && p.dma_waves == 8 && (p.tile == kTile256x256 || p.tile == kTile256x128)) threads = 512;
+        else fn = gemm_dma_kernel_for(p.tile, a.trans_b, 4);
+    }
     if (!fn)
         fn = a.ab_type == kBF16 ? gemm_kernel_bf16(p.tile, a.trans_a, a.trans_b, p.vec)
                                 : gemm_kernel_f32(p.tile, a.trans_a, a.trans_b, p.vec);
@@ -66,7 +71,7 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     t.k_per_split = p.k_splits > 1 ? p.k_per_split : a.K;
     if (t.k_per_split <= 0) t.k_per_split = 1;
     dim3 grid((unsigned)(t.tiles_m * t.tiles_n), (unsigned)(p.k_splits > 1 ? p.k_splits : 1));
-    dim3 block(256);
+    dim3 block(threads);
     hipLaunchKernelGGL(fn, grid, block, 0, s, a, t);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.k_splits <= 1) return e;

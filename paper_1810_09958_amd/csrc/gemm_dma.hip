@@ -4,7 +4,16 @@
 
 namespace isam {
 
-GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b) {
+GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves) {
+    if (waves == 8) {
+        switch (tile) {
+            case kTile256x256:
+                return trans_b ? gemm_dma_kernel<256, 256, true, 2, 4> : gemm_dma_kernel<256, 256, false, 2, 4>;
+            case kTile256x128:
+                return trans_b ? gemm_dma_kernel<256, 128, true, 4, 2> : gemm_dma_kernel<256, 128, false, 4, 2>;
+            default: break;
+        }
+    }
     switch (tile) {
         case kTile256x256: return trans_b ? gemm_dma_kernel<256, 256, true> : gemm_dma_kernel<256, 256, false>;
         case kTile256x128: return trans_b ? gemm_dma_kernel<256, 128, true> : gemm_dma_kernel<256, 128, false>;

@@ -73,14 +73,14 @@ __device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
 
-template <int BM, int BN, bool TB>
-__global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
-    constexpr int WM = 2, WN = 2, STAGES = 4, BK = 32;
+template <int BM, int BN, bool TB, int WM = 2, int WN = 2>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
+    constexpr int NW = WM * WN, STAGES = 4, BK = 32;
     constexpr int WTM = BM / WM, WTN = BN / WN, MI = WTM / 32, NI = WTN / 32;
     constexpr int A_BYTES = BM * 64, B_BYTES = BN * 64, STAGE = A_BYTES + B_BYTES;
-    constexpr int A_INSTR = A_BYTES / 1024 / 4, B_INSTR = B_BYTES / 1024 / 4;  // per wave per tile
+    constexpr int A_INSTR = A_BYTES / 1024 / NW, B_INSTR = B_BYTES / 1024 / NW;  // per wave per tile
     constexpr int PER_TILE = A_INSTR + B_INSTR;
-    static_assert(A_INSTR >= 1 && B_INSTR >= 1, "tile too small for 4 waves of copies");
+    static_assert(A_INSTR >= 1 && B_INSTR >= 1, "tile too small for one copy per wave");
     static_assert(2 * PER_TILE < 64, "vmcnt range");
     __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(256) void gemm_dma_kernel(GemmArgs a, TileMapArgs t
     // Epilogue: identical to the register-staged kernel's (LDS-staged vector stores).
     const bool split_out = gridDim.y > 1;
     constexpr int EPI_LD = WTN * 4 + 16;
-    static_assert(4 * 32 * EPI_LD <= STAGES * STAGE, "epilogue staging must fit in LDS");
+    static_assert(NW * 32 * EPI_LD <= STAGES * STAGE, "epilogue staging must fit in LDS");
     char* epi = smem + wid * 32 * EPI_LD;
     float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
     const int64_t ldo = split_out ? a.N : a.ldc;

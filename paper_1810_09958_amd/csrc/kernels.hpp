@@ -44,6 +44,7 @@ struct GemmPlan {
     int group_m;     // tile-row group size of the rasterisation
     int xcd_remap;   // spread consecutive tiles of one group over one XCD
     int dma;         // 1: direct-to-LDS kernel where it applies (bf16, A K-contiguous, vec)
+    int dma_waves;   // 4 or 8 waves per workgroup for the direct-to-LDS kernel
     int skinny;      // 1: streaming kernel for N <= 32 (k_splits = K slices of skinny_k_slice)
 };
 int64_t skinny_k_slice(int ab_type);
