@@ -276,10 +276,14 @@ def main():
     dom = "gemm_8192x8192x8192_bf16_out_bf16"
     if dom in results:
         ach = results[dom]["TFLOP/s"]
-        out["roofline"] = {"kernel": "gemm_tile_kernel<bf16, 256x256> (8192^3, bf16 out)",
+        traffic = measured_traffic("gemm_dma_256x256_bf16_8192cubed_traffic.json")
+        out["roofline"] = {"kernel": "gemm_dma_kernel<256, 256, false, 2, 4> (8192^3, bf16 out)",
                            "bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS,
                            "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                           "traffic": None}
+                           "traffic": traffic}
+        if traffic is not None:
+            out["roofline"]["traffic_unit"] = "bytes per launch (HBM-side, rocprofv3 FETCH_SIZE/WRITE_SIZE, copy-scaled)"
+            out["roofline"]["traffic_GBps"] = round(traffic / (results[dom]["us_avg"] * 1e-6) / 1e9, 1)
     if "gru_T64_B32_H1024_bf16" in results:
         out["gru_timesteps_per_s"] = results["gru_T64_B32_H1024_bf16"]["timesteps_per_s"]
     if "dwsep_32x56x56x128_256_bf16_out_f32" in results:
@@ -292,6 +296,32 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def csrc_hash() -> str:
+    """sha256 over the HIP/C++ sources of the library (names and contents)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_1810_09958_amd", "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(name: str):
+    """Traffic per launch recorded under profiles/, or None when the kernel sources changed
+    since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", name)
+    try:
+        with open(path) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("csrc_sha256") != csrc_hash():
+        return None
+    return rec.get("traffic_bytes_per_dispatch")
+
+
 def cpu_baseline():
     """The CPU oracle (fp64, as used for parity) on a bounded sample of the square GEMM:
     R full rows of C = A.B with K = 8192, timed on this host's cores."""
@@ -301,12 +331,12 @@ def cpu_baseline():
     sq = workloads.gemm_square_bf16()
     A, B = sq["A_bf16"], sq["B_bf16"]
     threads = oracle.max_threads()
-    rows = 8
+    # pilot, then scale the sample to about 12 s of oracle work
+    rows = max(16, threads)
     t = time.perf_counter()
     oracle.gemm(np.ascontiguousarray(A[:rows]), B, rows, 8192, 8192, with_norm=False)
     dt = time.perf_counter() - t
-    # scale the sample to about 10 s of work
-    rows2 = int(min(8192, max(rows, rows * 10.0 / max(dt, 1e-3))))
+    rows2 = int(min(8192, rows * 12.0 / max(dt, 1e-3)))
     rows2 = max(threads, (rows2 // threads) * threads)
     t = time.perf_counter()
     oracle.gemm(np.ascontiguousarray(A[:rows2]), B, rows2, 8192, 8192, with_norm=False)
