@@ -121,10 +121,24 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
         p.k_splits = (int)cdiv(K, p.k_per_split);
         return p;
     }
+    // Tile choice (measured on MI355X): 256x256 tiles (8 waves) whenever they
+    // fill the CUs; for deep K, 256x256 tiles split along K until they do
+    // (the partial sums cost one extra pass over C); otherwise the largest
+    // tile that fills the CUs, unsplit.
+    const int64_t t256 = tiles(kTile256x256);
     if (N <= 32) {
         p.tile = kTile128x32;
-    } else if (tiles(kTile256x256) >= cus) {
+    } else if (t256 >= cus) {
         p.tile = kTile256x256;
+    } else if (K >= 4096 && ab_type == kBF16) {
+        p.tile = kTile256x256;
+        tile_dims(p.tile, ab_type, &bm, &bn, &bk);
+        const int64_t want = std::min<int64_t>(8, cdiv(cus, t256));
+        const int64_t sp = std::max<int64_t>(1, std::min<int64_t>(want, K / (8 * bk)));
+        if (sp > 1) {
+            p.k_per_split = cdiv(cdiv(K, sp), bk) * bk;
+            p.k_splits = (int)cdiv(K, p.k_per_split);
+        }
     } else if (tiles(kTile256x128) >= cus) {
         p.tile = kTile256x128;
     } else if (tiles(kTile128x128) >= cus) {
@@ -134,16 +148,16 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     } else {
         p.tile = kTile64x64;
     }
+    tile_dims(p.tile, ab_type, &bm, &bn, &bk);
     if (p.tile == kTile256x256) p.dma_waves = 8;
     const int64_t nt = tiles(p.tile);
-    // Split K when the tile grid leaves compute units idle and K is deep
-    // enough that every split still runs several K tiles.
-    if (nt < 2 * (int64_t)cus && K >= 8 * bk) {
-        int64_t want = cdiv(2 * (int64_t)cus, nt);
-        int64_t max_by_k = K / (4 * bk);
-        int64_t s = std::max<int64_t>(1, std::min<int64_t>(want, std::min<int64_t>(max_by_k, 16)));
-        if (s > 1) {
-            p.k_per_split = cdiv(cdiv(K, s), bk) * bk;
+    // Other tiles with a grid smaller than the CU count and deep K: split K
+    // so the grid covers the CUs.
+    if (p.k_splits == 1 && p.tile != kTile256x256 && nt < cus && K >= 8 * bk) {
+        const int64_t want = cdiv(cus, nt);
+        const int64_t sp = std::max<int64_t>(1, std::min<int64_t>(want, std::min<int64_t>(K / (4 * bk), 16)));
+        if (sp > 1) {
+            p.k_per_split = cdiv(cdiv(K, sp), bk) * bk;
             p.k_splits = (int)cdiv(K, p.k_per_split);
         }
     }

@@ -38,17 +38,68 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int spli
         }
     }
 }
+
+// Same sum, four adjacent columns per thread: N, ldc and the C address allow
+// whole 4-column groups (16-byte partial loads, 16- or 8-byte C accesses).
+__global__ __launch_bounds__(256) void splitk_reduce4_kernel(GemmArgs a, int splits) {
+    const int64_t total = a.M * a.N;
+    const int64_t groups = total >> 2;
+    const float4* P = reinterpret_cast<const float4*>(a.partial);
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < groups;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t idx = q << 2;
+        const int64_t row = idx / a.N, col = idx - row * a.N;
+        float4 v = P[q];
+        for (int s = 1; s < splits; ++s) {
+            const float4 w = P[(int64_t)s * groups + q];
+            v.x += w.x; v.y += w.y; v.z += w.z; v.w += w.w;
+        }
+        if (a.bias) {
+            v.x += a.bias[col]; v.y += a.bias[col + 1]; v.z += a.bias[col + 2]; v.w += a.bias[col + 3];
+        }
+        const int64_t o = row * a.ldc + col;
+        if (a.c_type == kF32) {
+            float4* C = reinterpret_cast<float4*>(static_cast<float*>(a.C) + o);
+            if (a.accumulate) {
+                const float4 c = *C;
+                v.x = c.x + v.x; v.y = c.y + v.y; v.z = c.z + v.z; v.w = c.w + v.w;
+            }
+            *C = v;
+        } else {
+            uint2* C = reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.C) + o);
+            if (a.accumulate) {
+                const uint2 c = *C;
+                v.x = bf16lo(c.x) + v.x; v.y = bf16hi(c.x) + v.y;
+                v.z = bf16lo(c.y) + v.z; v.w = bf16hi(c.y) + v.w;
+            }
+            *C = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+        }
+    }
+}
+
+hipError_t launch_splitk_reduce(const GemmArgs& a, int splits, hipStream_t s) {
+    const int64_t total = a.M * a.N;
+    const size_t esz = a.c_type == kF32 ? 4 : 2;
+    const bool vec4 = a.N % 4 == 0 && a.ldc % 4 == 0 && ((uintptr_t)a.C % (4 * esz)) == 0 &&
+                      ((uintptr_t)a.partial % 16) == 0;
+    if (vec4) {
+        int64_t blocks = (total / 4 + 255) / 256;
+        if (blocks > 8192) blocks = 8192;
+        hipLaunchKernelGGL(splitk_reduce4_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, splits);
+    } else {
+        int64_t blocks = (total + 255) / 256;
+        if (blocks > 4096) blocks = 4096;
+        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, splits);
+    }
+    return hipGetLastError();
+}
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     if (p.skinny) {
         hipError_t e = launch_skinny(a, p.k_splits, s);
         if (e != hipSuccess || p.k_splits <= 1) return e;
-        const int64_t total = a.M * a.N;
-        int64_t blocks = (total + 255) / 256;
-        if (blocks > 4096) blocks = 4096;
-        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, p.k_splits);
-        return hipGetLastError();
+        return launch_splitk_reduce(a, p.k_splits, s);
     }
     int bm, bn, bk;
     tile_dims(p.tile, a.ab_type, &bm, &bn, &bk);
@@ -75,11 +126,7 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     hipLaunchKernelGGL(fn, grid, block, 0, s, a, t);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || p.k_splits <= 1) return e;
-    const int64_t total = a.M * a.N;
-    int64_t blocks = (total + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a, p.k_splits);
-    return hipGetLastError();
+    return launch_splitk_reduce(a, p.k_splits, s);
 }
 
 }  // namespace isam
