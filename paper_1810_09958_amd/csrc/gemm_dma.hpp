@@ -4,10 +4,13 @@
 // listing), with the HBM -> LDS -> VGPR path of Section 3.5 rebuilt around
 // the CDNA4 data movers:
 //   * buffer_load ... lds (16 bytes per lane) copies A and B tiles straight
-//     into LDS: no staging registers, no ds_write instructions, and copies
-//     for up to three K tiles ahead are in flight while the MFMAs of the
-//     current tile run (4-stage LDS ring, K depth 32 per stage), and LDS
-//     fragment reads run one K step ahead of the MFMAs;
+//     into LDS: no staging registers and no ds_write instructions;
+//   * the K depth of a stage is 64, so every copied row segment is a whole
+//     128-byte cache line (row segments of 64 bytes leave half of each line
+//     fetched into the vector L1 unused and cap the L1 -> LDS stream at about
+//     two thirds of its full-line rate); two stages, and the copies of tile
+//     t+2 are issued during the last K step of tile t, a whole tile of MFMAs
+//     ahead of their use;
 //   * a copy instruction writes 64 consecutive 16-byte LDS units, so the
 //     bank swizzle is applied by choosing which global chunk each lane
 //     fetches; out-of-range chunks are fetched at an offset past the buffer
@@ -19,13 +22,17 @@
 //     (e = 0..3), so pieces taken from four consecutive K rows arrive as
 //     four consecutive K values of one column -- the MFMA B operand -- with
 //     no transpose pass.
-// LDS layouts (one stage, bf16):
-//   A / K-contiguous B: row r (64 bytes = 32 K values), logical 16-byte chunk
-//     c at physical chunk c ^ (((r >> 1) ^ (r >> 3)) & 3);
+// LDS layouts (one stage, bf16), chosen for the gfx950 LDS as measured: 64
+// banks of 4 bytes; a ds_read_b128 is served in four 16-lane phases, lanes
+// {0-3, 12-15, 20-27}, {4-11, 16-19, 28-31} and the same sets + 32; a
+// ds_read_b64_tr_b16 in two 32-lane phases.  A phase with two different
+// addresses on one bank takes an extra pass.
+//   A / K-contiguous B: row r (128 bytes = 64 K values), logical 16-byte
+//     chunk c at physical chunk c ^ ((r ^ (r >> 3)) & 7): the 16 rows of a
+//     b128 phase then cover all 16 bank groups of 16 bytes;
 //   N-contiguous B: K row k (BN*2 bytes), logical 32-byte block b at physical
-//     block b ^ (k & 3).
-// Both make every 8-lane (b128) or 16-lane (b64) read phase hit distinct
-// banks of the 32-bank LDS.
+//     block b ^ (2 * (k & 3)): the 4 K rows x 2 column blocks of a 32-lane
+//     transpose-read phase land in 8 different 32-byte bank groups.
 #pragma once
 
 #include "common.hpp"
@@ -37,8 +44,11 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 
+__device__ __forceinline__ int dma_a_swz(int r) { return (r ^ (r >> 3)) & 7; }
+__device__ __forceinline__ int dma_b_swz(int k) { return 2 * (k & 3); }
+
 __device__ __forceinline__ uint32_t dma_a_off(int r, int c) {
-    return (uint32_t)(r * 64 + ((c ^ (((r >> 1) ^ (r >> 3)) & 3)) << 4));
+    return (uint32_t)(r * 128 + ((c ^ dma_a_swz(r)) << 4));
 }
 
 // The copies are issued with inline assembly so that the compiler, which
@@ -75,13 +85,15 @@ __device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
 
 template <int BM, int BN, bool TB, int WM = 2, int WN = 2>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
-    constexpr int NW = WM * WN, STAGES = 4, BK = 32;
+    constexpr int NW = WM * WN, STAGES = 2, BK = 64, KS = BK / 16;
     constexpr int WTM = BM / WM, WTN = BN / WN, MI = WTM / 32, NI = WTN / 32;
-    constexpr int A_BYTES = BM * 64, B_BYTES = BN * 64, STAGE = A_BYTES + B_BYTES;
+    constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128, STAGE = A_BYTES + B_BYTES;
     constexpr int A_INSTR = A_BYTES / 1024 / NW, B_INSTR = B_BYTES / 1024 / NW;  // per wave per tile
     constexpr int PER_TILE = A_INSTR + B_INSTR;
     static_assert(A_INSTR >= 1 && B_INSTR >= 1, "tile too small for one copy per wave");
-    static_assert(2 * PER_TILE < 64, "vmcnt range");
+    static_assert(PER_TILE < 64, "vmcnt range");
+    static_assert(TB || BN >= 128, "N-contiguous B swizzle needs 8 column blocks per K row");
+    static_assert(KS == 4, "the K-step schedule below is written for four 16-deep steps");
     __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -101,15 +113,16 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
 
     // Per-lane global byte offsets of this wave's copies, relative to tile
     // origin (row m0 / n0, K index 0 of the tile); -1 marks a chunk outside
-    // the M / N range.  The K position is added per tile.
+    // the M / N range.  The K position is added per tile.  A copy
+    // instruction fills 8 rows x 128 bytes (K-contiguous operands) or
+    // 1024 / (BN*2) K rows (N-contiguous B).
     int64_t a_row_off[A_INSTR];
     int a_k[A_INSTR];
 #pragma unroll
     for (int q = 0; q < A_INSTR; ++q) {
         const int unit = (wid * A_INSTR + q) * 64 + lane;  // 16-byte LDS unit within the A region
-        const int r = unit >> 2, pc = unit & 3;
-        const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
-        a_k[q] = c * 8;
+        const int r = unit >> 3, pc = unit & 7;
+        a_k[q] = (pc ^ dma_a_swz(r)) * 8;
         a_row_off[q] = (m0 + r < a.M) ? (m0 + r) * a.lda : -1;
     }
     int64_t b_off[B_INSTR];
@@ -118,42 +131,37 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     for (int q = 0; q < B_INSTR; ++q) {
         const int unit = (wid * B_INSTR + q) * 64 + lane;
         if constexpr (TB) {
-            const int r = unit >> 2, pc = unit & 3;
-            const int c = pc ^ (((r >> 1) ^ (r >> 3)) & 3);
-            b_k[q] = c * 8;
+            const int r = unit >> 3, pc = unit & 7;
+            b_k[q] = (pc ^ dma_a_swz(r)) * 8;
             b_off[q] = (n0 + r < a.N) ? (n0 + r) * a.ldb : -1;
         } else {
             constexpr int UPR = BN / 8;  // 16-byte units per K row
             const int k = unit / UPR, u = unit % UPR;
-            const int b = (u >> 1) ^ (k & 3);
+            const int b = (u >> 1) ^ dma_b_swz(k);
             const int64_t n = n0 + b * 16 + (u & 1) * 8;
             b_k[q] = k;
             b_off[q] = (n < a.N) ? n : -1;
         }
     }
 
-    auto issue = [&](int tile) {
-        const int stage = tile % STAGES;
+    // Copy instruction q of K tile `tile` (A first, then B) into its stage.
+    auto issue_part = [&](int tile, auto q_c) {
+        constexpr int q = decltype(q_c)::value;
+        const int stage = tile & 1;
         const int64_t k0 = kbeg + (int64_t)tile * BK;
         char* sa = smem + stage * STAGE;
         char* sb = sa + A_BYTES;
-#pragma unroll
-        for (int q = 0; q < A_INSTR; ++q) {
+        if constexpr (q < A_INSTR) {
             const int64_t k = k0 + a_k[q];
             const uint32_t off = (a_row_off[q] >= 0 && k < kend) ? (uint32_t)((a_row_off[q] + k) * 2) : kOob;
             dma16(rsA, __builtin_amdgcn_readfirstlane(lds_addr_of(sa + (wid * A_INSTR + q) * 1024)), off);
-        }
-#pragma unroll
-        for (int q = 0; q < B_INSTR; ++q) {
+        } else {
+            constexpr int qb = q - A_INSTR;
+            const int64_t k = k0 + b_k[qb];
             uint32_t off;
-            if constexpr (TB) {
-                const int64_t k = k0 + b_k[q];
-                off = (b_off[q] >= 0 && k < kend) ? (uint32_t)((b_off[q] + k) * 2) : kOob;
-            } else {
-                const int64_t k = k0 + b_k[q];
-                off = (b_off[q] >= 0 && k < kend) ? (uint32_t)((k * a.ldb + b_off[q]) * 2) : kOob;
-            }
-            dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(sb + (wid * B_INSTR + q) * 1024)), off);
+            if constexpr (TB) off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((b_off[qb] + k) * 2) : kOob;
+            else off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((k * a.ldb + b_off[qb]) * 2) : kOob;
+            dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(sb + (wid * B_INSTR + qb) * 1024)), off);
         }
     };
 
@@ -188,7 +196,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             const int g = lane >> 4, li = lane & 15;
             const int n = wn * WTN + j * 32 + (g & 1) * 16 + 4 * (li & 3);
             const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
-            const int b = (n >> 4) ^ (k & 3);
+            const int b = (n >> 4) ^ dma_b_swz(k);
             const char* p = sb + k * (BN * 2) + b * 32 + (n & 15) * 2;
             v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p);
             const uint2 u = __builtin_bit_cast(uint2, v);
@@ -198,26 +206,6 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     };
     auto read_all = [&](Frag& f, int stage, int ks) {
         static_for<N_READS>([&](auto idx) { read_part(f, stage, ks, idx); });
-    };
-    // Copies of one K tile, one instruction at a time (A first, then B).
-    auto issue_part = [&](int tile, auto q_c) {
-        constexpr int q = decltype(q_c)::value;
-        const int stage = tile % STAGES;
-        const int64_t k0 = kbeg + (int64_t)tile * BK;
-        char* sa = smem + stage * STAGE;
-        char* sb = sa + A_BYTES;
-        if constexpr (q < A_INSTR) {
-            const int64_t k = k0 + a_k[q];
-            const uint32_t off = (a_row_off[q] >= 0 && k < kend) ? (uint32_t)((a_row_off[q] + k) * 2) : kOob;
-            dma16(rsA, __builtin_amdgcn_readfirstlane(lds_addr_of(sa + (wid * A_INSTR + q) * 1024)), off);
-        } else {
-            constexpr int qb = q - A_INSTR;
-            const int64_t k = k0 + b_k[qb];
-            uint32_t off;
-            if constexpr (TB) off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((b_off[qb] + k) * 2) : kOob;
-            else off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((k * a.ldb + b_off[qb]) * 2) : kOob;
-            dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(sb + (wid * B_INSTR + qb) * 1024)), off);
-        }
     };
     // MI*NI MFMAs of fragment set f; after MFMA number k the side operation
     // side(k) is issued, so loads and copies go out while the matrix core is
@@ -230,46 +218,54 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             __builtin_amdgcn_sched_barrier(0);
         });
     };
-
-    // Per K tile t (stage t % 4):
-    //   MFMAs ks=0 of t   + reads of ks=1 of t
-    //   wait for tile t+1's copies, barrier
-    //   MFMAs ks=1 of t   + reads of ks=0 of t+1, copies of tile t+3 (into
-    //                       the stage tile t-1 used)
-    if (nk > 0) {
-        static_for<3>([&](auto pc) {
-            constexpr int p = decltype(pc)::value;
-            if (p < nk) static_for<PER_TILE>([&](auto q) { issue_part(p, q); });
+    // MFMAs of f with the N_READS reads of (stage, ks) into g spread evenly
+    // over the MFMA slots (slot k issues reads [k*N/S, (k+1)*N/S)).
+    auto mfma_reading = [&](const Frag& f, Frag& g, int stage, int ks) {
+        mfma_with(f, [&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            constexpr int S = MI * NI;
+            constexpr int lo = (k * N_READS + S - 1) / S, hi = ((k + 1) * N_READS + S - 1) / S;
+            static_for<hi - lo>([&](auto d) {
+                read_part(g, stage, ks, std::integral_constant<int, lo + decltype(d)::value>{});
+            });
         });
-        if (nk > 2) vm_wait<2 * PER_TILE>();
-        else if (nk > 1) vm_wait<PER_TILE>();
-        else vm_wait<0>();
+    };
+
+    // Per K tile t (stage t & 1), four 16-deep K steps:
+    //   ks 0..2: MFMAs of step ks, reads of step ks+1 (alternating fragment sets)
+    //   wait for tile t+1's copies, barrier (every wave is done reading
+    //     stage t, so it may be overwritten)
+    //   ks 3:    MFMAs of step 3, reads of step 0 of tile t+1, copies of tile
+    //            t+2 into stage t & 1
+    if (nk > 0) {
+        static_for<PER_TILE>([&](auto q) { issue_part(0, q); });
+        if (nk > 1) {
+            static_for<PER_TILE>([&](auto q) { issue_part(1, q); });
+            vm_wait<PER_TILE>();
+        } else {
+            vm_wait<0>();
+        }
         block_sync();
         Frag f0, f1;
         read_all(f0, 0, 0);
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): nothing pending at the loop head
         for (int t = 0; t < nk; ++t) {
-            const int st = t % STAGES;
+            const int st = t & 1;
             __builtin_amdgcn_sched_barrier(0);
-            mfma_with(f0, [&](auto kc) {
-                constexpr int k = decltype(kc)::value;
-                constexpr int S = MI * NI;
-                constexpr int lo = (k * N_READS + S - 1) / S, hi = ((k + 1) * N_READS + S - 1) / S;
-                static_for<hi - lo>([&](auto d) {
-                    read_part(f1, st, 1, std::integral_constant<int, lo + decltype(d)::value>{});
-                });
-            });
-            const bool more = t + 1 < nk;
-            if (more) {
-                if (t + 2 < nk) vm_wait<PER_TILE>();  // tiles issued after t+1: only t+2
-                else vm_wait<0>();
+            mfma_reading(f0, f1, st, 1);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            mfma_reading(f1, f0, st, 2);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            mfma_reading(f0, f1, st, 3);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            if (t + 1 < nk) {
+                vm_wait<0>();  // only tile t+1's copies are in flight here
                 block_sync();
             }
-            const bool next_copy = t + 3 < nk;
-            const int nst = (t + 1) % STAGES;
-            // Reads of ks=0 of t+1 are unconditional (after the last tile they
-            // read an idle stage and are unused) so every path reaching the
-            // MFMAs has the same LDS requests in flight.
+            const bool next_copy = t + 2 < nk;
+            // Reads of step 0 of tile t+1 are unconditional (after the last
+            // tile they read an idle stage and are unused) so every path
+            // reaching the MFMAs has the same LDS requests in flight.
             mfma_with(f1, [&](auto kc) {
                 // N_READS reads then PER_TILE copies, spread evenly over the
                 // MI*NI MFMA slots (slot k issues ops [k*NOPS/S, (k+1)*NOPS/S)).
@@ -278,8 +274,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
                 constexpr int lo = (k * NOPS + S - 1) / S, hi = ((k + 1) * NOPS + S - 1) / S;
                 static_for<hi - lo>([&](auto d) {
                     constexpr int o = lo + decltype(d)::value;
-                    if constexpr (o < N_READS) read_part(f0, nst, 0, std::integral_constant<int, o>{});
-                    else if (next_copy) issue_part(t + 3, std::integral_constant<int, o - N_READS>{});
+                    if constexpr (o < N_READS) read_part(f0, st ^ 1, 0, std::integral_constant<int, o>{});
+                    else if (next_copy) issue_part(t + 2, std::integral_constant<int, o - N_READS>{});
                 });
             });
             // The next K step's fragments were requested during these MFMAs;
