@@ -83,213 +83,119 @@ __device__ __forceinline__ uint32_t lds_addr_of(const void* p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
 }
 
-template <int BM, int BN, bool TB, int WM = 2, int WN = 2>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
-    constexpr int NW = WM * WN, STAGES = 2, BK = 64, KS = BK / 16;
-    constexpr int WTM = BM / WM, WTN = BN / WN, MI = WTM / 32, NI = WTN / 32;
-    constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128, STAGE = A_BYTES + B_BYTES;
-    constexpr int A_INSTR = A_BYTES / 1024 / NW, B_INSTR = B_BYTES / 1024 / NW;  // per wave per tile
-    constexpr int PER_TILE = A_INSTR + B_INSTR;
+// Per-lane copy plan for one workgroup's A and B tiles (K depth 64 per
+// tile): byte offsets relative to the tile origin, with -1 for chunks outside
+// the M / N range.  Copy instruction Q of an operand fills the 1 KB LDS
+// block Q of this wave inside the operand's region: 8 rows x 128 bytes for a
+// K-contiguous operand, 1024 / (BN*2) K rows for N-contiguous B.
+template <int BM, int BN, bool TB, int NW>
+struct DmaCopier {
+    static constexpr int A_INSTR = BM * 128 / 1024 / NW, B_INSTR = BN * 128 / 1024 / NW;
     static_assert(A_INSTR >= 1 && B_INSTR >= 1, "tile too small for one copy per wave");
-    static_assert(PER_TILE < 64, "vmcnt range");
     static_assert(TB || BN >= 128, "N-contiguous B swizzle needs 8 column blocks per K row");
-    static_assert(KS == 4, "the K-step schedule below is written for four 16-deep steps");
-    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+    __amdgpu_buffer_rsrc_t rsA, rsB;
+    int64_t a_row_off[A_INSTR], b_off[B_INSTR];
+    int a_k[A_INSTR], b_k[B_INSTR];
+    int64_t ldb, kend;
+    int wid;
 
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wm = wid / WN, wn = wid % WN;
-    int tm, tn;
-    map_tile(tmap, tm, tn);
-    const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
-    const int split = blockIdx.y;
-    const int64_t kbeg = (int64_t)split * tmap.k_per_split;
-    const int64_t kend = min(a.K, kbeg + tmap.k_per_split);
-    const int nk = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
-
-    const int64_t a_ext = (a.M - 1) * a.lda + a.K;
-    const int64_t b_ext = TB ? ((a.N - 1) * a.ldb + a.K) : ((a.K - 1) * a.ldb + a.N);
-    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(a_ext * 2));
-    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(a.B, (uint32_t)(b_ext * 2));
-
-    // Per-lane global byte offsets of this wave's copies, relative to tile
-    // origin (row m0 / n0, K index 0 of the tile); -1 marks a chunk outside
-    // the M / N range.  The K position is added per tile.  A copy
-    // instruction fills 8 rows x 128 bytes (K-contiguous operands) or
-    // 1024 / (BN*2) K rows (N-contiguous B).
-    int64_t a_row_off[A_INSTR];
-    int a_k[A_INSTR];
+    __device__ __forceinline__ DmaCopier(const GemmArgs& a, int64_t m0, int64_t n0, int64_t kend_, int wid_, int lane)
+        : ldb(a.ldb), kend(kend_), wid(wid_) {
+        const int64_t a_ext = (a.M - 1) * a.lda + a.K;
+        const int64_t b_ext = TB ? ((a.N - 1) * a.ldb + a.K) : ((a.K - 1) * a.ldb + a.N);
+        rsA = make_rsrc(a.A, (uint32_t)(a_ext * 2));
+        rsB = make_rsrc(a.B, (uint32_t)(b_ext * 2));
 #pragma unroll
-    for (int q = 0; q < A_INSTR; ++q) {
-        const int unit = (wid * A_INSTR + q) * 64 + lane;  // 16-byte LDS unit within the A region
-        const int r = unit >> 3, pc = unit & 7;
-        a_k[q] = (pc ^ dma_a_swz(r)) * 8;
-        a_row_off[q] = (m0 + r < a.M) ? (m0 + r) * a.lda : -1;
-    }
-    int64_t b_off[B_INSTR];
-    int b_k[B_INSTR];
-#pragma unroll
-    for (int q = 0; q < B_INSTR; ++q) {
-        const int unit = (wid * B_INSTR + q) * 64 + lane;
-        if constexpr (TB) {
+        for (int q = 0; q < A_INSTR; ++q) {
+            const int unit = (wid * A_INSTR + q) * 64 + lane;  // 16-byte LDS unit within the A region
             const int r = unit >> 3, pc = unit & 7;
-            b_k[q] = (pc ^ dma_a_swz(r)) * 8;
-            b_off[q] = (n0 + r < a.N) ? (n0 + r) * a.ldb : -1;
-        } else {
-            constexpr int UPR = BN / 8;  // 16-byte units per K row
-            const int k = unit / UPR, u = unit % UPR;
-            const int b = (u >> 1) ^ dma_b_swz(k);
-            const int64_t n = n0 + b * 16 + (u & 1) * 8;
-            b_k[q] = k;
-            b_off[q] = (n < a.N) ? n : -1;
+            a_k[q] = (pc ^ dma_a_swz(r)) * 8;
+            a_row_off[q] = (m0 + r < a.M) ? (m0 + r) * a.lda : -1;
         }
-    }
-
-    // Copy instruction q of K tile `tile` (A first, then B) into its stage.
-    auto issue_part = [&](int tile, auto q_c) {
-        constexpr int q = decltype(q_c)::value;
-        const int stage = tile & 1;
-        const int64_t k0 = kbeg + (int64_t)tile * BK;
-        char* sa = smem + stage * STAGE;
-        char* sb = sa + A_BYTES;
-        if constexpr (q < A_INSTR) {
-            const int64_t k = k0 + a_k[q];
-            const uint32_t off = (a_row_off[q] >= 0 && k < kend) ? (uint32_t)((a_row_off[q] + k) * 2) : kOob;
-            dma16(rsA, __builtin_amdgcn_readfirstlane(lds_addr_of(sa + (wid * A_INSTR + q) * 1024)), off);
-        } else {
-            constexpr int qb = q - A_INSTR;
-            const int64_t k = k0 + b_k[qb];
-            uint32_t off;
-            if constexpr (TB) off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((b_off[qb] + k) * 2) : kOob;
-            else off = (b_off[qb] >= 0 && k < kend) ? (uint32_t)((k * a.ldb + b_off[qb]) * 2) : kOob;
-            dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(sb + (wid * B_INSTR + qb) * 1024)), off);
-        }
-    };
-
-    f32x16_t acc[MI][NI];
-    static_for<MI>([&](auto i) {
-        static_for<NI>([&](auto j) {
-            static_for<16>([&](auto v) { acc[i][j][decltype(v)::value] = 0.0f; });
-        });
-    });
-
-    // Fragments of one 16-deep K step: MI A blocks and NI B blocks (32x32 each).
-    struct Frag {
-        uint4 a[MI], b[NI];
-    };
-    constexpr int B_READS = TB ? 1 : 2;               // LDS reads per B block
-    constexpr int N_READS = MI + NI * B_READS;        // LDS reads per fragment set
-    // Issue read number `idx` of fragment set f (stage, K step ks).
-    auto read_part = [&](Frag& f, int stage, int ks, auto idx_c) {
-        constexpr int idx = decltype(idx_c)::value;
-        const char* sa = smem + stage * STAGE;
-        const char* sb = sa + A_BYTES;
-        const int ch = ks * 2 + (lane >> 5);
-        if constexpr (idx < MI) {
-            const int r = wm * WTM + idx * 32 + (lane & 31);
-            f.a[idx] = *reinterpret_cast<const uint4*>(sa + dma_a_off(r, ch));
-        } else if constexpr (TB) {
-            constexpr int j = idx - MI;
-            const int r = wn * WTN + j * 32 + (lane & 31);
-            f.b[j] = *reinterpret_cast<const uint4*>(sb + dma_a_off(r, ch));
-        } else {
-            constexpr int j = (idx - MI) / 2, rr = (idx - MI) % 2;
-            const int g = lane >> 4, li = lane & 15;
-            const int n = wn * WTN + j * 32 + (g & 1) * 16 + 4 * (li & 3);
-            const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
-            const int b = (n >> 4) ^ dma_b_swz(k);
-            const char* p = sb + k * (BN * 2) + b * 32 + (n & 15) * 2;
-            v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p);
-            const uint2 u = __builtin_bit_cast(uint2, v);
-            if constexpr (rr == 0) { f.b[j].x = u.x; f.b[j].y = u.y; }
-            else { f.b[j].z = u.x; f.b[j].w = u.y; }
-        }
-    };
-    auto read_all = [&](Frag& f, int stage, int ks) {
-        static_for<N_READS>([&](auto idx) { read_part(f, stage, ks, idx); });
-    };
-    // MI*NI MFMAs of fragment set f; after MFMA number k the side operation
-    // side(k) is issued, so loads and copies go out while the matrix core is
-    // busy instead of between MFMA groups.  sched_barrier pins the order.
-    auto mfma_with = [&](const Frag& f, auto&& side) {
-        static_for<MI * NI>([&](auto kc) {
-            constexpr int k = decltype(kc)::value;
-            mfma32_bf16(acc[k / NI][k % NI], f.a[k / NI], f.b[k % NI]);
-            side(kc);
-            __builtin_amdgcn_sched_barrier(0);
-        });
-    };
-    // MFMAs of f with the N_READS reads of (stage, ks) into g spread evenly
-    // over the MFMA slots (slot k issues reads [k*N/S, (k+1)*N/S)).
-    auto mfma_reading = [&](const Frag& f, Frag& g, int stage, int ks) {
-        mfma_with(f, [&](auto kc) {
-            constexpr int k = decltype(kc)::value;
-            constexpr int S = MI * NI;
-            constexpr int lo = (k * N_READS + S - 1) / S, hi = ((k + 1) * N_READS + S - 1) / S;
-            static_for<hi - lo>([&](auto d) {
-                read_part(g, stage, ks, std::integral_constant<int, lo + decltype(d)::value>{});
-            });
-        });
-    };
-
-    // Per K tile t (stage t & 1), four 16-deep K steps:
-    //   ks 0..2: MFMAs of step ks, reads of step ks+1 (alternating fragment sets)
-    //   wait for tile t+1's copies, barrier (every wave is done reading
-    //     stage t, so it may be overwritten)
-    //   ks 3:    MFMAs of step 3, reads of step 0 of tile t+1, copies of tile
-    //            t+2 into stage t & 1
-    if (nk > 0) {
-        static_for<PER_TILE>([&](auto q) { issue_part(0, q); });
-        if (nk > 1) {
-            static_for<PER_TILE>([&](auto q) { issue_part(1, q); });
-            vm_wait<PER_TILE>();
-        } else {
-            vm_wait<0>();
-        }
-        block_sync();
-        Frag f0, f1;
-        read_all(f0, 0, 0);
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): nothing pending at the loop head
-        for (int t = 0; t < nk; ++t) {
-            const int st = t & 1;
-            __builtin_amdgcn_sched_barrier(0);
-            mfma_reading(f0, f1, st, 1);
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            mfma_reading(f1, f0, st, 2);
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            mfma_reading(f0, f1, st, 3);
-            __builtin_amdgcn_s_waitcnt(0xc07f);
-            if (t + 1 < nk) {
-                vm_wait<0>();  // only tile t+1's copies are in flight here
-                block_sync();
+#pragma unroll
+        for (int q = 0; q < B_INSTR; ++q) {
+            const int unit = (wid * B_INSTR + q) * 64 + lane;
+            if constexpr (TB) {
+                const int r = unit >> 3, pc = unit & 7;
+                b_k[q] = (pc ^ dma_a_swz(r)) * 8;
+                b_off[q] = (n0 + r < a.N) ? (n0 + r) * a.ldb : -1;
+            } else {
+                constexpr int UPR = BN / 8;  // 16-byte units per K row
+                const int k = unit / UPR, u = unit % UPR;
+                const int b = (u >> 1) ^ dma_b_swz(k);
+                const int64_t n = n0 + b * 16 + (u & 1) * 8;
+                b_k[q] = k;
+                b_off[q] = (n < a.N) ? n : -1;
             }
-            const bool next_copy = t + 2 < nk;
-            // Reads of step 0 of tile t+1 are unconditional (after the last
-            // tile they read an idle stage and are unused) so every path
-            // reaching the MFMAs has the same LDS requests in flight.
-            mfma_with(f1, [&](auto kc) {
-                // N_READS reads then PER_TILE copies, spread evenly over the
-                // MI*NI MFMA slots (slot k issues ops [k*NOPS/S, (k+1)*NOPS/S)).
-                constexpr int k = decltype(kc)::value;
-                constexpr int S = MI * NI, NOPS = N_READS + PER_TILE;
-                constexpr int lo = (k * NOPS + S - 1) / S, hi = ((k + 1) * NOPS + S - 1) / S;
-                static_for<hi - lo>([&](auto d) {
-                    constexpr int o = lo + decltype(d)::value;
-                    if constexpr (o < N_READS) read_part(f0, st ^ 1, 0, std::integral_constant<int, o>{});
-                    else if (next_copy) issue_part(t + 2, std::integral_constant<int, o - N_READS>{});
-                });
-            });
-            // The next K step's fragments were requested during these MFMAs;
-            // waiting here tells the compiler nothing is pending at the loop
-            // head, which keeps it from draining reads it does not need.
-            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
         }
     }
-    __syncthreads();
+    // A copy instruction Q of the K tile starting at k0 into region `dst`.
+    template <int Q>
+    __device__ __forceinline__ void a_part(int64_t k0, char* dst) const {
+        const int64_t k = k0 + a_k[Q];
+        const uint32_t off = (a_row_off[Q] >= 0 && k < kend) ? (uint32_t)((a_row_off[Q] + k) * 2) : kOob;
+        dma16(rsA, __builtin_amdgcn_readfirstlane(lds_addr_of(dst + (wid * A_INSTR + Q) * 1024)), off);
+    }
+    template <int Q>
+    __device__ __forceinline__ void b_part(int64_t k0, char* dst) const {
+        const int64_t k = k0 + b_k[Q];
+        uint32_t off;
+        if constexpr (TB) off = (b_off[Q] >= 0 && k < kend) ? (uint32_t)((b_off[Q] + k) * 2) : kOob;
+        else off = (b_off[Q] >= 0 && k < kend) ? (uint32_t)((k * ldb + b_off[Q]) * 2) : kOob;
+        dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(dst + (wid * B_INSTR + Q) * 1024)), off);
+    }
+};
 
-    // Epilogue: identical to the register-staged kernel's (LDS-staged vector stores).
+// MFMA operands of one 16-deep K step: MI A blocks and NI B blocks (32x32 each).
+template <int MI, int NI>
+struct Frag {
+    uint4 a[MI], b[NI];
+};
+
+// LDS read number IDX of a fragment set (K step ks of the tile whose A / B
+// regions are sa / sb): A blocks first (one ds_read_b128 each), then B
+// blocks (one ds_read_b128, or two ds_read_b64_tr_b16 when N-contiguous).
+// arow / bcol: the wave's first A row / B column inside the tile.
+template <int IDX, int MI, int NI, bool TB, int BN>
+__device__ __forceinline__ void read_frag_part(Frag<MI, NI>& f, const char* sa, const char* sb, int ks, int arow,
+                                               int bcol, int lane) {
+    const int ch = ks * 2 + (lane >> 5);
+    if constexpr (IDX < MI) {
+        const int r = arow + IDX * 32 + (lane & 31);
+        f.a[IDX] = *reinterpret_cast<const uint4*>(sa + dma_a_off(r, ch));
+    } else if constexpr (TB) {
+        constexpr int j = IDX - MI;
+        const int r = bcol + j * 32 + (lane & 31);
+        f.b[j] = *reinterpret_cast<const uint4*>(sb + dma_a_off(r, ch));
+    } else {
+        constexpr int j = (IDX - MI) / 2, rr = (IDX - MI) % 2;
+        const int g = lane >> 4, li = lane & 15;
+        const int n = bcol + j * 32 + (g & 1) * 16 + 4 * (li & 3);
+        const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
+        const int b = (n >> 4) ^ dma_b_swz(k);
+        const char* p = sb + k * (BN * 2) + b * 32 + (n & 15) * 2;
+        v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p);
+        const uint2 u = __builtin_bit_cast(uint2, v);
+        if constexpr (rr == 0) {
+            f.b[j].x = u.x;
+            f.b[j].y = u.y;
+        } else {
+            f.b[j].z = u.x;
+            f.b[j].w = u.y;
+        }
+    }
+}
+
+// Accumulators of the wave's WTM x WTN tile -> C (or the split-K partial
+// sums), staged through LDS so every store is a 16-byte (fp32) or 8-byte
+// (bf16) vector store.  `smem` must hold NW * 32 * (WTN*4 + 16) bytes and be
+// idle (no copies in flight).
+template <int MI, int NI, int WTM, int WTN, int NW>
+__device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc)[MI][NI], char* smem, int64_t m0,
+                                               int64_t n0, int wm, int wn, int wid, int lane) {
     const bool split_out = gridDim.y > 1;
+    const int split = blockIdx.y;
     constexpr int EPI_LD = WTN * 4 + 16;
-    static_assert(NW * 32 * EPI_LD <= STAGES * STAGE, "epilogue staging must fit in LDS");
     char* epi = smem + wid * 32 * EPI_LD;
     float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
     const int64_t ldo = split_out ? a.N : a.ldc;
@@ -355,6 +261,125 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
         }
         __syncthreads();
     });
+}
+
+
+// Two-stage kernel, any tile shape of the table.  Per K tile t (stage t & 1),
+// four 16-deep K steps:
+//   ks 0..2: MFMAs of step ks, reads of step ks+1 (alternating fragment sets)
+//   wait for tile t+1's copies, barrier (every wave is done reading stage
+//     t, so it may be overwritten)
+//   ks 3:    MFMAs of step 3, reads of step 0 of tile t+1, copies of tile
+//            t+2 into stage t & 1
+template <int BM, int BN, bool TB, int WM = 2, int WN = 2>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
+    constexpr int NW = WM * WN, STAGES = 2, BK = 64;
+    constexpr int WTM = BM / WM, WTN = BN / WN, MI = WTM / 32, NI = WTN / 32;
+    constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128, STAGE = A_BYTES + B_BYTES;
+    using Copier = DmaCopier<BM, BN, TB, NW>;
+    constexpr int A_INSTR = Copier::A_INSTR, PER_TILE = Copier::A_INSTR + Copier::B_INSTR;
+    static_assert(PER_TILE < 64, "vmcnt range");
+    static_assert(NW * 32 * (WTN * 4 + 16) <= STAGES * STAGE, "epilogue staging must fit in LDS");
+    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wm = wid / WN, wn = wid % WN;
+    int tm, tn;
+    map_tile(tmap, tm, tn);
+    const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+    const int64_t kbeg = (int64_t)blockIdx.y * tmap.k_per_split;
+    const int64_t kend = min(a.K, kbeg + tmap.k_per_split);
+    const int nk = kend > kbeg ? (int)((kend - kbeg + BK - 1) / BK) : 0;
+    const Copier cp(a, m0, n0, kend, wid, lane);
+
+    // Copy instruction Q of K tile `tile` (A first, then B) into its stage.
+    auto issue_part = [&](int tile, auto q_c) {
+        constexpr int q = decltype(q_c)::value;
+        char* sa = smem + (tile & 1) * STAGE;
+        const int64_t k0 = kbeg + (int64_t)tile * BK;
+        if constexpr (q < A_INSTR) cp.template a_part<q>(k0, sa);
+        else cp.template b_part<q - A_INSTR>(k0, sa + A_BYTES);
+    };
+
+    f32x16_t acc[MI][NI];
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) { acc[i][j][decltype(v)::value] = 0.0f; });
+        });
+    });
+
+    using F = Frag<MI, NI>;
+    constexpr int N_READS = MI + NI * (TB ? 1 : 2);  // LDS reads per fragment set
+    auto read_part = [&](F& f, int stage, int ks, auto idx_c) {
+        const char* sa = smem + stage * STAGE;
+        read_frag_part<decltype(idx_c)::value, MI, NI, TB, BN>(f, sa, sa + A_BYTES, ks, wm * WTM, wn * WTN, lane);
+    };
+    // MI*NI MFMAs of fragment set f; after MFMA number k the side operation
+    // side(k) is issued, so loads and copies go out while the matrix core is
+    // busy instead of between MFMA groups.  sched_barrier pins the order.
+    auto mfma_with = [&](const F& f, auto&& side) {
+        static_for<MI * NI>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            mfma32_bf16(acc[k / NI][k % NI], f.a[k / NI], f.b[k % NI]);
+            side(kc);
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+    // MFMAs of f with the N_READS reads of (stage, ks) into g, plus (when
+    // copy) the PER_TILE copies of tile ct, spread evenly over the MFMA slots
+    // (slot k issues side ops [k*NOPS/S, (k+1)*NOPS/S), reads first).
+    auto step = [&](const F& f, F& g, int stage, int ks, auto nc_c, bool copy, int ct) {
+        constexpr int NC = decltype(nc_c)::value;
+        mfma_with(f, [&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            constexpr int S = MI * NI, NOPS = N_READS + NC;
+            constexpr int lo = (k * NOPS + S - 1) / S, hi = ((k + 1) * NOPS + S - 1) / S;
+            static_for<hi - lo>([&](auto d) {
+                constexpr int o = lo + decltype(d)::value;
+                if constexpr (o < N_READS) read_part(g, stage, ks, std::integral_constant<int, o>{});
+                else if (copy) issue_part(ct, std::integral_constant<int, o - N_READS>{});
+            });
+        });
+    };
+    using None = std::integral_constant<int, 0>;
+
+    if (nk > 0) {
+        static_for<PER_TILE>([&](auto q) { issue_part(0, q); });
+        if (nk > 1) {
+            static_for<PER_TILE>([&](auto q) { issue_part(1, q); });
+            vm_wait<PER_TILE>();
+        } else {
+            vm_wait<0>();
+        }
+        block_sync();
+        F f0, f1;
+        static_for<N_READS>([&](auto idx) { read_part(f0, 0, 0, idx); });
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): nothing pending at the loop head
+        for (int t = 0; t < nk; ++t) {
+            const int st = t & 1;
+            __builtin_amdgcn_sched_barrier(0);
+            step(f0, f1, st, 1, None{}, false, 0);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            step(f1, f0, st, 2, None{}, false, 0);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            step(f0, f1, st, 3, None{}, false, 0);
+            __builtin_amdgcn_s_waitcnt(0xc07f);
+            if (t + 1 < nk) {
+                vm_wait<0>();  // only tile t+1's copies are in flight here
+                block_sync();
+            }
+            // Reads of step 0 of tile t+1 are unconditional (after the last
+            // tile they read an idle stage and are unused) so every path
+            // reaching the MFMAs has the same LDS requests in flight.
+            step(f1, f0, st ^ 1, 0, std::integral_constant<int, PER_TILE>{}, t + 2 < nk, t + 2);
+            // The next K step's fragments were requested during these MFMAs;
+            // waiting here tells the compiler nothing is pending at the loop
+            // head, which keeps it from draining reads it does not need.
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+        }
+    }
+    __syncthreads();
+    store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, lane);
 }
 
 }  // namespace isam
