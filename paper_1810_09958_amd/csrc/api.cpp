@@ -421,7 +421,7 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
     (void)input_size;
     if (T < 0 || batch <= 0 || hidden_size <= 0 || !valid_dtype(w_type)) return 0;
     const size_t gx = align256((size_t)T * (size_t)batch * 3 * (size_t)hidden_size * sizeof(float));
-    const size_t hb = align256(2 * (size_t)batch * (size_t)hidden_size * dsize(w_type));
+    const size_t hb = align256(((size_t)T + 1) * (size_t)batch * (size_t)hidden_size * dsize(w_type));
     return gx + hb + kGruSyncBytes;
 }
 
@@ -457,7 +457,8 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     if ((uintptr_t)U & 15) return fail(ISAM_ERR_UNSUPPORTED, "%s: U must be 16-byte aligned", who);
     const size_t xb = (size_t)T * batch * I * es, wb = (size_t)3 * H * I * es, ub = (size_t)3 * H * H * es;
     if ((int64_t)xb > kMaxExtent || (int64_t)wb > kMaxExtent || (int64_t)ub > kMaxExtent ||
-        (int64_t)((size_t)T * batch * 3 * H * sizeof(float)) > kMaxExtent)
+        (int64_t)((size_t)T * batch * 3 * H * sizeof(float)) > kMaxExtent ||
+        (int64_t)(((size_t)T + 1) * batch * H * es) > kMaxExtent)
         return fail(ISAM_ERR_UNSUPPORTED, "%s: a tensor spans more than 2^31 bytes", who);
     const void* ins[6] = {x, W, U, h0, bias, bias_hn};
     const size_t inb[6] = {xb, wb, ub, state, (size_t)3 * H * sizeof(float), (size_t)H * sizeof(float)};
@@ -521,7 +522,7 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     float* gx = reinterpret_cast<float*>(ws);
     const size_t gx_b = align256((size_t)T * batch * 3 * H * sizeof(float));
     void* hbuf = ws + gx_b;
-    const size_t hb_b = align256(2 * (size_t)batch * H * es);
+    const size_t hb_b = align256(((size_t)T + 1) * batch * H * es);
     unsigned* sync = reinterpret_cast<unsigned*>(ws + gx_b + hb_b);
 
     // Input projection for all steps: Gx[T*batch][3H] = x[T*batch][I] . W^T.

@@ -32,19 +32,32 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kSyncWords = kGruSyncBytes / 4;
+constexpr int kRedLd = 20;  // floats per row of the cross-wave sums (20: the 4 row groups written by
+                            // one store instruction fall on different banks)
 // Upper bound on one barrier wait, in ticks of the 100 MHz constant clock.
 constexpr uint64_t kBarrierTimeoutTicks = 200000000ull;  // 2 s
 
 __device__ __forceinline__ int gru_rows(int J) { return ((3 * J + 15) / 16) * 16; }
+// U rows in LDS: a multiple of 256 bytes, so the chunk swizzle below stays
+// inside the row.
+__host__ __device__ __forceinline__ int64_t gru_row_bytes(int64_t H, int64_t es) { return (H * es + 255) / 256 * 256; }
+// 16-byte chunk c of U row r sits at chunk c ^ (2 * (r & 7)): the 16 lanes of
+// every ds_read_b128 phase (rows r = lane % 16, chunk offsets lane / 16) then
+// fall on 16 different bank groups.
+__device__ __forceinline__ int u_chunk(int r, int c) { return c ^ (2 * (r & 7)); }
 
 // Cross-workgroup exchange of h and the step barrier.
 //
 // h_{t-1} travels between workgroups (and XCDs, whose L2 caches are not
-// coherent with each other) through device-scope (sc1) buffer stores and
-// loads: stores write through to the device coherence point and loads are
-// served from it, so no L2 write-back or invalidation is needed per step.
-// __syncthreads() waits for each thread's stores to complete (vmcnt(0))
-// before the workgroup signals arrival.
+// coherent with each other) through a ring of T+1 slots, one per step: h_t is
+// written to slot t+1 with device-scope (sc1) stores, which write through to
+// the device coherence point, and __syncthreads() waits for each thread's
+// stores to complete (vmcnt(0)) before the workgroup signals arrival.  After
+// the barrier, slot t+1 is read with ordinary (L2-cached) loads: no
+// workgroup has touched that slot earlier in the launch, so no L2 can hold a
+// stale copy of it, and the first reader on each XCD brings it into that
+// XCD's L2 for the other 31 workgroups there -- each step's state leaves
+// memory once per XCD instead of once per workgroup.
 //
 // The barrier is two-level to limit serialised atomics on one address:
 // workgroups arrive on a counter of their group of kGroup, the last arrival
@@ -90,7 +103,7 @@ template <typename T>
 __global__ void gru_init_kernel(GruArgs a) {
     const int64_t n = a.batch * a.H;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
+         i += (int64_t)gridDim.x * blockDim.x) {  // slot 0 of the ring: h0 in the operand type
         const float v = a.h0 ? a.h0[i] : 0.0f;
         if constexpr (sizeof(T) == 2) static_cast<uint16_t*>(a.hbuf)[i] = (uint16_t)f32_to_bf16(v);
         else static_cast<float*>(a.hbuf)[i] = v;
@@ -106,7 +119,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
     const int J = a.units_per_wg, BB = a.batch_per_wg;
     const int64_t H = a.H, B = a.batch;
     const int RT = gru_rows(J), MT = RT / 16;
-    const int row_bytes = (int)(H * (int64_t)sizeof(T)) + 16;
+    const int row_bytes = (int)gru_row_bytes(H, sizeof(T));
     const int n_ug = (int)(H / J);
     const int ug = blockIdx.x % n_ug, bg = blockIdx.x / n_ug;
     const int64_t j0 = (int64_t)ug * J, b0 = (int64_t)bg * BB;
@@ -114,7 +127,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
 
     char* u_lds = smem;
-    float* red = reinterpret_cast<float*>(smem + RT * row_bytes);  // [kWaves][RT][16]
+    float* red = reinterpret_cast<float*>(smem + RT * row_bytes);  // [kWaves][RT][kRedLd]
 
     // Priming: U rows (g*H + j0 + jj) for local row g*J + jj; padding rows are zero.
     {
@@ -127,7 +140,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
                 const int g = lr / J, jj = lr - g * J;
                 v = *reinterpret_cast<const uint4*>(U + (g * H + j0 + jj) * H + (int64_t)c * E);
             }
-            *reinterpret_cast<uint4*>(u_lds + lr * row_bytes + c * 16) = v;
+            *reinterpret_cast<uint4*>(u_lds + lr * row_bytes + u_chunk(lr, c) * 16) = v;
         }
     }
 
@@ -166,14 +179,15 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
     fetch_gx(0);
 
     constexpr int kBatch = 8;  // h chunks requested together per lane
-    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)(2 * B * H * (int64_t)sizeof(T)));
+    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)((a.T + 1) * B * H * (int64_t)sizeof(T)));
     for (int64_t t = 0; t < a.T; ++t) {
-        const int64_t hcur_off = (t & 1) * B * H;  // element offset of h_{t-1} in hbuf
+        const int64_t hcur_off = t * B * H;  // element offset of h_{t-1}: ring slot t
         f32x4_t acc[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) acc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         for (int kg0 = kg_lo; kg0 < kg_hi; kg0 += kBatch) {
-            // Issue every h load of the batch before the first MFMA needs one.
+            // Issue every h load of the batch, then the U fragment reads (they
+            // do not depend on h), before the first MFMA needs either.
             uint4 hv[kBatch];
 #pragma unroll
             for (int u = 0; u < kBatch; ++u) {
@@ -181,21 +195,28 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
                 const int64_t k = (int64_t)(kg * 4 + quarter) * E;
                 const bool ok = kg < kg_hi && col_ok && k < H;
                 const uint32_t off = ok ? (uint32_t)((hcur_off + hb_row * H + k) * (int64_t)sizeof(T)) : kOob;
-                hv[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs_h, (int)off, 0, kCpolDevice));
+                hv[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs_h, (int)off, 0, 0));
+            }
+            uint4 uf[kBatch][3];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int chunk = (kg0 + u) * 4 + quarter;
+                const bool kok = kg0 + u < kg_hi && (int64_t)chunk * E < H;
+#pragma unroll
+                for (int m = 0; m < 3; ++m) {
+                    const int r = m * 16 + n_col;
+                    uf[u][m] = (m < MT && kok) ? *reinterpret_cast<const uint4*>(u_lds + r * row_bytes + u_chunk(r, chunk) * 16)
+                                               : make_uint4(0, 0, 0, 0);
+                }
             }
 #pragma unroll
             for (int u = 0; u < kBatch; ++u) {
-                const int kg = kg0 + u;
-                if (kg >= kg_hi) break;
-                const int chunk = kg * 4 + quarter;
-                const int64_t k = (int64_t)chunk * E;
+                if (kg0 + u >= kg_hi) break;
 #pragma unroll
-                for (int m = 0; m < 4; ++m) {
+                for (int m = 0; m < 3; ++m) {
                     if (m >= MT) break;
-                    uint4 uv = make_uint4(0, 0, 0, 0);
-                    if (k < H) uv = *reinterpret_cast<const uint4*>(u_lds + (m * 16 + n_col) * row_bytes + chunk * 16);
-                    if constexpr (sizeof(T) == 2) mfma16_bf16(acc[m], uv, hv[u]);
-                    else mfma16_f32x4(acc[m], uv, hv[u]);
+                    if constexpr (sizeof(T) == 2) mfma16_bf16(acc[m], uf[u][m], hv[u]);
+                    else mfma16_f32x4(acc[m], uf[u][m], hv[u]);
                 }
             }
         }
@@ -205,7 +226,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
             if (m >= MT) break;
 #pragma unroll
             for (int v = 0; v < 4; ++v)
-                red[(wid * RT + m * 16 + 4 * quarter + v) * 16 + n_col] = acc[m][v];
+                red[(wid * RT + m * 16 + 4 * quarter + v) * kRedLd + n_col] = acc[m][v];
         }
         __syncthreads();
         if (owner) {
@@ -214,7 +235,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
             for (int g = 0; g < 3; ++g) {
                 float s = 0.0f;
 #pragma unroll
-                for (int w = 0; w < kWaves; ++w) s += red[(w * RT + g * J + jj) * 16 + nn];
+                for (int w = 0; w < kWaves; ++w) s += red[(w * RT + g * J + jj) * kRedLd + nn];
                 gh[g] = s;
             }
             const float r = sigmoidf(gx_r + bias_r + gh[0]);
@@ -223,7 +244,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
             const float h = (1.0f - z) * n + z * h_prev;
             h_prev = h;
             if (a.h_seq) a.h_seq[(t * B + bb) * H + j] = h;
-            const int64_t hn = ((t + 1) & 1) * B * H + bb * H + j;
+            const int64_t hn = (t + 1) * B * H + bb * H + j;  // ring slot t+1
             if constexpr (sizeof(T) == 2)
                 __builtin_amdgcn_raw_buffer_store_b16((unsigned short)f32_to_bf16(h), rs_h, (int)(hn * 2), 0, kCpolDevice);
             else
@@ -264,8 +285,8 @@ hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStre
 
 size_t gru_lds_bytes(int w_type, int64_t H, int J) {
     const int RT = ((3 * J + 15) / 16) * 16;
-    const size_t es = w_type == kBF16 ? 2 : 4;
-    return (size_t)RT * (size_t)(H * es + 16) + (size_t)kWaves * RT * 16 * sizeof(float);
+    const int64_t es = w_type == kBF16 ? 2 : 4;
+    return (size_t)RT * (size_t)gru_row_bytes(H, es) + (size_t)kWaves * RT * kRedLd * sizeof(float);
 }
 
 hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s) {

@@ -79,7 +79,7 @@ struct GruArgs {
     const float* bias_hn;   // [H] or null
     float* h_seq;           // [T][batch][H] or null
     float* h_T;             // [batch][H] or null
-    void* hbuf;             // 2 x [batch][H] in w_type: MFMA copy of h_{t-1}
+    void* hbuf;             // [T+1][batch][H] in w_type: ring of per-step MFMA copies of h
     unsigned* sync;         // barrier counters and error word (kGruSyncBytes, zeroed by the launch)
     int units_per_wg;       // J
     int batch_per_wg;       // BB
