@@ -9,7 +9,10 @@ HBM:
   * separable depthwise conv 32 x 56 x 56 x 128 -> 256, bf16 (fp32 out) and fp32
   * fp32 GEMM 128^3
 Each part is bracketed by HIP events on the stream the library launches on (torch's current
-stream), so the per-part times are device times.  `value` is the GEMM throughput of the
+stream), so the per-part times are device times.  The HBM-bound parts (skinny GEMM, GRU,
+separable conv) rotate over enough input copies that every call reads from HBM rather than
+the 256 MB memory-side cache; the same call on one warm buffer set is reported beside it as
+"<name>_mall_warm".  `value` is the GEMM throughput of the
 large bf16 GEMMs (total FLOP / total time); GRU timesteps/s, separable-conv GB/s and the
 rest are reported under "components".  `roofline` covers the dominant kernel (the square
 bf16 GEMM, bf16 output); `cpu_baseline` times the CPU oracle on a bounded sample.
@@ -142,49 +145,82 @@ def main():
                           {"kind": "gemm_bf16", "flop": fl,
                            "bytes": gemm_bytes(M, N, K, C.element_size())}))
 
+    # The HBM-bound parts (skinny GEMM, GRU, separable conv) have working sets that fit the
+    # 256 MB memory-side cache.  Their reported numbers rotate over enough copies of the
+    # inputs (and large outputs) that one pass over the rotation set exceeds 2 x 256 MB, so
+    # every call reads from HBM; the same call on one buffer set is reported beside it as
+    # "<name>_mall_warm".
+    ROTATE_BYTES = 2 * 256 * (1 << 20)
+
+    def n_sets(bytes_per_set):
+        return max(2, -(-ROTATE_BYTES // bytes_per_set) + 1)
+
+    def add_rotated(name, make_call, sets, info):
+        """make_call(i) -> the call on buffer set i; adds the rotated and the MALL-warm entry."""
+        calls = [make_call(i) for i in range(sets)]
+        state = {"i": 0}
+
+        def rotated():
+            calls[state["i"]]()
+            state["i"] = (state["i"] + 1) % len(calls)
+
+        comps.append((name, rotated, dict(info, rotation_sets=sets)))
+        # MALL-warm: the same call on set 0, right after an untimed call on set 0.
+        comps.append((name + "_mall_warm", calls[0], dict(info, rotation_sets=1, pre=calls[0])))
+
     # -- skinny GEMM ------------------------------------------------------------------
     sk = workloads.skinny()
     for name, A_h, B_h, es in [("skinny_4096x32x4096_bf16", sk["A_bf16"], sk["B_bf16"], 2),
                                ("skinny_4096x32x4096_f32", sk["A"], sk["B"], 4)]:
-        A, B = gpu(A_h), gpu(B_h)
-        C = torch.empty((4096, 32), device=dev, dtype=torch.float32)
+        if not want(name):
+            continue
+        A0, B0 = gpu(A_h), gpu(B_h)
+        sets = n_sets(A0.numel() * es)
+        As = [A0] + [A0.clone() for _ in range(sets - 1)]
+        Bs = [B0] + [B0.clone() for _ in range(sets - 1)]
+        Cs = [torch.empty((4096, 32), device=dev, dtype=torch.float32) for _ in range(sets)]
         ws = torch.empty(max(1, isam.gemm_workspace_size(4096, 32, 4096, 1 if es == 2 else 0, 0)),
                          device=dev, dtype=torch.uint8)
-        if want(name):
-            comps.append((name, (lambda A=A, B=B, C=C, ws=ws: isam.gemm(A, B, C, workspace=ws)),
-                          {"kind": "skinny", "flop": 2.0 * 4096 * 32 * 4096,
-                           "bytes": es * (4096 * 4096 + 4096 * 32) + 4 * 4096 * 32}))
+        add_rotated(name, lambda i, As=As, Bs=Bs, Cs=Cs, ws=ws: (lambda: isam.gemm(As[i], Bs[i], Cs[i], workspace=ws)),
+                    sets, {"kind": "skinny", "flop": 2.0 * 4096 * 32 * 4096,
+                           "bytes": es * (4096 * 4096 + 4096 * 32) + 4 * 4096 * 32})
     del sk
 
     # -- GRU --------------------------------------------------------------------------
-    g = workloads.gru()
     T, Bt, I, H = 64, 32, 1024, 1024
-    gx, gW, gU, gb = gpu(g["x_bf16"]), gpu(g["W_bf16"]), gpu(g["U_bf16"]), gpu(g["bias"])
-    g_hseq = torch.empty((T, Bt, H), device=dev)
-    g_hT = torch.empty((Bt, H), device=dev)
-    g_ws = torch.empty(isam.gru_forward_workspace_size(T, Bt, I, H, 1), device=dev, dtype=torch.uint8)
-    del g
     if want("gru_T64_B32_H1024_bf16"):
-        comps.append(("gru_T64_B32_H1024_bf16",
-                      lambda: isam.gru_forward(gx, gW, gU, bias=gb, h_seq=g_hseq, h_T=g_hT, workspace=g_ws),
-                      {"kind": "gru", "steps": T,
-                       "flop": 2.0 * T * Bt * 3 * H * (I + H),
-                       "bytes": 2 * (3 * H * I + 3 * H * H + T * Bt * I) + 4 * T * Bt * H}))
+        g = workloads.gru()
+        gx, gW, gU, gb = gpu(g["x_bf16"]), gpu(g["W_bf16"]), gpu(g["U_bf16"]), gpu(g["bias"])
+        del g
+        sets = n_sets(2 * (T * Bt * I + 6 * H * I) + 4 * T * Bt * H)
+        gsets = [(gx, gW, gU)] + [(gx.clone(), gW.clone(), gU.clone()) for _ in range(sets - 1)]
+        hseqs = [torch.empty((T, Bt, H), device=dev) for _ in range(sets)]
+        g_hT = torch.empty((Bt, H), device=dev)
+        g_ws = torch.empty(isam.gru_forward_workspace_size(T, Bt, I, H, 1), device=dev, dtype=torch.uint8)
+        add_rotated("gru_T64_B32_H1024_bf16",
+                    lambda i: (lambda: isam.gru_forward(gsets[i][0], gsets[i][1], gsets[i][2], bias=gb,
+                                                        h_seq=hseqs[i], h_T=g_hT, workspace=g_ws)),
+                    sets, {"kind": "gru", "steps": T,
+                           "flop": 2.0 * T * Bt * 3 * H * (I + H),
+                           "bytes": 2 * (3 * H * I + 3 * H * H + T * Bt * I) + 4 * T * Bt * H})
 
     # -- separable depthwise conv -------------------------------------------------------
     d = workloads.dwsep()
     for name, X_h, D_h, P_h, es in [("dwsep_32x56x56x128_256_bf16_out_f32", d["X_bf16"], d["D_bf16"], d["P_bf16"], 2),
                                     ("dwsep_32x56x56x128_256_f32", d["X"], d["D"], d["P"], 4)]:
-        X, Dw, P = gpu(X_h), gpu(D_h), gpu(P_h)
-        y = torch.empty((32, 56, 56, 256), device=dev, dtype=torch.float32)
+        if not want(name):
+            continue
+        X0, Dw, P = gpu(X_h), gpu(D_h), gpu(P_h)
+        sets = n_sets(X0.numel() * es + 4 * 100352 * 256)
+        Xs = [X0] + [X0.clone() for _ in range(sets - 1)]
+        ys = [torch.empty((32, 56, 56, 256), device=dev, dtype=torch.float32) for _ in range(sets)]
         it = 1 if es == 2 else 0
         ws = torch.empty(isam.dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, it, 0),
                          device=dev, dtype=torch.uint8)
-        if want(name):
-            comps.append((name, (lambda X=X, Dw=Dw, P=P, y=y, ws=ws: isam.dwsep_conv(X, Dw, P, out=y, workspace=ws)),
-                          {"kind": "dwsep", "flop": 2.0 * 100352 * (9 * 128 + 128 * 256),
+        add_rotated(name, lambda i, Xs=Xs, Dw=Dw, P=P, ys=ys, ws=ws: (lambda: isam.dwsep_conv(Xs[i], Dw, P, out=ys[i], workspace=ws)),
+                    sets, {"kind": "dwsep", "flop": 2.0 * 100352 * (9 * 128 + 128 * 256),
                            # fused minimum: X read once, y written once (+ the small filters)
-                           "bytes": es * (32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + 4 * 100352 * 256}))
+                           "bytes": es * (32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + 4 * 100352 * 256})
     del d
 
     # -- small fp32 GEMM ------------------------------------------------------------------
@@ -200,7 +236,9 @@ def main():
     stream = torch.cuda.current_stream()
 
     def run_step(evs=None):
-        for i, (_, fn, _) in enumerate(comps):
+        for i, (_, fn, info) in enumerate(comps):
+            if info.get("pre") is not None:
+                info["pre"]()
             if evs is not None:
                 evs[i][0].record(stream)
             fn()
@@ -238,6 +276,8 @@ def main():
             r["frac_f32_peak"] = round(tfl / PEAK_F32_TFLOPS, 6)
         elif info["kind"] in ("skinny", "dwsep"):
             r["frac_hbm_peak"] = round(gbs / PEAK_HBM_GBPS, 4)
+        if info.get("rotation_sets", 1) > 1:
+            r["rotation_sets"] = info["rotation_sets"]
         if info["kind"] == "gru":
             r["timesteps_per_s"] = round(info["steps"] / s, 1)
             r["us_per_timestep"] = round(avg * 1e3 / info["steps"], 3)
