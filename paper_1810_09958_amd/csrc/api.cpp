@@ -115,8 +115,15 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     // fallback).
     if (allow_skinny && N <= 32 && K > 0 && N % (ab_type == kBF16 ? 8 : 4) == 0 &&
         !(getenv("ISAM_GEMM_CONFIG") && strstr(getenv("ISAM_GEMM_CONFIG"), "skinny=0"))) {
-        p.skinny = 1;
         p.tile = kTile128x32;
+        if (ab_type == kBF16 && cdiv(M, skinny_stream_rows()) >= cus / 2) {
+            // Enough 16-row workgroups to cover the CUs: one pass over A, no split.
+            p.skinny = 2;
+            p.k_splits = 1;
+            p.k_per_split = K;
+            return p;
+        }
+        p.skinny = 1;
         p.k_per_split = skinny_k_slice(ab_type);
         p.k_splits = (int)cdiv(K, p.k_per_split);
         return p;

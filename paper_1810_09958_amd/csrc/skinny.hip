@@ -206,11 +206,153 @@ __global__ __launch_bounds__(64 * kSkWaves) void skinny_kernel(GemmArgs a) {
     }
 }
 
+// Row-streaming variant (bf16, N <= 32, one pass, no split): a workgroup
+// owns 16 rows of C and the whole K range; its 8 waves split K and each runs
+// a private 3-stage pipeline of direct-to-LDS copies (64-deep K chunks: A
+// 16 rows x 128 bytes, B 64 rows x 64 bytes -- whole cache lines), so no
+// workgroup barrier is needed until the final cross-wave sum.  A streams
+// from HBM once in 1 KB contiguous copies; 16x16x32 MFMAs take A fragments
+// with ds_read_b128 and B fragments with ds_read_b64_tr_b16.
+// LDS layouts per stage: A row r (128 bytes) chunk c at c ^ ((r >> 1) & 7);
+// B K row k (64 bytes) 32-byte block b at b ^ ((k >> 3) & 1) -- both
+// conflict-free for the reads below.
+constexpr int kRowsPerWg = 16;
+constexpr int kStreamStages = 3;
+constexpr int kStageA = kRowsPerWg * 128;   // 2 KB
+constexpr int kStageB = 64 * 64;            // 4 KB
+constexpr int kStage = kStageA + kStageB;
+
+__device__ __forceinline__ int sr_a_swz(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ uint32_t sr_a_off(int r, int c) { return (uint32_t)(r * 128 + ((c ^ sr_a_swz(r)) << 4)); }
+__device__ __forceinline__ uint32_t sr_b_off(int k, int n) {
+    return (uint32_t)(k * 64 + ((((n >> 4) ^ ((k >> 3) & 1))) << 5) + (n & 15) * 2);
+}
+
+__global__ __launch_bounds__(64 * kSkWaves) void skinny_rows_kernel(GemmArgs a) {
+    __shared__ __attribute__((aligned(1024))) char smem[kSkWaves * kStreamStages * kStage];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int64_t m0 = (int64_t)blockIdx.x * kRowsPerWg;
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(((a.M - 1) * a.lda + a.K) * 2));
+    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(a.B, (uint32_t)(((a.K - 1) * a.ldb + a.N) * 2));
+    char* ws = smem + wid * kStreamStages * kStage;  // this wave's stages
+
+    // This wave's K range, in 64-deep chunks.
+    const int64_t nchunk_all = (a.K + 63) / 64;
+    const int64_t c_lo = nchunk_all * wid / kSkWaves, c_hi = nchunk_all * (wid + 1) / kSkWaves;
+    const int nc = (int)(c_hi - c_lo);
+
+    // Copy plan: A copy q (0..1) fills rows 8q .. 8q+7 (lane -> row 8q + lane/8,
+    // physical chunk lane%8); B copy q (0..3) fills K rows 16q .. 16q+15 (lane
+    // -> row 16q + lane/4, physical 16-byte unit lane%4).
+    int64_t a_row_off[2];
+    int a_k[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int r = 8 * q + (lane >> 3), pc = lane & 7;
+        a_k[q] = (pc ^ sr_a_swz(r)) * 8;
+        a_row_off[q] = (m0 + r < a.M) ? (m0 + r) * a.lda : -1;
+    }
+    int b_kr[4], b_n[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int k = 16 * q + (lane >> 2), pu = lane & 3;  // physical 16-byte unit in the 64-byte row
+        const int blk = (pu >> 1) ^ ((k >> 3) & 1);         // logical 32-byte block held there
+        b_kr[q] = k;
+        b_n[q] = blk * 16 + (pu & 1) * 8;
+    }
+    auto issue = [&](int c) {  // chunk index relative to this wave
+        char* st = ws + (c % kStreamStages) * kStage;
+        const int64_t k0 = (c_lo + c) * 64;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int64_t k = k0 + a_k[q];
+            const uint32_t off = (a_row_off[q] >= 0 && k < a.K) ? (uint32_t)((a_row_off[q] + k) * 2) : kOob;
+            sk_dma16(rsA, __builtin_amdgcn_readfirstlane(sk_lds_addr(st + q * 1024)), off);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t k = k0 + b_kr[q];
+            const uint32_t off = (k < a.K && b_n[q] < a.N) ? (uint32_t)((k * a.ldb + b_n[q]) * 2) : kOob;
+            sk_dma16(rsB, __builtin_amdgcn_readfirstlane(sk_lds_addr(st + kStageA + q * 1024)), off);
+        }
+    };
+
+    f32x4_t acc[2];
+    acc[0] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    acc[1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int g = lane >> 4, li = lane & 15;
+    if (nc > 0) issue(0);
+    if (nc > 1) issue(1);
+    for (int c = 0; c < nc; ++c) {
+        // Chunk c has landed once at most the copies of chunk c+1 are in flight.
+        if (c + 1 < nc) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        // Stage (c+2) % 3 was last read for chunk c-1, whose reads completed
+        // before its MFMAs: refill it now.
+        if (c + 2 < nc) issue(c + 2);
+        const char* st = ws + (c % kStreamStages) * kStage;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {  // two 32-deep MFMA steps per chunk
+            // A fragment: row li, K chunk ks*4 + g (8 values).
+            const uint4 af = *reinterpret_cast<const uint4*>(st + sr_a_off(li, ks * 4 + g));
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                uint32_t w[4];
+#pragma unroll
+                for (int rr = 0; rr < 2; ++rr) {
+                    const int k = ks * 32 + g * 8 + rr * 4 + (li >> 2);
+                    const int n = nt * 16 + 4 * (li & 3);
+                    v4i16_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)(st + kStageA + sr_b_off(k, n)));
+                    const uint2 u = __builtin_bit_cast(uint2, v);
+                    w[2 * rr] = u.x;
+                    w[2 * rr + 1] = u.y;
+                }
+                mfma16_bf16(acc[nt], af, make_uint4(w[0], w[1], w[2], w[3]));
+            }
+        }
+    }
+
+    // Sum the 8 waves' 16x32 tiles in wave order (stages no longer needed).
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(smem);  // [wave][16][32]
+    // acc[nt] element v of lane l: row 4*(l/16) + v, column nt*16 + l%16
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) red[(wid * 16 + 4 * g + v) * 32 + nt * 16 + li] = acc[nt][v];
+    __syncthreads();
+    for (int o = tid; o < kRowsPerWg * 32; o += 64 * kSkWaves) {
+        const int row = o >> 5, col = o & 31;
+        float sum = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kSkWaves; ++w) sum += red[(w * 16 + row) * 32 + col];
+        const int64_t gr = m0 + row;
+        if (gr >= a.M || col >= a.N) continue;
+        const int64_t idx = gr * a.ldc + col;
+        if (a.bias) sum += a.bias[col];
+        if (a.c_type == kF32) {
+            float* C = static_cast<float*>(a.C);
+            C[idx] = a.accumulate ? C[idx] + sum : sum;
+        } else {
+            uint16_t* C = static_cast<uint16_t*>(a.C);
+            C[idx] = (uint16_t)f32_to_bf16(a.accumulate ? bf16_to_f32(C[idx]) + sum : sum);
+        }
+    }
+}
+
 }  // namespace
 
 // K depth of one workgroup's slice (the split-K unit) for the skinny kernel.
 int64_t skinny_k_slice(int ab_type) { return ab_type == kBF16 ? 2048 : 1024; }
 int skinny_rows_per_wg(int ab_type) { return ab_type == kBF16 ? 32 : 64; }
+
+int skinny_stream_rows() { return kRowsPerWg; }
+
+hipError_t launch_skinny_rows(const GemmArgs& a, hipStream_t s) {
+    const dim3 grid((unsigned)((a.M + kRowsPerWg - 1) / kRowsPerWg)), block(64 * kSkWaves);
+    hipLaunchKernelGGL(skinny_rows_kernel, grid, block, 0, s, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_skinny(const GemmArgs& a, int splits, hipStream_t s) {
     const int R = skinny_rows_per_wg(a.ab_type);
