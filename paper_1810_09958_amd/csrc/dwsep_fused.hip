@@ -29,6 +29,7 @@ namespace {
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned u32x2_t __attribute__((vector_size(2 * sizeof(unsigned))));
 
 constexpr int kFBM = 128;     // MFMA rows per workgroup
 constexpr int kFBN = 256;     // output channels per workgroup (padded)
@@ -78,6 +79,7 @@ constexpr int kFWaves = 8;
 constexpr int kARegion = 32768;        // A tile (<= 128 x 128 bf16), also 8 x 4 KiB store staging
 constexpr int kXBuf = 32768;           // bytes of one input half-tile buffer
 constexpr int kXInstr = kXBuf / 1024 / kFWaves;  // copies per wave per half (4)
+constexpr int kStoresPerWave = 16;     // output stores per wave per tile (MI x 2 slabs x 4)
 
 // Persistent form: one workgroup per CU walks its tiles (tile = R output rows
 // of one image).  LDS: P [C][256] (copied once) | A [128][C] | two buffers of
@@ -106,6 +108,8 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
 
     const __amdgpu_buffer_rsrc_t rsP = make_rsrc(pw, (uint32_t)(C * C_out * 2));
     const __amdgpu_buffer_rsrc_t rsX = make_rsrc(d.x, (uint32_t)(d.batch * (int64_t)H * W * C * 2));
+    const __amdgpu_buffer_rsrc_t rsO =
+        make_rsrc(out, (uint32_t)(d.batch * (int64_t)H * W * C_out * (int64_t)sizeof(TO)));
 
     // Copy channel half h of tile `tile`'s input rows into buffer h.
     auto copy_half = [&](int tile, int h) {
@@ -141,77 +145,87 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
     f_vm_wait<0>();
     f_barrier();
 
-    // Depthwise of one channel half into the A tile: item = (column j, unit u).
+    // Depthwise of one channel half into the A tile: thread tid < W*UH owns
+    // item (column j, channel unit u) = (tid / UH, tid % UH) in both halves
+    // (W*UH <= 512 is checked at dispatch), so its filter taps are fixed and
+    // are loaded once, before the tile loop.  Taps (di, 0) and (di, 1) of
+    // channel c are paired as bf16x2 for v_dot2_f32_bf16; tap (di, 2) is
+    // applied with an fp32 FMA.
     const uint16_t* wp = static_cast<const uint16_t*>(d.w);
-    auto depthwise_half = [&](int h) {
+    const bool dw_item = tid < W * UH;
+    const int dj_col = dw_item ? tid / UH : 0, dj_u = dw_item ? tid % UH : 0;
+    uint32_t w01[2][3][8];
+    float w2[2][3][8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int cv = h * UH + dj_u;
+#pragma unroll
+        for (int di = 0; di < 3; ++di) {
+            uint4 t0 = make_uint4(0, 0, 0, 0), t1 = t0, t2 = t0;
+            if (dw_item) {
+                t0 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 0) * C + cv * 8);
+                t1 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 1) * C + cv * 8);
+                t2 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 2) * C + cv * 8);
+            }
+            const uint32_t a0[4] = {t0.x, t0.y, t0.z, t0.w}, a1[4] = {t1.x, t1.y, t1.z, t1.w},
+                           a2[4] = {t2.x, t2.y, t2.z, t2.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                w01[h][di][2 * q] = (a0[q] & 0xffffu) | (a1[q] << 16);
+                w01[h][di][2 * q + 1] = (a0[q] >> 16) | (a1[q] & 0xffff0000u);
+                w2[h][di][2 * q] = bf16lo(a2[q]);
+                w2[h][di][2 * q + 1] = bf16hi(a2[q]);
+            }
+        }
+    }
+    auto depthwise_half = [&](auto h_c) {
+        constexpr int h = decltype(h_c)::value;
+        if (!dw_item) return;
         const char* xs = sX0 + h * kXBuf;
-        for (int item = tid; item < W * UH; item += 64 * kFWaves) {
-            const int j = item / UH, u = item % UH;
-            const int cv = h * UH + u;                   // channel vector within C
-            // Taps (di, 0) and (di, 1) of channel c are paired as bf16x2 for
-            // v_dot2_f32_bf16; tap (di, 2) is applied with an fp32 FMA.  The
-            // input pairs of each row are built once and shared by the output
-            // rows that use it.
-            uint32_t w01[3][8];
-            float w2[3][8];
+        const int j = dj_col, u = dj_u;
+        const int cv = h * UH + u;  // channel vector within C
+        uint32_t pr[3][8];  // sliding window of rows: (x=j-1, x=j) pairs per channel
+        float sg[3][8];     // x=j+1 values per channel
+        auto load_row = [&](int rr, int slot) {
+            uint4 v[3];
 #pragma unroll
-            for (int di = 0; di < 3; ++di) {
-                const uint4 t0 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 0) * C + cv * 8);
-                const uint4 t1 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 1) * C + cv * 8);
-                const uint4 t2 = *reinterpret_cast<const uint4*>(wp + (di * 3 + 2) * C + cv * 8);
-                const uint32_t a0[4] = {t0.x, t0.y, t0.z, t0.w}, a1[4] = {t1.x, t1.y, t1.z, t1.w},
-                               a2[4] = {t2.x, t2.y, t2.z, t2.w};
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    w01[di][2 * q] = (a0[q] & 0xffffu) | (a1[q] << 16);
-                    w01[di][2 * q + 1] = (a0[q] >> 16) | (a1[q] & 0xffff0000u);
-                    w2[di][2 * q] = bf16lo(a2[q]);
-                    w2[di][2 * q + 1] = bf16hi(a2[q]);
-                }
+            for (int dj = 0; dj < 3; ++dj) {
+                const int x = j + dj - 1;
+                v[dj] = (x >= 0 && x < W) ? *reinterpret_cast<const uint4*>(xs + ((rr * W + x) * UH + u) * 16)
+                                          : make_uint4(0, 0, 0, 0);
             }
-            uint32_t pr[3][8];  // sliding window of rows: (x=j-1, x=j) pairs per channel
-            float sg[3][8];     // x=j+1 values per channel
-            auto load_row = [&](int rr, int slot) {
-                uint4 v[3];
+            const uint32_t b0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, b1[4] = {v[1].x, v[1].y, v[1].z, v[1].w},
+                           b2[4] = {v[2].x, v[2].y, v[2].z, v[2].w};
 #pragma unroll
-                for (int dj = 0; dj < 3; ++dj) {
-                    const int x = j + dj - 1;
-                    v[dj] = (x >= 0 && x < W) ? *reinterpret_cast<const uint4*>(xs + ((rr * W + x) * UH + u) * 16)
-                                              : make_uint4(0, 0, 0, 0);
-                }
-                const uint32_t b0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, b1[4] = {v[1].x, v[1].y, v[1].z, v[1].w},
-                               b2[4] = {v[2].x, v[2].y, v[2].z, v[2].w};
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    pr[slot][2 * q] = (b0[q] & 0xffffu) | (b1[q] << 16);
-                    pr[slot][2 * q + 1] = (b0[q] >> 16) | (b1[q] & 0xffff0000u);
-                    sg[slot][2 * q] = bf16lo(b2[q]);
-                    sg[slot][2 * q + 1] = bf16hi(b2[q]);
-                }
-            };
-            load_row(0, 0);
-            load_row(1, 1);
-#pragma unroll
-            for (int rl = 0; rl < R; ++rl) {
-                load_row(rl + 2, (rl + 2) % 3);
-                float acc[8];
-#pragma unroll
-                for (int c = 0; c < 8; ++c) {
-                    float a = 0.0f;
-#pragma unroll
-                    for (int di = 0; di < 3; ++di) {
-                        const int slot = (rl + di) % 3;
-                        a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pr[slot][c]),
-                                                            __builtin_bit_cast(bf16x2_t, w01[di][c]), a, false);
-                        a = fmaf(sg[slot][c], w2[di][c], a);
-                    }
-                    acc[c] = a;
-                }
-                const int px = rl * W + j;
-                *reinterpret_cast<uint4*>(sA + f_a_off(px, cv, a_row_bytes)) =
-                    make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
-                               pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
+            for (int q = 0; q < 4; ++q) {
+                pr[slot][2 * q] = (b0[q] & 0xffffu) | (b1[q] << 16);
+                pr[slot][2 * q + 1] = (b0[q] >> 16) | (b1[q] & 0xffff0000u);
+                sg[slot][2 * q] = bf16lo(b2[q]);
+                sg[slot][2 * q + 1] = bf16hi(b2[q]);
             }
+        };
+        load_row(0, 0);
+        load_row(1, 1);
+#pragma unroll
+        for (int rl = 0; rl < R; ++rl) {
+            load_row(rl + 2, (rl + 2) % 3);
+            float acc[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                float a = 0.0f;
+#pragma unroll
+                for (int di = 0; di < 3; ++di) {
+                    const int slot = (rl + di) % 3;
+                    a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pr[slot][c]),
+                                                        __builtin_bit_cast(bf16x2_t, w01[h][di][c]), a, false);
+                    a = fmaf(sg[slot][c], w2[h][di][c], a);
+                }
+                acc[c] = a;
+            }
+            const int px = rl * W + j;
+            *reinterpret_cast<uint4*>(sA + f_a_off(px, cv, a_row_bytes)) =
+                make_uint4(pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]),
+                           pack_bf16x2(acc[4], acc[5]), pack_bf16x2(acc[6], acc[7]));
         }
     };
     // Rows R*W .. 127 of the A tile stay zero for every tile.
@@ -224,11 +238,14 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
 
     for (; tile < n_tiles; tile += gridDim.x) {
         const int next = tile + (int)gridDim.x;
-        depthwise_half(0);
-        f_vm_wait<0>();            // half 1 of this tile (and earlier stores) done
+        depthwise_half(std::integral_constant<int, 0>{});
+        // Half 1 of this tile has landed once at most the previous tile's
+        // kStoresPerWave stores (issued after it) are still in flight.
+        if (tile == (int)blockIdx.x) f_vm_wait<0>();
+        else f_vm_wait<kStoresPerWave>();
         f_barrier();
         copy_half(next, 0);
-        depthwise_half(1);
+        depthwise_half(std::integral_constant<int, 1>{});
         f_barrier();               // A complete, buffer 1 free
         copy_half(next, 1);
 
@@ -292,14 +309,18 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
                     const int prow = wm * 64 + i * 32 + hh * 16 + r;
                     const int64_t col = wn * 64 + c4 * 4;
                     const float4 v4 = *reinterpret_cast<const float4*>(stage + r * 64 + c4 * 4);
-                    if (prow < valid_rows && col < C_out) {
-                        const int64_t idx = (m0 + prow) * C_out + col;
-                        if constexpr (sizeof(TO) == 4)
-                            *reinterpret_cast<float4*>(static_cast<float*>(out) + idx) = v4;
-                        else
-                            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out) + idx) =
-                                make_uint2(pack_bf16x2(v4.x, v4.y), pack_bf16x2(v4.z, v4.w));
-                    }
+                    // Every lane issues its store (rows or columns outside the
+                    // output go to an offset past the buffer end and are
+                    // dropped), so each wave issues exactly kStoresPerWave.
+                    const bool ok = prow < valid_rows && col < C_out;
+                    const int64_t idx = (m0 + prow) * C_out + col;
+                    if constexpr (sizeof(TO) == 4)
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, v4), rsO,
+                                                               ok ? (int)(idx * 4) : (int)kOob, 0, 0);
+                    else
+                        __builtin_amdgcn_raw_buffer_store_b64(
+                            __builtin_bit_cast(u32x2_t, make_uint2(pack_bf16x2(v4.x, v4.y), pack_bf16x2(v4.z, v4.w))),
+                            rsO, ok ? (int)(idx * 2) : (int)kOob, 0, 0);
                 }
                 __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the slab is overwritten
                 __builtin_amdgcn_wave_barrier();
