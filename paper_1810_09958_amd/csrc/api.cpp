@@ -398,8 +398,9 @@ isam_status_t isam_dwsep_conv(int64_t batch, int64_t H, int64_t W, int64_t C_in,
     d.Wo = Wo;
     d.in_type = in_type;
     d.y_type = in_type;
-    // Fused path: the depthwise result stays in LDS and feeds the MFMA
-    // product directly (bf16 input, 3x3 stride 1 pad 1 shapes that fit).
+    // Fused paths: the depthwise result stays in LDS and feeds the MFMA
+    // product directly (bf16 input, or fp32 input and output; 3x3 stride 1
+    // pad 1 shapes that fit).
     const bool fused_off = getenv("ISAM_DWSEP_FUSED") && getenv("ISAM_DWSEP_FUSED")[0] == '0';
     if (!fused_off && !((uintptr_t)y & 15) && !((uintptr_t)pw_weight & 15)) {
         int dev = 0, lds_max = 0;
@@ -409,6 +410,11 @@ isam_status_t isam_dwsep_conv(int64_t batch, int64_t H, int64_t W, int64_t C_in,
             if (R > 0) {
                 if (log_enabled()) fprintf(stderr, "[isam] dwsep fused R=%d\n", R);
                 hipError_t e = launch_dwsep_fused(d, pw_weight, y, C_out, out_type, R, device_cus(), s);
+                return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
+            }
+            if (out_type == ISAM_F32 && dwsep_fused_f32_ok(d, C_out, lds_max)) {
+                if (log_enabled()) fprintf(stderr, "[isam] dwsep fused fp32\n");
+                hipError_t e = launch_dwsep_fused_f32(d, pw_weight, y, C_out, device_cus(), s);
                 return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
             }
         } else {

@@ -70,6 +70,9 @@ hipError_t launch_depthwise(const DwArgs& a, hipStream_t s);
 int dwsep_fused_rows(const DwArgs& d, int64_t C_out, int lds_max);
 hipError_t launch_dwsep_fused(const DwArgs& d, const void* pw, void* out, int64_t C_out, int out_type, int R,
                               int cus, hipStream_t s);
+// Fused depthwise + pointwise, fp32 in and out (fp32 MFMA).
+bool dwsep_fused_f32_ok(const DwArgs& d, int64_t C_out, int lds_max);
+hipError_t launch_dwsep_fused_f32(const DwArgs& d, const void* pw, void* out, int64_t C_out, int cus, hipStream_t s);
 
 // GRU recurrence (the input projection is a GemmArgs launch done before).
 struct GruArgs {

@@ -76,3 +76,12 @@ def test_fused_path_shapes(ot, C, Co):
     # widths for 4, 2 and 1 rows per tile, heights not a multiple of the rows per tile
     for (b, H, W) in [(2, 5, 7), (1, 9, 32), (2, 7, 56), (1, 3, 64), (1, 5, 100)]:
         _case(b, H, W, C, Co, dt="bf16", ot=ot, seed=H * W + C)
+
+
+@pytest.mark.parametrize("C,Co", [(32, 16), (64, 48), (96, 256), (128, 256), (128, 112)])
+def test_fused_f32_path_shapes(C, Co):
+    # fp32 3x3 stride-1 pad-1 shapes taken by the fused fp32 kernel (W % 8 == 0,
+    # W <= 64): one to eight 16-pixel tiles per 2-row tile, odd heights (a
+    # partial last tile), C_out below 256 (idle waves)
+    for (b, H, W) in [(2, 5, 8), (1, 9, 16), (2, 7, 56), (1, 3, 64), (1, 4, 24)]:
+        _case(b, H, W, C, Co, dt="f32", ot="f32", seed=H * W + C + Co)
