@@ -511,7 +511,7 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
             if (lds > (size_t)lds_max) break;
             const int64_t wgs = (H / cand) * n_bg;
             const int per_cu = pass == 0 ? 1 : gru_blocks_per_cu(w_type, lds);
-            if (wgs <= (int64_t)cus * per_cu && H / cand <= 31 * 16) { J = cand; n_wg = (int)wgs; break; }
+            if (wgs <= (int64_t)cus * per_cu) { J = cand; n_wg = (int)wgs; break; }
         }
     }
     if (!J) return fail(ISAM_ERR_UNSUPPORTED, "%s: no resident tiling for hidden=%lld batch=%lld on %d CUs",
@@ -520,7 +520,7 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
         const int v = atoi(env);
         const size_t lds = (v >= 1 && v <= 16) ? gru_lds_bytes(w_type, H, v) : 0;
         if (v >= 1 && v <= 16 && H % v == 0 && v * BB <= 256 && lds <= (size_t)lds_max &&
-            (H / v) * n_bg <= (int64_t)cus * std::min(2, gru_blocks_per_cu(w_type, lds)) && H / v <= 31 * 16) {
+            (H / v) * n_bg <= (int64_t)cus * std::min(2, gru_blocks_per_cu(w_type, lds))) {
             J = v;
             n_wg = (int)((H / v) * n_bg);
         }
@@ -560,6 +560,9 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     g.units_per_wg = J;
     g.batch_per_wg = BB;
     g.n_wg = n_wg;
+    // First-level barrier groups of 8 workgroups (measured fastest), larger
+    // when a domain would otherwise need more group counters than it has.
+    g.barrier_group = (int)std::max<int64_t>(8, cdiv(H / J, kGruMaxGroupsPerDomain));
     e = launch_gru_recurrent(g, s);
     if (e != hipSuccess) return hip_fail(e, who);
     return ISAM_OK;

@@ -60,19 +60,21 @@ __device__ __forceinline__ int u_chunk(int r, int c) { return c ^ (2 * (r & 7));
 // memory once per XCD instead of once per workgroup.
 //
 // The barrier is two-level to limit serialised atomics on one address:
-// workgroups arrive on a counter of their group of kGroup, the last arrival
+// workgroups arrive on a counter of their group (a.barrier_group members:
+// 8, or more when a domain would need more than 31 groups), the last arrival
 // of a group bumps the domain counter, and every workgroup polls the domain
 // counter.  All counters are monotonic over the steps of one launch (zeroed
 // by the init kernel).  Each wait is bounded in time; a timeout sets the
 // sticky error word, after which every wait returns at once.
-constexpr int kGroup = 16;
+
 constexpr int kSyncError = 0;           // word offsets; counters sit 64 bytes apart
 constexpr int kSyncDomainWords = 512;   // per batch group: global counter + group counters
 constexpr int kCpolDevice = 16;         // sc1: device-scope coherence
 
 // Workgroups of one batch group form a barrier domain: batch groups are
 // independent sequences, so they never wait for each other.
-__device__ __forceinline__ void grid_barrier(unsigned* sync, int64_t step, int domain, int member, int n_members) {
+__device__ __forceinline__ void grid_barrier(unsigned* sync, int64_t step, int domain, int member, int n_members,
+                                             int kGroup) {
     __syncthreads();
     if (threadIdx.x == 0) {
         unsigned* dom = sync + kSyncDomainWords * (1 + domain);
@@ -251,7 +253,7 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), rs_h, (int)(hn * 4), 0, kCpolDevice);
         }
         fetch_gx(t + 1);
-        if (t + 1 < a.T) grid_barrier(a.sync, t, bg, ug, n_ug);
+        if (t + 1 < a.T) grid_barrier(a.sync, t, bg, ug, n_ug, a.barrier_group);
     }
     if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
 }

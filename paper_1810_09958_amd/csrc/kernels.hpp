@@ -90,7 +90,12 @@ struct GruArgs {
     int units_per_wg;       // J
     int batch_per_wg;       // BB
     int n_wg;
+    int barrier_group;      // workgroups per first-level barrier counter
 };
+// Barrier layout of the GRU kernel: per batch group a domain of 512 words
+// holds the domain counter and up to 31 first-level group counters (64
+// bytes apart).
+constexpr int kGruMaxGroupsPerDomain = 31;
 size_t gru_lds_bytes(int w_type, int64_t H, int J);
 // Resident workgroups of the recurrent kernel per compute unit at this LDS size.
 int gru_blocks_per_cu(int w_type, size_t lds);
