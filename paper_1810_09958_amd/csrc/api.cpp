@@ -149,7 +149,9 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     } else if (tiles(kTile256x128) >= cus) {
         p.tile = kTile256x128;
     } else if (tiles(kTile128x128) >= cus) {
-        p.tile = kTile128x128;
+        // Shallow K with under two tiles per CU: the 128x64 grid balances
+        // better (measured: 2048x3072x1024 bf16 27 us vs 38 us).
+        p.tile = (K <= 2048 && tiles(kTile128x128) < 2 * (int64_t)cus) ? kTile128x64 : kTile128x128;
     } else if (tiles(kTile128x64) >= cus) {
         p.tile = kTile128x64;
     } else {
