@@ -13,8 +13,10 @@
 //      thread owns one channel vector of one column and reuses the vertical
 //      window in registers; taps are paired for v_dot2_f32_bf16), rounds it
 //      to bf16 and stores it as the A tile [128][C] in LDS;
-//   3. runs the [128 x C] . [C x 256] product on MFMA (A with ds_read_b128,
-//      P with ds_read_b64_tr_b16) and writes the output tile.
+//   3. runs the product on MFMA, transposed ([256 x C] . [C x 128]: P with
+//      ds_read_b64_tr_b16 as the A operand, the tile with ds_read_b128 as
+//      the B operand) and writes the output channels of each pixel straight
+//      from the accumulators.
 // Supported: bf16 input, 3x3, stride 1, pad 1, depth multiplier 1,
 // C in {64, 128}, C_out % 8 == 0, C_out <= 256, W <= 128 / R, and
 // the LDS footprint within the device limit; everything else uses the
@@ -76,10 +78,10 @@ __device__ __forceinline__ void f_barrier() {
 }
 
 constexpr int kFWaves = 8;
-constexpr int kARegion = 32768;        // A tile (<= 128 x 128 bf16), also 8 x 4 KiB store staging
+constexpr int kARegion = 32768;        // A tile (<= 128 x 128 bf16)
 constexpr int kXBuf = 32768;           // bytes of one input half-tile buffer
 constexpr int kXInstr = kXBuf / 1024 / kFWaves;  // copies per wave per half (4)
-constexpr int kStoresPerWave = 16;     // output stores per wave per tile (MI x 2 slabs x 4)
+constexpr int kStoresPerWave = 16;     // output stores per wave per tile (MI x NI x 4)
 
 // Persistent form: one workgroup per CU walks its tiles (tile = R output rows
 // of one image).  LDS: P [C][256] (copied once) | A [128][C] | two buffers of
@@ -232,8 +234,14 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
     for (int q = R * W * (C / 8) + tid; q < kFBM * (C / 8); q += 64 * kFWaves)
         *reinterpret_cast<uint4*>(sA + f_a_off(q / (C / 8), q % (C / 8), a_row_bytes)) = make_uint4(0, 0, 0, 0);
 
-    constexpr int MI = 2, NI = 2;  // wave tile 64 x 64; waves 2 (M) x 4 (N)
-    const int wm = wid >> 2, wn = wid & 3;
+    // The product is formed transposed, out^T[cout][pixel] = P^T . A^T: the
+    // P fragments (read with ds_read_b64_tr_b16) are the MFMA A operand and
+    // the pixel fragments of the A tile (ds_read_b128) the B operand, so each
+    // accumulator holds 4 consecutive output channels of one pixel and goes
+    // straight to memory as one 16-byte (fp32) or 8-byte (bf16) store.
+    // Waves: 4 blocks of 64 output channels x 2 blocks of 64 pixels.
+    constexpr int MI = 2, NI = 2;  // wave tile 64 couts x 64 pixels
+    const int cb = wid & 3, pb = wid >> 2;
     const int g = lane >> 4, li = lane & 15;
 
     for (; tile < n_tiles; tile += gridDim.x) {
@@ -256,13 +264,10 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
             });
         });
         for (int ks = 0; ks < C / 16; ++ks) {
-            uint4 af[MI], bfr[NI];
+            uint4 pf[MI], yf[NI];
             const int ch = ks * 2 + (lane >> 5);
             static_for<MI>([&](auto i) {
-                af[i] = *reinterpret_cast<const uint4*>(sA + f_a_off(wm * 64 + i * 32 + (lane & 31), ch, a_row_bytes));
-            });
-            static_for<NI>([&](auto jj) {
-                const int n = wn * 64 + jj * 32 + (g & 1) * 16 + 4 * (li & 3);
+                const int n = cb * 64 + i * 32 + (g & 1) * 16 + 4 * (li & 3);
                 uint32_t w[4];
                 static_for<2>([&](auto rr) {
                     const int k = ks * 16 + (g >> 1) * 8 + rr * 4 + (li >> 2);
@@ -271,62 +276,49 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
                     w[rr * 2] = uu.x;
                     w[rr * 2 + 1] = uu.y;
                 });
-                bfr[jj] = make_uint4(w[0], w[1], w[2], w[3]);
+                pf[i] = make_uint4(w[0], w[1], w[2], w[3]);
+            });
+            static_for<NI>([&](auto jj) {
+                yf[jj] = *reinterpret_cast<const uint4*>(sA + f_a_off(pb * 64 + jj * 32 + (lane & 31), ch, a_row_bytes));
             });
             static_for<MI>([&](auto i) {
-                static_for<NI>([&](auto jj) { mfma32_bf16(acc[i][jj], af[i], bfr[jj]); });
+                static_for<NI>([&](auto jj) { mfma32_bf16(acc[i][jj], pf[i], yf[jj]); });
             });
         }
-        // Next tile's half 0 (issued before this wave's half-1 copies) must
-        // have landed before the next depthwise; loads complete in order.
+        // Every wave is done reading the A tile before the next depthwise
+        // overwrites it; the next tile's half 0 (issued before this wave's
+        // half-1 copies) has landed.
         f_vm_wait<kXInstr>();
         f_barrier();
 
-        // Store this tile through LDS: the A tile is consumed, so each wave
-        // stages 16-row x 64-column fp32 slabs of its block in its own 4 KiB
-        // of the A region and writes them back as 16-byte row segments
-        // (rows are the tile's pixels, contiguous in NHWC).
+        // Store: accumulator element v of lane l is output channel
+        // cb*64 + i*32 + 8*(v/4) + 4*(l/32) + v%4 of pixel pb*64 + jj*32 + l%32.
+        // Every lane issues its stores (pixels past the tile's valid rows and
+        // channels past C_out go to an offset beyond the buffer and are
+        // dropped), so each wave issues exactly kStoresPerWave.
         const int b = tile / tiles_per_img, i0 = (tile % tiles_per_img) * R;
         const int valid_rows = min(R, H - i0) * W;
         const int64_t m0 = ((int64_t)b * H + i0) * W;
-        float* stage = reinterpret_cast<float*>(sA + wid * 4096);  // [16][64] fp32
         static_for<MI>([&](auto i) {
-            static_for<2>([&](auto hh) {
-                // rows 16*hh .. 16*hh+15 of the 32-row block i: accumulator elements 8*hh .. 8*hh+7
-                static_for<NI>([&](auto jj) {
-                    static_for<8>([&](auto vc) {
-                        constexpr int vv = 8 * decltype(hh)::value + decltype(vc)::value;
-                        const int r = 8 * ((vv >> 2) & 1) + 4 * (lane >> 5) + (vv & 3);
-                        stage[r * 64 + jj * 32 + (lane & 31)] = acc[i][jj][vv];
-                    });
-                });
-                __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the wave's slab is in LDS
-                __builtin_amdgcn_wave_barrier();
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int q = lane + 64 * k;
-                    const int r = q >> 4, c4 = q & 15;
-                    const int prow = wm * 64 + i * 32 + hh * 16 + r;
-                    const int64_t col = wn * 64 + c4 * 4;
-                    const float4 v4 = *reinterpret_cast<const float4*>(stage + r * 64 + c4 * 4);
-                    // Every lane issues its store (rows or columns outside the
-                    // output go to an offset past the buffer end and are
-                    // dropped), so each wave issues exactly kStoresPerWave.
-                    const bool ok = prow < valid_rows && col < C_out;
-                    const int64_t idx = (m0 + prow) * C_out + col;
+            static_for<NI>([&](auto jj) {
+                static_for<4>([&](auto v4c) {
+                    constexpr int v4 = decltype(v4c)::value;
+                    const int px = pb * 64 + jj * 32 + (lane & 31);
+                    const int64_t co = cb * 64 + i * 32 + 8 * v4 + 4 * (lane >> 5);
+                    const bool ok = px < valid_rows && co < C_out;
+                    const int64_t idx = (m0 + px) * C_out + co;
+                    const float x0 = acc[i][jj][4 * v4], x1 = acc[i][jj][4 * v4 + 1];
+                    const float x2 = acc[i][jj][4 * v4 + 2], x3 = acc[i][jj][4 * v4 + 3];
                     if constexpr (sizeof(TO) == 4)
-                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, v4), rsO,
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, make_float4(x0, x1, x2, x3)), rsO,
                                                                ok ? (int)(idx * 4) : (int)kOob, 0, 0);
                     else
                         __builtin_amdgcn_raw_buffer_store_b64(
-                            __builtin_bit_cast(u32x2_t, make_uint2(pack_bf16x2(v4.x, v4.y), pack_bf16x2(v4.z, v4.w))),
-                            rsO, ok ? (int)(idx * 2) : (int)kOob, 0, 0);
-                }
-                __builtin_amdgcn_s_waitcnt(0xc07f);  // reads done before the slab is overwritten
-                __builtin_amdgcn_wave_barrier();
+                            __builtin_bit_cast(u32x2_t, make_uint2(pack_bf16x2(x0, x1), pack_bf16x2(x2, x3))), rsO,
+                            ok ? (int)(idx * 2) : (int)kOob, 0, 0);
+                });
             });
         });
-        f_barrier();  // every wave is done with the A region before the next depthwise
     }
     f_vm_wait<0>();
 }
