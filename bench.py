@@ -7,6 +7,7 @@ HBM:
   * skinny GEMM 4096 x 32 x 4096, bf16 and fp32 inputs (fp32 out)
   * GRU forward T=64, batch 32, input = hidden = 1024, bf16 weights
   * separable depthwise conv 32 x 56 x 56 x 128 -> 256, bf16 (fp32 out) and fp32
+  * 1D convolution 32 sequences x 1024 positions, 512 -> 512 channels, 5 taps, bf16 (fp32 out)
   * fp32 GEMM 128^3
 Each part is bracketed by HIP events on the stream the library launches on (torch's current
 stream), so the per-part times are device times.  The HBM-bound parts (skinny GEMM, GRU,
@@ -223,6 +224,16 @@ def main():
                            "bytes": es * (32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + 4 * 100352 * 256})
     del d
 
+    # -- 1D convolution (second listing) as implicit GEMM --------------------------------
+    if want("conv1d_32x1024_512x5x512_bf16"):
+        w = workloads.conv1d()
+        cA, cB = gpu(w["A_bf16"]), gpu(w["B_bf16"])
+        del w
+        cC = torch.empty((32, 1024, 512), device=dev, dtype=torch.float32)
+        comps.append(("conv1d_32x1024_512x5x512_bf16", lambda: isam.conv1d(cA, cB, out=cC),
+                      {"kind": "gemm_bf16_ctx", "flop": 2.0 * 32 * 1024 * 512 * 5 * 512,
+                       "bytes": 2 * (32 * 1028 * 512 + 5 * 512 * 512) + 4 * 32 * 1024 * 512}))
+
     # -- small fp32 GEMM ------------------------------------------------------------------
     s1 = workloads.gemm_small_fp32()
     A1, B1 = gpu(s1["A"]), gpu(s1["B"])
@@ -270,7 +281,7 @@ def main():
         gbs = info["bytes"] / s / 1e9
         r["TFLOP/s"] = round(tfl, 2)
         r["GB/s"] = round(gbs, 1)
-        if info["kind"] == "gemm_bf16":
+        if info["kind"] in ("gemm_bf16", "gemm_bf16_ctx"):
             r["frac_bf16_peak"] = round(tfl / PEAK_BF16_TFLOPS, 4)
         elif info["kind"] == "gemm_f32":
             r["frac_f32_peak"] = round(tfl / PEAK_F32_TFLOPS, 6)

@@ -135,12 +135,32 @@ isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int
 size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_size,
                                        int64_t hidden_size, int w_type);
 
+/*
+ * 1D convolution of the paper's second listing (Section 2), valid positions,
+ * stride 1:
+ *   C[i][x][ko] (+)= sum_{d < D} sum_{ki < Ki} A[i][x+d][ki] * B[d][ki][ko]
+ * for x < X = L - D + 1.  Computed as the matrix-multiply mapping of Section
+ * 2.2 without materialising anything: per sequence i one product
+ * C_i[X][Ko] = A'_i[X][D*Ki] . B'[D*Ki][Ko], where row x of A'_i is the D*Ki
+ * contiguous values A[i][x .. x+D-1][:] (rows of A_i read with leading
+ * dimension Ki) and B' is B read as [D*Ki][Ko]; all sequences in one launch.
+ *
+ *   A  [batch][L][Ki]   (ab_type)        B  [D][Ki][Ko] (ab_type)
+ *   C  [batch][X][Ko]   (c_type), fp32 accumulation, bf16 output rounded RNE
+ * accumulate = 1 adds to C.  batch, Ko == 0 or X <= 0: no-op.  No workspace.
+ * Errors: INVALID_ARG (bad sizes or dtype, NULL tensor, C overlapping A or B),
+ * UNSUPPORTED (one sequence's A or C, or B, over 2^31 bytes; batch > 65535).
+ */
+isam_status_t isam_conv1d(int64_t batch, int64_t L, int64_t Ki, int64_t D, int64_t Ko, int ab_type,
+                          const void* A, const void* B, int accumulate, int c_type, void* C,
+                          void* stream);
+
 /* Static text for a status code. */
 const char* isam_status_string(int status);
 /* Detail of the last non-OK status returned on the calling thread ("" if none). */
 const char* isam_last_error(void);
 /* Library version, major*10000 + minor*100 + patch. */
-int isam_version(void);
+int isam_version(void);  /* 101: adds isam_conv1d */
 
 #ifdef __cplusplus
 }

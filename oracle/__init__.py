@@ -51,9 +51,10 @@ def lib():
         L.isam_ref_dwsep.argtypes = [i64] * 10 + [ci, vp, vp, vp, dp, dp, ci]
         L.isam_ref_dwsep_direct.argtypes = [i64] * 10 + [ci, vp, vp, vp, dp]
         L.isam_ref_gru.argtypes = [i64, i64, i64, i64, ci, vp, dp, vp, vp, fp, fp, dp, ci]
+        L.isam_ref_conv1d.argtypes = [i64] * 5 + [ci, vp, vp, dp, dp, dp, ci]
         L.isam_ref_max_threads.argtypes = []
         for f in ("isam_ref_gemm", "isam_ref_depthwise", "isam_ref_dwsep",
-                  "isam_ref_dwsep_direct", "isam_ref_gru", "isam_ref_max_threads"):
+                  "isam_ref_dwsep_direct", "isam_ref_gru", "isam_ref_conv1d", "isam_ref_max_threads"):
             getattr(L, f).restype = ci
         _lib = L
     return _lib
@@ -96,6 +97,26 @@ def gemm(A, B, M, N, K, trans_a=0, trans_b=0, lda=None, ldb=None, C_in=None,
     cin = None if C_in is None else np.ascontiguousarray(C_in, dtype=np.float64).reshape(M, N)
     _check(lib().isam_ref_gemm(trans_a, trans_b, M, N, K, dt, _ptr(A), lda, _ptr(B), ldb,
                                _ptr(cin), _ptr(C), _ptr(S), threads), "isam_ref_gemm")
+    return C, S
+
+
+def conv1d(A, B, C_in=None, with_norm=True, threads=0):
+    """1D convolution (the paper's second listing, valid positions, stride 1):
+    A [batch][L][Ki], B [D][Ki][Ko] -> (C, S) fp64 [batch][L-D+1][Ko]."""
+    A = np.ascontiguousarray(A)
+    B = np.ascontiguousarray(B)
+    dt = _dtype_of(A)
+    if _dtype_of(B) != dt:
+        raise TypeError("A and B must share one dtype")
+    nb, L, Ki = A.shape
+    D, Ki2, Ko = B.shape
+    assert Ki2 == Ki
+    X = max(L - D + 1, 0)
+    C = np.empty((nb, X, Ko), np.float64)
+    S = np.empty_like(C) if with_norm else None
+    cin = None if C_in is None else np.ascontiguousarray(C_in, dtype=np.float64).reshape(nb, X, Ko)
+    _check(lib().isam_ref_conv1d(nb, L, Ki, D, Ko, dt, _ptr(A), _ptr(B), _ptr(cin), _ptr(C), _ptr(S), threads),
+           "isam_ref_conv1d")
     return C, S
 
 

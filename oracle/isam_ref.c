@@ -92,6 +92,44 @@ int isam_ref_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int
 }
 
 /*
+ * 1D convolution, the paper's second listing (Section 2): for every sequence i,
+ * position x and output channel ko,
+ *   C[i][x][ko] = (C_in ? C_in[i][x][ko] : 0) + sum over d, ki of A[i][x+d][ki] * B[d][ki][ko]
+ * over the valid positions x < X = L - D + 1 (the listing has no padding and
+ * stride 1).  S (optional) is the same sum of |A| |B| (+ |C_in|).
+ *   A [batch][L][Ki], B [D][Ki][Ko], C, S [batch][X][Ko] fp64.
+ * Summation order: d ascending, then ki ascending.
+ */
+int isam_ref_conv1d(int64_t batch, int64_t L, int64_t Ki, int64_t D, int64_t Ko, int dtype,
+                    const void* A, const void* B, const double* C_in, double* C, double* S, int threads) {
+    if (batch < 0 || L < 0 || Ki <= 0 || D <= 0 || Ko < 0 || !C) return 1;
+    const int64_t X = L - D + 1;
+    if (batch == 0 || Ko == 0 || X <= 0) return 0;
+    set_threads(threads);
+#pragma omp parallel for collapse(2) schedule(dynamic, 4)
+    for (int64_t i = 0; i < batch; ++i) {
+        for (int64_t x = 0; x < X; ++x) {
+            for (int64_t ko = 0; ko < Ko; ++ko) {
+                const int64_t o = (i * X + x) * Ko + ko;
+                double acc = C_in ? C_in[o] : 0.0;
+                double nrm = C_in ? fabs(C_in[o]) : 0.0;
+                for (int64_t d = 0; d < D; ++d) {
+                    for (int64_t ki = 0; ki < Ki; ++ki) {
+                        const double a = ld_elem(A, dtype, (i * L + x + d) * Ki + ki);
+                        const double b = ld_elem(B, dtype, (d * Ki + ki) * Ko + ko);
+                        acc += a * b;
+                        nrm += fabs(a) * fabs(b);
+                    }
+                }
+                C[o] = acc;
+                if (S) S[o] = nrm;
+            }
+        }
+    }
+    return 0;
+}
+
+/*
  * Depthwise half of the separable depthwise convolution (third listing,
  * Section 2), after factoring the pointwise weight out of the (di, dj)
  * reduction (Section 2.3):

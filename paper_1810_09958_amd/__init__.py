@@ -16,7 +16,7 @@ import torch
 
 from ._lib import (ISAM_BF16, ISAM_F32, IsamError, lib, lib_path)
 
-__all__ = ["gemm", "dwsep_conv", "gru_forward", "gemm_workspace_size",
+__all__ = ["gemm", "conv1d", "dwsep_conv", "gru_forward", "gemm_workspace_size",
            "dwsep_conv_workspace_size", "gru_forward_workspace_size", "IsamError",
            "lib", "lib_path", "ISAM_F32", "ISAM_BF16", "version"]
 
@@ -52,6 +52,35 @@ def _call(rc, name):
 
 def version() -> int:
     return lib().isam_version()
+
+
+def conv1d(A: torch.Tensor, B: torch.Tensor, out: torch.Tensor | None = None, *, accumulate=False,
+           out_dtype=None):
+    """1D convolution (valid, stride 1): C[i][x][ko] (+)= sum_{d,ki} A[i][x+d][ki] * B[d][ki][ko].
+    A is [batch][L][Ki], B is [D][Ki][Ko], both contiguous and of one dtype; returns C
+    ([batch][L-D+1][Ko], float32 unless out_dtype / out say otherwise)."""
+    _check_dev(A, B, out)
+    if A.dim() != 3 or B.dim() != 3:
+        raise ValueError("A must be [batch][L][Ki] and B [D][Ki][Ko]")
+    if not A.is_contiguous() or not B.is_contiguous():
+        raise ValueError("A and B must be contiguous")
+    if A.dtype != B.dtype:
+        raise TypeError("A and B must share a dtype")
+    nb, L, Ki = A.shape
+    D, Ki2, Ko = B.shape
+    if Ki2 != Ki:
+        raise ValueError(f"channel counts differ: {Ki} vs {Ki2}")
+    X = max(L - D + 1, 0)
+    if out is None:
+        if accumulate:
+            raise ValueError("accumulate needs out")
+        out = torch.empty((nb, X, Ko), device=A.device, dtype=out_dtype or torch.float32)
+    elif tuple(out.shape) != (nb, X, Ko) or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous [{nb}][{X}][{Ko}] tensor")
+    rc = lib().isam_conv1d(nb, L, Ki, D, Ko, _dt(A), _ptr(A), _ptr(B), int(accumulate), _dt(out), _ptr(out),
+                           _stream())
+    _call(rc, "isam_conv1d")
+    return out
 
 
 def gemm_workspace_size(M, N, K, ab_type, c_type, trans_a=0, trans_b=0) -> int:

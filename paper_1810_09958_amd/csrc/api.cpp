@@ -247,8 +247,16 @@ isam_status_t validate_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int6
 isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type,
                        const void* A, int64_t lda, const void* B, int64_t ldb, int accumulate,
                        int c_type, void* C, int64_t ldc, const float* bias, void* workspace,
-                       size_t workspace_bytes, hipStream_t stream, const char* who) {
-    GemmPlan p = plan_gemm(M, N, K, ab_type, device_cus());
+                       size_t workspace_bytes, hipStream_t stream, const char* who, int64_t batch = 1,
+                       int64_t stride_a = 0, int64_t stride_b = 0, int64_t stride_c = 0) {
+    // A strided batch is planned as one product of batch*M rows (for the tile
+    // choice) and never split along K.
+    GemmPlan p = batch > 1 ? plan_gemm(M * batch, N, K, ab_type, device_cus(), /*allow_skinny=*/false)
+                           : plan_gemm(M, N, K, ab_type, device_cus());
+    if (batch > 1) {
+        p.k_splits = 1;
+        p.k_per_split = K;
+    }
     p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     if (p.skinny && (!p.vec || trans_a || trans_b || K == 0)) {
         p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
@@ -285,6 +293,10 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
     a.ab_type = ab_type;
     a.c_type = c_type;
     a.accumulate = accumulate;
+    a.batch = batch;
+    a.stride_a = stride_a;
+    a.stride_b = stride_b;
+    a.stride_c = stride_c;
     hipError_t e = launch_gemm(a, p, stream);
     if (e != hipSuccess) return hip_fail(e, who);
     return ISAM_OK;
@@ -570,6 +582,33 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     return ISAM_OK;
 }
 
+extern "C" isam_status_t isam_conv1d(int64_t batch, int64_t L, int64_t Ki, int64_t D, int64_t Ko, int ab_type,
+                                     const void* A, const void* B, int accumulate, int c_type, void* C,
+                                     void* stream) {
+    g_last_error.clear();
+    const char* who = "isam_conv1d";
+    if (batch < 0 || L < 0 || Ki <= 0 || D <= 0 || Ko < 0)
+        return fail(ISAM_ERR_INVALID_ARG, "%s: batch, L, Ko >= 0 and Ki, D > 0 required", who);
+    if (!valid_dtype(ab_type) || !valid_dtype(c_type)) return fail(ISAM_ERR_INVALID_ARG, "%s: bad dtype", who);
+    if (accumulate != 0 && accumulate != 1) return fail(ISAM_ERR_INVALID_ARG, "%s: accumulate must be 0 or 1", who);
+    const int64_t X = L - D + 1;  // valid output positions
+    if (batch == 0 || Ko == 0 || X <= 0) return ISAM_OK;
+    if (!A || !B || !C) return fail(ISAM_ERR_INVALID_ARG, "%s: NULL tensor", who);
+    const int64_t es = (int64_t)dsize(ab_type), cs = (int64_t)dsize(c_type);
+    const int64_t a_bytes = batch * L * Ki * es, b_bytes = D * Ki * Ko * es, c_bytes = batch * X * Ko * cs;
+    if (L * Ki * es > kMaxExtent || b_bytes > kMaxExtent || X * Ko * cs > kMaxExtent)
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: a tensor of one sequence spans more than 2^31 bytes", who);
+    if (batch > 65535) return fail(ISAM_ERR_UNSUPPORTED, "%s: more than 65535 sequences in one call", who);
+    if (overlaps(C, (size_t)c_bytes, A, (size_t)a_bytes) || overlaps(C, (size_t)c_bytes, B, (size_t)b_bytes))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: C overlaps A or B", who);
+    // Sequence i is one product C_i[X][Ko] = A'_i[X][D*Ki] . B'[D*Ki][Ko]: row x of
+    // A'_i is the D*Ki contiguous values A[i][x .. x+D-1][:], i.e. rows of A_i
+    // read with leading dimension Ki (consecutive rows overlap), and B' is B
+    // read as [D*Ki][Ko].
+    return run_gemm(0, 0, X, Ko, D * Ki, ab_type, A, Ki, B, Ko, accumulate, c_type, C, Ko, nullptr, nullptr, 0,
+                    static_cast<hipStream_t>(stream), who, batch, L * Ki * es, 0, X * Ko * cs);
+}
+
 extern "C" {
 
 const char* isam_status_string(int status) {
@@ -585,6 +624,6 @@ const char* isam_status_string(int status) {
 
 const char* isam_last_error(void) { return g_last_error.c_str(); }
 
-int isam_version(void) { return 100; }
+int isam_version(void) { return 101; }
 
 }  // extern "C"

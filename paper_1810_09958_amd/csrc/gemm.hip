@@ -96,6 +96,7 @@ hipError_t launch_splitk_reduce(const GemmArgs& a, int splits, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
+    if (a.batch > 1 && (p.k_splits > 1 || p.skinny)) return hipErrorInvalidValue;
     if (p.skinny == 2) return launch_skinny_rows(a, s);
     if (p.skinny) {
         hipError_t e = launch_skinny(a, p.k_splits, s);
@@ -122,7 +123,8 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     t.xcd_remap = p.xcd_remap;
     t.k_per_split = p.k_splits > 1 ? p.k_per_split : a.K;
     if (t.k_per_split <= 0) t.k_per_split = 1;
-    dim3 grid((unsigned)(t.tiles_m * t.tiles_n), (unsigned)(p.k_splits > 1 ? p.k_splits : 1));
+    dim3 grid((unsigned)(t.tiles_m * t.tiles_n), (unsigned)(p.k_splits > 1 ? p.k_splits : 1),
+              (unsigned)(a.batch > 1 ? a.batch : 1));
     dim3 block(threads);
     hipLaunchKernelGGL(fn, grid, block, 0, s, a, t);
     hipError_t e = hipGetLastError();

@@ -273,6 +273,7 @@ __device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc
 //            t+2 into stage t & 1
 template <int BM, int BN, bool TB, int WM = 2, int WN = 2>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
+    gemm_batch_offset(a);
     constexpr int NW = WM * WN, STAGES = 2, BK = 64;
     constexpr int WTM = BM / WM, WTN = BN / WN, MI = WTM / 32, NI = WTN / 32;
     constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128, STAGE = A_BYTES + B_BYTES;

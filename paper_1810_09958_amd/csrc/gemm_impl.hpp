@@ -155,8 +155,19 @@ __device__ __forceinline__ void map_tile(const TileMapArgs& t, int& tm, int& tn)
     tn = inner / gm;
 }
 
+// Problem blockIdx.z of a strided batch: offset the operand pointers.
+__device__ __forceinline__ void gemm_batch_offset(GemmArgs& a) {
+    if (a.batch > 1) {
+        const int64_t z = blockIdx.z;
+        a.A = static_cast<const char*>(a.A) + z * a.stride_a;
+        a.B = static_cast<const char*>(a.B) + z * a.stride_b;
+        a.C = static_cast<char*>(a.C) + z * a.stride_c;
+    }
+}
+
 template <typename T, int BM, int BN, int WM, int WN, bool TA, bool TB, bool VEC>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, TileMapArgs tmap) {
+    gemm_batch_offset(a);
     constexpr int NT = 64 * WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int MI = WTM / 32, NI = WTN / 32;

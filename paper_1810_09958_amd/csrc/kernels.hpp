@@ -23,6 +23,11 @@ struct GemmArgs {
     int ab_type;           // kF32 / kBF16
     int c_type;            // kF32 / kBF16
     int accumulate;        // C += instead of C =
+    // Strided batch (grid z): problem z uses A, B, C offset by z times these
+    // byte strides.  batch == 1 for a single product; batched launches never
+    // split K and never take the skinny kernels.
+    int64_t batch;
+    int64_t stride_a, stride_b, stride_c;
 };
 
 // Tile configurations of the MFMA tile kernel (see gemm.hip).

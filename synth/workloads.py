@@ -1,4 +1,4 @@
-"""Input recipes for the five benchmark workloads (seed 0, one stream per tensor).
+"""Input recipes for the benchmark workloads (seed 0, one stream per tensor).
 
 Each builder returns host numpy arrays: fp32 values and, where the workload is
 bf16, the bf16 bit patterns (uint16) obtained by RNE from those fp32 values.
@@ -67,6 +67,16 @@ def gemm_square_bf16(seed=SEED):
 
 def gemm_rect_bf16(seed=SEED):
     return gemm_large_bf16(8192, 1024, 16384, streams=(2, 3), seed=seed)
+
+
+def conv1d(batch=32, X=1024, Ki=512, D=5, Ko=512, seed=SEED):
+    """1D convolution (the paper's second listing) at a speech-model-like size:
+    A [batch][X+D-1][Ki] normal(0, 1), B [D][Ki][Ko] uniform[-1/sqrt(D*Ki), +); fp32 and bf16."""
+    L = X + D - 1
+    A = normal(seed, 0, (batch, L, Ki))
+    r = 1.0 / math.sqrt(D * Ki)
+    B = uniform(seed, 1, (D, Ki, Ko), -r, r)
+    return {"A": A, "B": B, "A_bf16": to_bf16_bits(A), "B_bf16": to_bf16_bits(B)}
 
 
 def rows_sample(M: int, count: int, seed: int = 1234) -> np.ndarray:

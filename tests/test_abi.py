@@ -139,3 +139,25 @@ def test_gru_workspace_query(L):
     n = L.isam_gru_forward_workspace_size(64, 32, 1024, 1024, BF16)
     assert n >= 64 * 32 * 3 * 1024 * 4 + 2 * 32 * 1024 * 2
     assert gru(L, B=0) == OK
+
+
+def conv1d(L, nb=2, Ln=10, Ki=8, D=3, Ko=8, ab=F32, A=FAKE, B=FAKE2, acc=0, ct=F32,
+           C=ctypes.c_void_p(0x70000000)):
+    return L.isam_conv1d(nb, Ln, Ki, D, Ko, ab, A, B, acc, ct, C, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    ({"Ki": 0}, INVALID), ({"D": 0}, INVALID), ({"nb": -1}, INVALID), ({"Ko": -1}, INVALID),
+    ({"ab": 2}, INVALID), ({"ct": 5}, INVALID), ({"acc": 2}, INVALID),
+    ({"A": None}, INVALID), ({"C": None}, INVALID),
+    ({"C": FAKE}, INVALID),                           # C overlaps A
+    ({"nb": 70000, "Ln": 4, "Ki": 4, "D": 1, "Ko": 4}, UNSUPPORTED),
+])
+def test_conv1d_validation(L, kw, code):
+    assert conv1d(L, **kw) == code
+
+
+def test_conv1d_noops(L):
+    assert conv1d(L, nb=0, A=None, B=None, C=None) == OK
+    assert conv1d(L, Ko=0, A=None, B=None, C=None) == OK
+    assert conv1d(L, Ln=2, D=3, A=None, B=None, C=None) == OK   # no valid position
