@@ -5,7 +5,7 @@ HBM:
   * bf16 GEMM 8192 x 8192 x 8192, bf16 and fp32 outputs
   * bf16 GEMM M=8192 N=1024 K=16384, bf16 and fp32 outputs
   * skinny GEMM 4096 x 32 x 4096, bf16 and fp32 inputs (fp32 out)
-  * GRU forward T=64, batch 32, input = hidden = 1024, bf16 weights
+  * GRU forward T=64, batch 32, input = hidden = 1024, bf16 weights (also T=128 and batch 4)
   * separable depthwise conv 32 x 56 x 56 x 128 -> 256, bf16 (fp32 out) and fp32
   * 1D convolution 32 sequences x 1024 positions, 512 -> 512 channels, 5 taps, bf16 (fp32 out)
   * fp32 GEMM 128^3
@@ -204,6 +204,21 @@ def main():
                     sets, {"kind": "gru", "steps": T,
                            "flop": 2.0 * T * Bt * 3 * H * (I + H),
                            "bytes": 2 * (3 * H * I + 3 * H * H + T * Bt * I) + 4 * T * Bt * H})
+
+    # GRU variants (context points): the paper's 128 steps; a small batch.
+    for (gT, gB, gname) in [(128, 32, "gru_T128_B32_H1024_bf16"), (64, 4, "gru_T64_B4_H1024_bf16")]:
+        if not want(gname):
+            continue
+        g = workloads.gru(T=gT, batch=gB)
+        vx, vW, vU, vb = gpu(g["x_bf16"]), gpu(g["W_bf16"]), gpu(g["U_bf16"]), gpu(g["bias"])
+        del g
+        vh = torch.empty((gT, gB, H), device=dev)
+        vT = torch.empty((gB, H), device=dev)
+        vws = torch.empty(isam.gru_forward_workspace_size(gT, gB, I, H, 1), device=dev, dtype=torch.uint8)
+        comps.append((gname, (lambda vx=vx, vW=vW, vU=vU, vb=vb, vh=vh, vT=vT, vws=vws:
+                              isam.gru_forward(vx, vW, vU, bias=vb, h_seq=vh, h_T=vT, workspace=vws)),
+                      {"kind": "gru", "steps": gT, "flop": 2.0 * gT * gB * 3 * H * (I + H),
+                       "bytes": 2 * (3 * H * I + 3 * H * H + gT * gB * I) + 4 * gT * gB * H}))
 
     # -- separable depthwise conv -------------------------------------------------------
     d = workloads.dwsep()

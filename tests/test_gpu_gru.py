@@ -113,3 +113,9 @@ def test_config_full_size_sampled_sequences(variant):
     got = hs[:, seqs].cpu().numpy().astype(np.float64)
     err = float(np.max(np.abs(got - ref)))
     assert err <= (TOL_BF16 if variant == "bf16" else TOL_F32), err
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_paper_step_count_128(dt):
+    # 128 recurrent steps (the paper's sequence length) through one persistent launch
+    _run(128, 8, 128, 256, dt, seed=128, with_h0=True, scale=1 / 8)
