@@ -222,21 +222,25 @@ def main():
 
     # -- separable depthwise conv -------------------------------------------------------
     d = workloads.dwsep()
-    for name, X_h, D_h, P_h, es in [("dwsep_32x56x56x128_256_bf16_out_f32", d["X_bf16"], d["D_bf16"], d["P_bf16"], 2),
-                                    ("dwsep_32x56x56x128_256_f32", d["X"], d["D"], d["P"], 4)]:
+    for name, X_h, D_h, P_h, es, oes in [
+            ("dwsep_32x56x56x128_256_bf16_out_f32", d["X_bf16"], d["D_bf16"], d["P_bf16"], 2, 4),
+            ("dwsep_32x56x56x128_256_bf16_out_bf16", d["X_bf16"], d["D_bf16"], d["P_bf16"], 2, 2),
+            ("dwsep_32x56x56x128_256_f32", d["X"], d["D"], d["P"], 4, 4)]:
         if not want(name):
             continue
         X0, Dw, P = gpu(X_h), gpu(D_h), gpu(P_h)
-        sets = n_sets(X0.numel() * es + 4 * 100352 * 256)
+        sets = n_sets(X0.numel() * es + oes * 100352 * 256)
         Xs = [X0] + [X0.clone() for _ in range(sets - 1)]
-        ys = [torch.empty((32, 56, 56, 256), device=dev, dtype=torch.float32) for _ in range(sets)]
+        ys = [torch.empty((32, 56, 56, 256), device=dev, dtype=torch.float32 if oes == 4 else torch.bfloat16)
+              for _ in range(sets)]
         it = 1 if es == 2 else 0
-        ws = torch.empty(isam.dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, it, 0),
+        ot = 0 if oes == 4 else 1
+        ws = torch.empty(isam.dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, it, ot),
                          device=dev, dtype=torch.uint8)
         add_rotated(name, lambda i, Xs=Xs, Dw=Dw, P=P, ys=ys, ws=ws: (lambda: isam.dwsep_conv(Xs[i], Dw, P, out=ys[i], workspace=ws)),
                     sets, {"kind": "dwsep", "flop": 2.0 * 100352 * (9 * 128 + 128 * 256),
                            # fused minimum: X read once, y written once (+ the small filters)
-                           "bytes": es * (32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + 4 * 100352 * 256})
+                           "bytes": es * (32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + oes * 100352 * 256})
     del d
 
     # -- 1D convolution (second listing) as implicit GEMM --------------------------------

@@ -423,7 +423,7 @@ isam_status_t isam_dwsep_conv(int64_t batch, int64_t H, int64_t W, int64_t C_in,
             const int R = dwsep_fused_rows(d, C_out, lds_max);
             if (R > 0) {
                 if (log_enabled()) fprintf(stderr, "[isam] dwsep fused R=%d\n", R);
-                hipError_t e = launch_dwsep_fused(d, pw_weight, y, C_out, out_type, R, device_cus(), s);
+                hipError_t e = launch_dwsep_fused(d, pw_weight, y, C_out, out_type, lds_max, device_cus(), s);
                 return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
             }
             if (out_type == ISAM_F32 && dwsep_fused_f32_ok(d, C_out, lds_max)) {

@@ -73,7 +73,7 @@ struct DwArgs {
 hipError_t launch_depthwise(const DwArgs& a, hipStream_t s);
 // Fused depthwise + pointwise (bf16 input): rows per tile, 0 if not applicable.
 int dwsep_fused_rows(const DwArgs& d, int64_t C_out, int lds_max);
-hipError_t launch_dwsep_fused(const DwArgs& d, const void* pw, void* out, int64_t C_out, int out_type, int R,
+hipError_t launch_dwsep_fused(const DwArgs& d, const void* pw, void* out, int64_t C_out, int out_type, int lds_max,
                               int cus, hipStream_t s);
 // Fused depthwise + pointwise, fp32 in and out (fp32 MFMA).
 bool dwsep_fused_f32_ok(const DwArgs& d, int64_t C_out, int lds_max);

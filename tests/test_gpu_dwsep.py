@@ -78,6 +78,15 @@ def test_fused_path_shapes(ot, C, Co):
         _case(b, H, W, C, Co, dt="bf16", ot=ot, seed=H * W + C)
 
 
+@pytest.mark.parametrize("ot", ["f32", "bf16"])
+def test_fused_tile_ranges_cross_images(ot):
+    # More tiles than CUs: each workgroup walks a contiguous range of tiles that
+    # crosses image boundaries (the input-row sequence restarts), and with 8-9
+    # two-row tiles per workgroup the 16-row input ring wraps.
+    _case(60, 5, 56, 128, 256, dt="bf16", ot=ot, seed=7)
+    _case(150, 28, 16, 64, 40, dt="bf16", ot=ot, seed=8)
+
+
 @pytest.mark.parametrize("C,Co", [(32, 16), (64, 48), (96, 256), (128, 256), (128, 112)])
 def test_fused_f32_path_shapes(C, Co):
     # fp32 3x3 stride-1 pad-1 shapes taken by the fused fp32 kernel (W % 8 == 0,
