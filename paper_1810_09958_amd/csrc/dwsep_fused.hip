@@ -9,12 +9,13 @@
 // all but R of their R+2 input rows.  The 8 waves are specialised:
 //   * producer waves 0-3 each own a quarter of the channels.  A wave streams
 //     its channel slice of every input row it needs into a private LDS ring
-//     (buffer_load ... lds, rows outside the image arrive as zeros), up to
-//     the ring's depth ahead, computes the depthwise result of its channels
-//     for the tile in fp32 (taps in registers, the two left taps of a row
-//     paired for v_dot2_f32_bf16), rounds it to bf16 and writes it into one
-//     of two A tiles [64 px][C].  Depthwise is per channel, so a producer
-//     reads only what it copied itself and waits only on its own copies.
+//     (buffer_load ... lds; each row with a zero column on either side, rows
+//     outside the image arrive as zeros), up to the ring's depth ahead,
+//     computes the depthwise result of its channels for the tile in fp32
+//     (taps in registers, the two left taps of a row paired for
+//     v_dot2_f32_bf16), rounds it to bf16 and writes it into one of two A
+//     tiles [64 px][C].  Depthwise is per channel, so a producer reads only
+//     what it copied itself and waits only on its own copies.
 //   * consumer waves 4-7 each own 64 output channels, keep that slice of P
 //     in registers for the whole launch, form out^T = P^T . A^T on MFMA
 //     (P fragments as the A operand, pixel fragments of the A tile read with
@@ -38,7 +39,9 @@ typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned u32x2_t __attribute__((vector_size(2 * sizeof(unsigned))));
 
-constexpr int kFWaves = 8;       // 4 producer + 4 consumer waves
+constexpr int kProducers = 4;    // depthwise waves, a quarter of the channels each
+constexpr int kConsumers = 4;    // MFMA + store waves, 64 output channels each
+constexpr int kFWaves = kProducers + kConsumers;
 constexpr int kFPix = 64;        // MFMA pixel columns per tile
 constexpr int kFBN = 256;        // output channels (4 consumer waves x 64)
 constexpr int kMaxSlots = 16;    // input rows per producer ring
@@ -104,11 +107,11 @@ __device__ __forceinline__ void f_barrier() {
 template <int C>
 constexpr int a_tile_bytes() { return kFPix * C * 2; }
 
-template <int R, int C, typename TO>
-__global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, const void* pw, void* out,
+template <int R, int C, typename TO, int NP = kProducers>
+__global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwArgs d, const void* pw, void* out,
                                                                    int64_t C_out, int n_slots, int row_instr) {
     extern __shared__ __attribute__((aligned(1024))) char smem[];
-    constexpr int UPW = C / 32;      // 16-byte channel units per producer wave
+    constexpr int UPW = C / (8 * NP);  // 16-byte channel units per producer wave
     constexpr int CPP = 64 / UPW;    // columns per producer pass
     constexpr int KS = C / 16;       // MFMA K steps
     constexpr int kA = a_tile_bytes<C>();
@@ -127,8 +130,8 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
     const __amdgpu_buffer_rsrc_t rsX = make_rsrc(d.x, (uint32_t)(d.batch * (int64_t)H * W * C * 2));
     const __amdgpu_buffer_rsrc_t rsO =
         make_rsrc(out, (uint32_t)(d.batch * (int64_t)H * W * C_out * (int64_t)sizeof(TO)));
-    const bool producer = wid < 4;
-    const int pw4 = wid & 3;  // producer index / consumer index
+    const bool producer = wid < NP;
+    const int pw4 = producer ? wid : wid - NP;  // producer index / consumer index
 
     // Producer lane: channel unit ug (8 channels) of columns jl, jl + CPP, ...
     // Its taps are fixed: (di, 0) and (di, 1) paired as bf16x2, (di, 2) fp32.
@@ -157,9 +160,9 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
         char* dst = ring + nx_slot * slot_bytes;
         const bool row_ok = ir >= 0 && ir < H;
         for (int q = 0; q < row_instr; ++q) {
-            const int v = q * 64 + lane;
-            const int x = v / UPW, u = v % UPW;
-            const bool ok = row_ok && x < W;
+            const int v = q * 64 + lane;  // unit v holds column v / UPW - 1: zero halo at -1 and W
+            const int x = v / UPW - 1, u = v % UPW;
+            const bool ok = row_ok && x >= 0 && x < W;
             const uint32_t off =
                 ok ? (uint32_t)(((((int64_t)img * H + ir) * W + x) * C + (pw4 * UPW + u) * 8) * 2) : kOob;
             f_dma16(rsX, __builtin_amdgcn_readfirstlane(f_lds_addr(dst + q * 1024)), off);
@@ -173,6 +176,11 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
     };
 
     if (producer) {
+        // The rings do not overlap the P staging: stream the first tile's
+        // rows at once, then load the taps (the compiler's wait for them
+        // also covers those rows, which the first tile needs anyway), then
+        // fill the rest of the ring.
+        while (nx_tile < n_local && issued < R + 2) issue_row();
         const uint16_t* wp = static_cast<const uint16_t*>(d.w);
 #pragma unroll
         for (int di = 0; di < 3; ++di) {
@@ -189,7 +197,11 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
                 w2[di][2 * q + 1] = bf16hi(a2[q]);
             }
         }
-        // The rings do not overlap the P staging: start streaming rows now.
+        // Pin the taps here, before the next copies are issued.
+#pragma unroll
+        for (int di = 0; di < 3; ++di)
+#pragma unroll
+            for (int c = 0; c < 8; ++c) asm volatile("" : : "v"(w01[di][c]), "v"(w2[di][c]));
         while (nx_tile < n_local && issued < n_slots) issue_row();
     } else {
         // Stage this wave's P slice [C][64] (columns past C_out read as zero),
@@ -235,63 +247,71 @@ __global__ __launch_bounds__(64 * kFWaves) void dwsep_fused_kernel(DwArgs d, con
             f_vm_wait_rt((issued - e) * row_instr);  // rows up to e - 1 have landed
 
             char* A = sA + (t & 1) * kA;
-            int slot0 = first % n_slots;
-            for (int cp = 0; cp * CPP < W; ++cp) {
+            const char* rowp[R + 2];  // this tile's input rows in the ring
+#pragma unroll
+            for (int k = 0; k < R + 2; ++k) {
+                int sl = first % n_slots + k;
+                if (sl >= n_slots) sl -= n_slots;
+                rowp[k] = ring + sl * slot_bytes;
+            }
+            // Column passes of CPP columns each.
+            uint4 v[R + 2][3];
+            auto load_pass = [&](int cp, uint4 (&dst)[R + 2][3]) {
+                // columns j-1 .. j+1 sit at units (j + dj) * UPW (the halo
+                // makes every read unconditional); idle lanes read column W-1
+                const int j = min(cp * CPP + jl, W - 1);
+#pragma unroll
+                for (int k = 0; k < R + 2; ++k)
+#pragma unroll
+                    for (int dj = 0; dj < 3; ++dj)
+                        dst[k][dj] = *reinterpret_cast<const uint4*>(rowp[k] + ((j + dj) * UPW + ul) * 16);
+            };
+            auto compute_pass = [&](int cp, const uint4 (&src)[R + 2][3]) {
                 const int j = cp * CPP + jl;
-                if (j < W) {
-                    uint32_t pr[3][8];  // per row: (x=j-1, x=j) pairs per channel
-                    float sg[3][8];     // per row: x=j+1 per channel
-                    auto load_row = [&](int k, int slot_i) {
-                        int sl = slot0 + k;
-                        if (sl >= n_slots) sl -= n_slots;
-                        const char* rp = ring + sl * slot_bytes;
-                        uint4 v[3];
+                if (j >= W) return;
+                uint32_t pr[R + 2][8];  // per row: (x=j-1, x=j) pairs per channel
+                float sg[R + 2][8];     // per row: x=j+1 per channel
 #pragma unroll
-                        for (int dj = 0; dj < 3; ++dj) {
-                            const int x = j + dj - 1;
-                            v[dj] = (x >= 0 && x < W) ? *reinterpret_cast<const uint4*>(rp + (x * UPW + ul) * 16)
-                                                      : make_uint4(0, 0, 0, 0);
-                        }
-                        const uint32_t b0[4] = {v[0].x, v[0].y, v[0].z, v[0].w},
-                                       b1[4] = {v[1].x, v[1].y, v[1].z, v[1].w},
-                                       b2[4] = {v[2].x, v[2].y, v[2].z, v[2].w};
+                for (int k = 0; k < R + 2; ++k) {
+                    const uint32_t b0[4] = {src[k][0].x, src[k][0].y, src[k][0].z, src[k][0].w},
+                                   b1[4] = {src[k][1].x, src[k][1].y, src[k][1].z, src[k][1].w},
+                                   b2[4] = {src[k][2].x, src[k][2].y, src[k][2].z, src[k][2].w};
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            pr[slot_i][2 * q] = __builtin_amdgcn_perm(b1[q], b0[q], 0x05040100u);
-                            pr[slot_i][2 * q + 1] = __builtin_amdgcn_perm(b1[q], b0[q], 0x07060302u);
-                            sg[slot_i][2 * q] = bf16lo(b2[q]);
-                            sg[slot_i][2 * q + 1] = bf16hi(b2[q]);
-                        }
-                    };
-                    load_row(0, 0);
-                    load_row(1, 1);
-#pragma unroll
-                    for (int rl = 0; rl < R; ++rl) {
-                        load_row(rl + 2, (rl + 2) % 3);
-                        float acc[8];
-#pragma unroll
-                        for (int c = 0; c < 8; ++c) {
-                            float a = 0.0f;
-#pragma unroll
-                            for (int di = 0; di < 3; ++di) {
-                                const int sl = (rl + di) % 3;
-                                a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pr[sl][c]),
-                                                                    __builtin_bit_cast(bf16x2_t, w01[di][c]), a, false);
-                                a = fmaf(sg[sl][c], w2[di][c], a);
-                            }
-                            acc[c] = a;
-                        }
-                        *reinterpret_cast<uint4*>(A + f_a_off<C>(rl * W + j, ug)) =
-                            make_uint4(f_pack_bf16(acc[0], acc[1]), f_pack_bf16(acc[2], acc[3]),
-                                       f_pack_bf16(acc[4], acc[5]), f_pack_bf16(acc[6], acc[7]));
+                    for (int q = 0; q < 4; ++q) {
+                        pr[k][2 * q] = __builtin_amdgcn_perm(b1[q], b0[q], 0x05040100u);
+                        pr[k][2 * q + 1] = __builtin_amdgcn_perm(b1[q], b0[q], 0x07060302u);
+                        sg[k][2 * q] = bf16lo(b2[q]);
+                        sg[k][2 * q + 1] = bf16hi(b2[q]);
                     }
                 }
+#pragma unroll
+                for (int rl = 0; rl < R; ++rl) {
+                    float acc[8];
+#pragma unroll
+                    for (int c = 0; c < 8; ++c) {
+                        float a = 0.0f;
+#pragma unroll
+                        for (int di = 0; di < 3; ++di) {
+                            a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pr[rl + di][c]),
+                                                                __builtin_bit_cast(bf16x2_t, w01[di][c]), a, false);
+                            a = fmaf(sg[rl + di][c], w2[di][c], a);
+                        }
+                        acc[c] = a;
+                    }
+                    *reinterpret_cast<uint4*>(A + f_a_off<C>(rl * W + j, ug)) =
+                        make_uint4(f_pack_bf16(acc[0], acc[1]), f_pack_bf16(acc[2], acc[3]),
+                                   f_pack_bf16(acc[4], acc[5]), f_pack_bf16(acc[6], acc[7]));
+                }
+            };
+            for (int cp = 0; cp * CPP < W; ++cp) {
+                load_pass(cp, v);
+                compute_pass(cp, v);
             }
             f_lds_wait();
             f_barrier();  // A tile t complete
         }
     } else {
-        const int cb = wid - 4;
+        const int cb = wid - NP;
         const bool active = cb * 64 < C_out;
         for (int t = 0; t < n_local; ++t) {
             f_barrier();  // A tile t complete; A tile t-1 may be overwritten after the next barrier
@@ -360,12 +380,12 @@ FusedPlan fused_plan(const DwArgs& d, int64_t C_out, int lds_max) {
     if ((reinterpret_cast<uintptr_t>(d.x) & 15) || (reinterpret_cast<uintptr_t>(d.w) & 15)) return p;
     if (d.W <= 0 || d.W > kFPix || d.H <= 0) return p;
     const int R = d.W <= kFPix / 2 ? 2 : 1;
-    const int upw = (int)d.C / 32;
-    const int row_instr = (int)((d.W * upw + 63) / 64);
+    const int upw = (int)d.C / (8 * kProducers);
+    const int row_instr = (int)(((d.W + 2) * upw + 63) / 64);  // a row with its zero halo
     // two A tiles (C*256 bytes) and as much again for the P staging of the
     // other two consumers, then the four producer rings
     const size_t fixed = 2 * (size_t)kFPix * d.C * 2 * 2;
-    const size_t set_bytes = 4 * (size_t)row_instr * 1024;  // one slot of each producer ring
+    const size_t set_bytes = kProducers * (size_t)row_instr * 1024;  // one slot of each producer ring
     if ((size_t)lds_max <= fixed) return p;
     const int n_slots = (int)std::min<size_t>(kMaxSlots, ((size_t)lds_max - fixed) / set_bytes);
     if (n_slots < R + 2) return p;
