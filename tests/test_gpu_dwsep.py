@@ -94,3 +94,12 @@ def test_fused_f32_path_shapes(C, Co):
     # partial last tile), C_out below 256 (idle waves)
     for (b, H, W) in [(2, 5, 8), (1, 9, 16), (2, 7, 56), (1, 3, 64), (1, 4, 24)]:
         _case(b, H, W, C, Co, dt="f32", ot="f32", seed=H * W + C + Co)
+
+
+def test_fused_f32_row_ranges_cross_images():
+    # More rows than CUs: each workgroup takes a contiguous range of rows whose
+    # tiles (up to two rows, never crossing an image) include one-row tiles and
+    # image boundaries, and its step pipeline spans several tiles.
+    _case(40, 9, 16, 64, 48, dt="f32", ot="f32", seed=21)
+    _case(20, 30, 8, 32, 16, dt="f32", ot="f32", seed=22)
+    _case(6, 56, 56, 128, 256, dt="f32", ot="f32", seed=23)
