@@ -366,28 +366,27 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def csrc_hash() -> str:
-    """sha256 over the HIP/C++ sources of the library (names and contents)."""
-    import glob
+def sources_hash(names) -> str:
+    """sha256 over the named library sources under csrc/ (names and contents)."""
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_1810_09958_amd", "csrc", "*"))):
-        h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
+    for n in sorted(names):
+        h.update(n.encode())
+        with open(os.path.join(ROOT, "paper_1810_09958_amd", "csrc", n), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
 def measured_traffic(name: str):
-    """Traffic per launch recorded under profiles/, or None when the kernel sources changed
-    since the counters were taken."""
+    """Traffic per launch recorded under profiles/, or None when any source the kernel is
+    built from (the record lists them) changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", name)
     try:
         with open(path) as fh:
             rec = json.load(fh)
-    except (OSError, ValueError):
-        return None
-    if rec.get("csrc_sha256") != csrc_hash():
+        if rec.get("sources_sha256") != sources_hash(rec["sources"]):
+            return None
+    except (OSError, ValueError, KeyError, TypeError):
         return None
     return rec.get("traffic_bytes_per_dispatch")
 
