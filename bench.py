@@ -4,7 +4,7 @@ A step runs every part of the path once, on seeded synthetic inputs already resi
 HBM:
   * bf16 GEMM 8192 x 8192 x 8192, bf16 and fp32 outputs
   * bf16 GEMM M=8192 N=1024 K=16384, bf16 and fp32 outputs
-  * skinny GEMM 4096 x 32 x 4096, bf16 and fp32 inputs (fp32 out)
+  * skinny GEMM 4096 x 32 x 4096, bf16 and fp32 inputs (fp32 out); also N = 1 (bf16)
   * GRU forward T=64, batch 32, input = hidden = 1024, bf16 weights (also T=128 and batch 4)
   * separable depthwise conv 32 x 56 x 56 x 128 -> 256, bf16 (fp32 out) and fp32
   * 1D convolution 32 sequences x 1024 positions, 512 -> 512 channels, 5 taps, bf16 (fp32 out)
@@ -185,6 +185,16 @@ def main():
         add_rotated(name, lambda i, As=As, Bs=Bs, Cs=Cs, ws=ws: (lambda: isam.gemm(As[i], Bs[i], Cs[i], workspace=ws)),
                     sets, {"kind": "skinny", "flop": 2.0 * 4096 * 32 * 4096,
                            "bytes": es * (4096 * 4096 + 4096 * 32) + 4 * 4096 * 32})
+    # narrow product (batch 1, matrix-vector), context point: dot-product kernel
+    if want("gemv_4096x1x4096_bf16"):
+        A0, B0 = gpu(sk["A_bf16"]), gpu(np.ascontiguousarray(sk["B_bf16"][:, :1]))
+        sets = n_sets(A0.numel() * 2)
+        As = [A0] + [A0.clone() for _ in range(sets - 1)]
+        Cs = [torch.empty((4096, 1), device=dev, dtype=torch.float32) for _ in range(sets)]
+        ws = torch.empty(1, device=dev, dtype=torch.uint8)
+        add_rotated("gemv_4096x1x4096_bf16", lambda i, As=As, Cs=Cs, B0=B0, ws=ws: (lambda: isam.gemm(As[i], B0, Cs[i], workspace=ws)),
+                    sets, {"kind": "skinny", "flop": 2.0 * 4096 * 4096,
+                           "bytes": 2 * (4096 * 4096 + 4096) + 4 * 4096})
     del sk
 
     # -- GRU --------------------------------------------------------------------------

@@ -110,11 +110,19 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
         tile_dims(t, ab_type, &bm, &bn, &bk);
         return cdiv(M, bm) * cdiv(N, bn);
     };
+    const bool skinny_off = getenv("ISAM_GEMM_CONFIG") && strstr(getenv("ISAM_GEMM_CONFIG"), "skinny=0");
+    // N < 8 and not a multiple of the vector width: the dot-product kernel
+    // (NN with aligned A rows, checked at dispatch; the tile kernel is the
+    // fallback).
+    if (allow_skinny && !skinny_off && N < 8 && K > 0 && N % (ab_type == kBF16 ? 8 : 4) != 0) {
+        p.tile = kTile128x32;
+        p.skinny = 4;
+        return p;
+    }
     // N <= 32 with A and B in NN layout streams A through the skinny kernel
     // (layout and alignment are checked at dispatch; the tile kernel is the
     // fallback).
-    if (allow_skinny && N <= 32 && K > 0 && N % (ab_type == kBF16 ? 8 : 4) == 0 &&
-        !(getenv("ISAM_GEMM_CONFIG") && strstr(getenv("ISAM_GEMM_CONFIG"), "skinny=0"))) {
+    if (allow_skinny && N <= 32 && K > 0 && N % (ab_type == kBF16 ? 8 : 4) == 0 && !skinny_off) {
         p.tile = kTile128x32;
         if (ab_type == kBF16 && cdiv(M, skinny_stream_rows()) >= cus / 2) {
             // Enough 16-row workgroups to cover the CUs: one pass over A, no split.
@@ -258,7 +266,14 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         p.k_per_split = K;
     }
     p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
-    if (p.skinny && (!p.vec || trans_a || trans_b || K == 0)) {
+    if (p.skinny == 4) {
+        // the narrow kernel reads A in 16-byte pieces and B element-wise
+        const int64_t es = (int64_t)dsize(ab_type);
+        if (trans_a || trans_b || K == 0 || ((uintptr_t)A & 15) || (lda * es) % 16) {
+            p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
+            p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
+        }
+    } else if (p.skinny && (!p.vec || trans_a || trans_b || K == 0)) {
         p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
         p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     }

@@ -51,13 +51,17 @@ struct GemmPlan {
     int dma;         // 1: direct-to-LDS kernel where it applies (bf16, A K-contiguous, vec)
     int dma_waves;   // 4 or 8 waves per workgroup for the direct-to-LDS kernel
     int skinny;      // 1: streaming kernel for N <= 32 (k_splits = K slices of skinny_k_slice);
-                     // 2: bf16 row-streaming kernel (16 rows per workgroup, whole K, no split)
+                     // 2: bf16 row-streaming kernel (16 rows per workgroup, whole K, no split);
+                     // 4: narrow dot-product kernel (N < 8, not a multiple of the vector width)
 };
 int64_t skinny_k_slice(int ab_type);
 int skinny_rows_per_wg(int ab_type);
 hipError_t launch_skinny(const GemmArgs& a, int splits, hipStream_t s);
 int skinny_stream_rows();
 hipError_t launch_skinny_rows(const GemmArgs& a, hipStream_t s);
+// Narrow product (N < 8): dot-product kernel streaming A once (NN, A rows
+// 16-byte aligned, any ldb).
+hipError_t launch_narrow(const GemmArgs& a, hipStream_t s);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk);
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s);

@@ -340,6 +340,152 @@ __global__ __launch_bounds__(64 * kSkWaves) void skinny_rows_kernel(GemmArgs a) 
     }
 }
 
+// Narrow product (N < 8, any ldb): the batch-1..7 matrix-vector form, where
+// the paper's mapper would pick a dot-product instruction rather than a
+// matrix one (Section 4).  Bound by streaming A once.  A workgroup owns 8
+// rows; in each wave eight lanes share a row, and the 4 waves split K: wave
+// w takes the 64-value K blocks w, w+4, w+8, ... of the current slice, lane j
+// of a row the 16-byte piece j of each block (8 lanes read 128 contiguous
+// bytes), 16 (bf16) or 8 (fp32) blocks per batch.  Each piece is dotted with the
+// matching K values of the N columns of B, which sit transposed in LDS
+// (B^T[n][k], zero past K; all lanes with the same j read the same
+// address): v_dot2_f32_bf16 for bf16, FMAs for fp32.  K runs in LDS-sized
+// slices; the next batch of A loads is always in flight during the
+// arithmetic.  At the end the 8 lanes of a row are summed (butterfly), then the
+// 4 waves in wave order through LDS, and C is written.
+constexpr int kNarrowRows = 8;
+constexpr int kNarrowWaves = 4;
+constexpr int kNarrowSliceBytes = 64 * 1024;  // B^T slice in LDS
+
+typedef __bf16 nbf16x2_t __attribute__((ext_vector_type(2)));
+
+template <typename T>
+__global__ __launch_bounds__(64 * kNarrowWaves) void narrow_kernel(GemmArgs a, int ks_len) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr bool BF = sizeof(T) == 2;
+    constexpr int PIECES = BF ? 1 : 2;  // 16-byte loads per 8 K values
+    constexpr int kNarrowUnroll = BF ? 16 : 8;  // blocks per batch and lane
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int N = (int)a.N;
+    const int r = lane >> 3, j = lane & 7;
+    const int64_t row = (int64_t)blockIdx.x * kNarrowRows + r;
+    const bool row_ok = row < a.M;
+    const T* B = static_cast<const T*>(a.B);
+    T* bt = reinterpret_cast<T*>(smem);  // [N][ks_len]
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(((a.M - 1) * a.lda + a.K) * sizeof(T)));
+    const uint32_t a_row = row_ok ? (uint32_t)(row * a.lda * sizeof(T)) : 0u;
+    float acc[7];
+#pragma unroll
+    for (int n = 0; n < 7; ++n) acc[n] = 0.0f;
+
+    // Batch b of a slice: this wave's blocks wid + 4*(b*U + u), u < U.  The
+    // loads of batch b+1 are issued before the arithmetic of batch b, and the
+    // first batch of a slice before its B^T is staged.
+    uint4 av[kNarrowUnroll][PIECES], nx[kNarrowUnroll][PIECES];
+    auto load_batch = [&](uint4 (&dst)[kNarrowUnroll][PIECES], int64_t k0, int blocks, int b) {
+#pragma unroll
+        for (int u = 0; u < kNarrowUnroll; ++u) {
+            const int blk = wid + kNarrowWaves * (b * kNarrowUnroll + u);
+            const int kk = blk * 64 + j * 8;
+            const bool ok = row_ok && blk < blocks;
+#pragma unroll
+            for (int p = 0; p < PIECES; ++p)
+                dst[u][p] = buf_load16(rsA, ok ? a_row + (uint32_t)((k0 + kk) * sizeof(T)) + p * 16 : kOob);
+        }
+    };
+    for (int64_t k0 = 0; k0 < a.K; k0 += ks_len) {
+        const int len = (int)min((int64_t)ks_len, a.K - k0);
+        const int blocks = (len + 63) / 64;
+        const int batches = (blocks + kNarrowWaves * kNarrowUnroll - 1) / (kNarrowWaves * kNarrowUnroll);
+        __syncthreads();  // the previous slice's reads are done
+        // Stage B^T: a thread takes 8 consecutive K values of one column per
+        // step, its 8 element loads issued together, then the LDS stores.
+        for (int g0 = tid; g0 < (ks_len / 8) * N; g0 += 64 * kNarrowWaves) {
+            const int n = g0 / (ks_len / 8), kk = (g0 - n * (ks_len / 8)) * 8;
+            T v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = kk + e < len ? B[(k0 + kk + e) * a.ldb + n] : T(0);
+            T* d = bt + n * ks_len + kk;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) d[e] = v[e];
+        }
+        load_batch(nx, k0, blocks, 0);
+        __syncthreads();
+        for (int bb = 0; bb < batches; ++bb) {
+#pragma unroll
+            for (int u = 0; u < kNarrowUnroll; ++u)
+#pragma unroll
+                for (int p = 0; p < PIECES; ++p) av[u][p] = nx[u][p];
+            if (bb + 1 < batches) load_batch(nx, k0, blocks, bb + 1);
+#pragma unroll
+            for (int u = 0; u < kNarrowUnroll; ++u) {
+                const int blk = wid + kNarrowWaves * (bb * kNarrowUnroll + u);
+                if (blk >= blocks) break;
+                const int kk = blk * 64 + j * 8;
+#pragma unroll
+                for (int n = 0; n < 7; ++n) {
+                    if (n >= N) break;
+                    const T* bp = bt + n * ks_len + kk;
+                    if constexpr (BF) {
+                        const uint4 bv = *reinterpret_cast<const uint4*>(bp);
+                        const uint32_t aw[4] = {av[u][0].x, av[u][0].y, av[u][0].z, av[u][0].w};
+                        const uint32_t bw[4] = {bv.x, bv.y, bv.z, bv.w};
+                        float t = acc[n];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            t = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(nbf16x2_t, aw[q]),
+                                                                __builtin_bit_cast(nbf16x2_t, bw[q]), t, false);
+                        acc[n] = t;
+                    } else {
+                        const float4 b0v = *reinterpret_cast<const float4*>(bp);
+                        const float4 b1v = *reinterpret_cast<const float4*>(bp + 4);
+                        const float4 a0 = __builtin_bit_cast(float4, av[u][0]);
+                        const float4 a1 = __builtin_bit_cast(float4, av[u][PIECES - 1]);
+                        float t = acc[n];
+                        t = fmaf(a0.x, b0v.x, t); t = fmaf(a0.y, b0v.y, t); t = fmaf(a0.z, b0v.z, t); t = fmaf(a0.w, b0v.w, t);
+                        t = fmaf(a1.x, b1v.x, t); t = fmaf(a1.y, b1v.y, t); t = fmaf(a1.z, b1v.z, t); t = fmaf(a1.w, b1v.w, t);
+                        acc[n] = t;
+                    }
+                }
+            }
+        }
+    }
+    // Sum the 8 lanes of each row (lane j += lane j^1, then ^2, then ^4),
+    // then the 4 waves in wave order.
+#pragma unroll
+    for (int n = 0; n < 7; ++n) {
+        float v = acc[n];
+        v += __shfl_xor(v, 1, 64);
+        v += __shfl_xor(v, 2, 64);
+        v += __shfl_xor(v, 4, 64);
+        acc[n] = v;
+    }
+    __syncthreads();  // B^T reads are done: reuse LDS
+    float* red = reinterpret_cast<float*>(smem);  // [wave][row][7]
+    if (j == 0) {
+#pragma unroll
+        for (int n = 0; n < 7; ++n) red[(wid * kNarrowRows + r) * 7 + n] = acc[n];
+    }
+    __syncthreads();
+    if (wid != 0 || j != 0 || !row_ok) return;
+#pragma unroll
+    for (int n = 0; n < 7; ++n) {
+        if (n >= N) break;
+        float v = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kNarrowWaves; ++w) v += red[(w * kNarrowRows + r) * 7 + n];
+        if (a.bias) v += a.bias[n];
+        const int64_t idx = row * a.ldc + n;
+        if (a.c_type == kF32) {
+            float* C = static_cast<float*>(a.C);
+            C[idx] = a.accumulate ? C[idx] + v : v;
+        } else {
+            uint16_t* C = static_cast<uint16_t*>(a.C);
+            C[idx] = (uint16_t)f32_to_bf16(a.accumulate ? bf16_to_f32(C[idx]) + v : v);
+        }
+    }
+}
+
 }  // namespace
 
 // K depth of one workgroup's slice (the split-K unit) for the skinny kernel.
@@ -347,6 +493,25 @@ int64_t skinny_k_slice(int ab_type) { return ab_type == kBF16 ? 2048 : 1024; }
 int skinny_rows_per_wg(int ab_type) { return ab_type == kBF16 ? 32 : 64; }
 
 int skinny_stream_rows() { return kRowsPerWg; }
+
+hipError_t launch_narrow(const GemmArgs& a, hipStream_t s) {
+    if (a.N < 1 || a.N > 7) return hipErrorInvalidValue;
+    const size_t es = a.ab_type == kBF16 ? 2 : 4;
+    // K slice: a multiple of 64 whose N x slice B^T fits the LDS budget
+    int64_t ks = (int64_t)(kNarrowSliceBytes / (a.N * es)) / 64 * 64;
+    if (ks > ((a.K + 63) / 64) * 64) ks = ((a.K + 63) / 64) * 64;
+    if (ks < 64) ks = 64;
+    // (at least room for the cross-wave sums)
+    const size_t lds = std::max<size_t>((size_t)ks * a.N * es, kNarrowWaves * kNarrowRows * 7 * sizeof(float));
+    const void* fn = a.ab_type == kBF16 ? reinterpret_cast<const void*>(narrow_kernel<uint16_t>)
+                                        : reinterpret_cast<const void*>(narrow_kernel<float>);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    const dim3 grid((unsigned)((a.M + kNarrowRows - 1) / kNarrowRows)), block(64 * kNarrowWaves);
+    if (a.ab_type == kBF16) hipLaunchKernelGGL(narrow_kernel<uint16_t>, grid, block, lds, s, a, (int)ks);
+    else hipLaunchKernelGGL(narrow_kernel<float>, grid, block, lds, s, a, (int)ks);
+    return hipGetLastError();
+}
 
 hipError_t launch_skinny_rows(const GemmArgs& a, hipStream_t s) {
     const dim3 grid((unsigned)((a.M + kRowsPerWg - 1) / kRowsPerWg)), block(64 * kSkWaves);

@@ -165,6 +165,18 @@ def test_skinny_shapes(dt, N):
     _run_case(300, N, 3000, dt, "bf16", seed=N)
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("N", [1, 2, 3, 5, 6, 7])
+def test_narrow_shapes(dt, N):
+    # dot-product kernel for N < 8: ragged M, K within one and over several
+    # LDS slices of B^T, B rows wider than N, bf16 output, accumulate
+    for M, K in [(1, 8), (33, 1000), (100, 2048), (4097, 4104), (70, 7168)]:
+        _run_case(M, N, K, dt, "f32", seed=M + K + N)
+    _run_case(300, N, 3000, dt, "bf16", seed=N, pad_ld=8)
+    _run_case(129, N, 520, dt, "f32", accumulate=True, seed=2 * N)
+    _run_case(64, N, 333, dt, "f32", seed=3 * N)   # A rows not 16-byte aligned: tile kernel
+
+
 def test_skinny_accumulate_and_fallback_layouts():
     _run_case(513, 32, 5000, "bf16", "f32", accumulate=True)
     _run_case(513, 32, 5000, "f32", "f32", accumulate=True)
