@@ -87,6 +87,15 @@ def test_fused_tile_ranges_cross_images(ot):
     _case(150, 28, 16, 64, 40, dt="bf16", ot=ot, seed=8)
 
 
+def test_fused_tiny_images_many_tiles():
+    # One- and two-row images: every tile starts a new image (all R+2 input
+    # rows new, two of them outside the image), several tiles per workgroup,
+    # the input ring wraps; tiny widths leave most MFMA columns unused.
+    _case(300, 1, 5, 64, 16, dt="bf16", ot="f32", seed=31)
+    _case(1200, 2, 3, 128, 24, dt="bf16", ot="bf16", seed=32)
+    _case(40, 3, 1, 128, 256, dt="bf16", ot="f32", seed=33)
+
+
 @pytest.mark.parametrize("C,Co", [(32, 16), (64, 48), (96, 256), (128, 256), (128, 112)])
 def test_fused_f32_path_shapes(C, Co):
     # fp32 3x3 stride-1 pad-1 shapes taken by the fused fp32 kernel (W % 8 == 0,
