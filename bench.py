@@ -215,6 +215,14 @@ def main():
                            "flop": 2.0 * T * Bt * 3 * H * (I + H),
                            "bytes": 2 * (3 * H * I + 3 * H * H + T * Bt * I) + 4 * T * Bt * H})
 
+        # the same call (MALL-warm, one buffer set) under the persistent schedule
+        comps.append(("gru_T64_B32_H1024_bf16_persistent_mall_warm",
+                      (lambda: isam.gru_forward(gsets[0][0], gsets[0][1], gsets[0][2], bias=gb,
+                                                h_seq=hseqs[0], h_T=g_hT, workspace=g_ws)),
+                      {"kind": "gru", "steps": T, "env": {"ISAM_GRU_MODE": "persistent"},
+                       "flop": 2.0 * T * Bt * 3 * H * (I + H),
+                       "bytes": 2 * (3 * H * I + 3 * H * H + T * Bt * I) + 4 * T * Bt * H}))
+
     # GRU variants (context points): the paper's 128 steps; a small batch.
     for (gT, gB, gname) in [(128, 32, "gru_T128_B32_H1024_bf16"), (64, 4, "gru_T64_B4_H1024_bf16")]:
         if not want(gname):
@@ -277,6 +285,8 @@ def main():
 
     def run_step(evs=None):
         for i, (_, fn, info) in enumerate(comps):
+            saved = {k: os.environ.get(k) for k in info.get("env", {})}
+            os.environ.update(info.get("env", {}))
             if info.get("pre") is not None:
                 info["pre"]()
             if evs is not None:
@@ -284,6 +294,11 @@ def main():
             fn()
             if evs is not None:
                 evs[i][1].record(stream)
+            for k, v in saved.items():
+                if v is None:
+                    os.environ.pop(k, None)
+                else:
+                    os.environ[k] = v
 
     for _ in range(args.warmup):
         run_step()

@@ -123,8 +123,16 @@ size_t isam_dwsep_conv_workspace_size(int64_t batch, int64_t H, int64_t W, int64
  * hidden must be a multiple of 8 (bf16) or 4 (fp32).  The bf16 path rounds
  * h_{t-1} to bf16 only as the matrix-core operand; the state stays fp32.
  * T == 0: h_T = h0 (or zeros).  batch == 0: no-op.
- * The recurrent kernel needs all its workgroups resident at once; if the
- * device cannot hold them the call returns ISAM_ERR_UNSUPPORTED.
+ * Two schedules compute the same values bit for bit: a persistent kernel with
+ * U held in on-chip memory and a grid barrier per step, or the priming,
+ * recursive and finish iterations as separate kernels (one per step) replayed
+ * from a graph that the library builds and caches per call signature (sizes
+ * and every pointer, workspace included; up to 32 signatures).  The faster one
+ * for the shape runs by default; the environment variable ISAM_GRU_MODE
+ * (persistent | steps) overrides, and the stepwise schedule runs whenever the
+ * persistent kernel cannot keep all its workgroups resident, so any hidden size
+ * that meets the multiple rule is supported.  Calls on one workspace must not
+ * overlap in time.
  */
 isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
                                int w_type, const void* x, const float* h0, const void* W,

@@ -464,7 +464,8 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
     if (T < 0 || batch <= 0 || hidden_size <= 0 || !valid_dtype(w_type)) return 0;
     const size_t gx = align256((size_t)T * (size_t)batch * 3 * (size_t)hidden_size * sizeof(float));
     const size_t hb = align256(((size_t)T + 1) * (size_t)batch * (size_t)hidden_size * dsize(w_type));
-    return gx + hb + kGruSyncBytes;
+    const size_t hs = align256(2 * (size_t)batch * (size_t)hidden_size * sizeof(float));
+    return gx + hb + kGruSyncBytes + hs;
 }
 
 }  // extern "C"
@@ -526,39 +527,69 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     int lds_max = 0;
     e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (e != hipSuccess) return hip_fail(e, who);
+    // Two schedules of the same step arithmetic: one persistent kernel with U
+    // resident in LDS and a grid barrier between steps, or one kernel per step
+    // replayed from a graph, which re-reads U from the memory-side cache every
+    // step (the L2 does not keep it across kernel boundaries) but pays no grid
+    // barrier.  Measured on MI355X (T = 64, I = 1024): the stepwise schedule
+    // is faster up to batch 16 while U is at most 16 MB (H = 1024 bf16: 257
+    // vs 369 us at batch 1, 326 vs 337 at 16; 391 vs 320 at 32), and up to
+    // batch 4 while U is at most 32 MB; the persistent one elsewhere.
+    // ISAM_GRU_MODE=persistent|steps overrides; the stepwise schedule also
+    // runs whenever the persistent kernel has no resident tiling.
+    const char* mode_env = getenv("ISAM_GRU_MODE");
+    const double u_mb = 3.0 * (double)H * (double)H * (double)es / (1 << 20);
+    bool step_mode = (batch <= 16 && u_mb <= 16.0) || (batch <= 4 && u_mb <= 32.0);
+    if (mode_env && strcmp(mode_env, "persistent") == 0) step_mode = false;
+    if (mode_env && strcmp(mode_env, "steps") == 0) step_mode = true;
     // Units per workgroup: the smallest power of two whose grid fits one
     // workgroup per CU (measured faster than packing two per CU); if none
     // does, the smallest that fits at the occupancy limit.  Batch groups
     // have separate barriers.
     int J = 0;
     int n_wg = 0;
-    for (int pass = 0; pass < 2 && !J; ++pass) {
+    if (!step_mode) {
+        for (int pass = 0; pass < 2 && !J; ++pass) {
+            for (int cand = 1; cand <= 16; cand *= 2) {
+                if (H % cand) continue;
+                if (cand * BB > 256) break;
+                const size_t lds = gru_lds_bytes(w_type, H, cand);
+                if (lds > (size_t)lds_max) break;
+                const int64_t wgs = (H / cand) * n_bg;
+                const int per_cu = pass == 0 ? 1 : gru_blocks_per_cu(w_type, lds);
+                if (wgs <= (int64_t)cus * per_cu) { J = cand; n_wg = (int)wgs; break; }
+            }
+        }
+        const char* jenv = getenv("ISAM_GRU_J");
+        if (J && jenv) {  // tuning override, ignored when it does not fit
+            const int v = atoi(jenv);
+            const size_t lds = (v >= 1 && v <= 16) ? gru_lds_bytes(w_type, H, v) : 0;
+            if (v >= 1 && v <= 16 && H % v == 0 && v * BB <= 256 && lds <= (size_t)lds_max &&
+                (H / v) * n_bg <= (int64_t)cus * std::min(2, gru_blocks_per_cu(w_type, lds))) {
+                J = v;
+                n_wg = (int)((H / v) * n_bg);
+            }
+        }
+        if (!J || n_bg > kGruSyncBytes / 4 / 512 - 1) step_mode = true;  // one 512-word barrier domain per batch group
+    }
+    if (step_mode) {
+        // No residency constraint: the smallest power of two whose grid fits
+        // one workgroup per CU, else the largest that divides H.
         for (int cand = 1; cand <= 16; cand *= 2) {
-            if (H % cand) continue;
-            if (cand * BB > 256) break;
-            const size_t lds = gru_lds_bytes(w_type, H, cand);
-            if (lds > (size_t)lds_max) break;
-            const int64_t wgs = (H / cand) * n_bg;
-            const int per_cu = pass == 0 ? 1 : gru_blocks_per_cu(w_type, lds);
-            if (wgs <= (int64_t)cus * per_cu) { J = cand; n_wg = (int)wgs; break; }
+            if (H % cand || cand * BB > 256) continue;
+            J = cand;
+            if ((H / cand) * n_bg <= (int64_t)cus) break;
         }
-    }
-    if (!J) return fail(ISAM_ERR_UNSUPPORTED, "%s: no resident tiling for hidden=%lld batch=%lld on %d CUs",
-                        who, (long long)H, (long long)batch, cus);
-    if (const char* env = getenv("ISAM_GRU_J")) {  // tuning override, ignored when it does not fit
-        const int v = atoi(env);
-        const size_t lds = (v >= 1 && v <= 16) ? gru_lds_bytes(w_type, H, v) : 0;
-        if (v >= 1 && v <= 16 && H % v == 0 && v * BB <= 256 && lds <= (size_t)lds_max &&
-            (H / v) * n_bg <= (int64_t)cus * std::min(2, gru_blocks_per_cu(w_type, lds))) {
-            J = v;
-            n_wg = (int)((H / v) * n_bg);
+        if (const char* env = getenv("ISAM_GRU_J")) {  // tuning override, ignored when invalid
+            const int v = atoi(env);
+            if (v >= 1 && v <= 16 && H % v == 0 && v * BB <= 256) J = v;
         }
+        if ((H / J) * n_bg > INT32_MAX) return fail(ISAM_ERR_UNSUPPORTED, "%s: grid too large", who);
+        n_wg = (int)((H / J) * n_bg);
     }
-    if (n_bg > kGruSyncBytes / 4 / 512 - 1)  // one 512-word domain per batch group after the error word's
-        return fail(ISAM_ERR_UNSUPPORTED, "%s: batch %lld needs too many barrier domains", who, (long long)batch);
     if (log_enabled())
-        fprintf(stderr, "[isam] gru T=%lld B=%lld I=%lld H=%lld w=%d J=%d BB=%d wgs=%d lds=%zu\n", (long long)T,
-                (long long)batch, (long long)I, (long long)H, w_type, J, BB, n_wg, gru_lds_bytes(w_type, H, J));
+        fprintf(stderr, "[isam] gru T=%lld B=%lld I=%lld H=%lld w=%d mode=%s J=%d BB=%d wgs=%d\n", (long long)T,
+                (long long)batch, (long long)I, (long long)H, w_type, step_mode ? "steps" : "persistent", J, BB, n_wg);
 
     char* ws = static_cast<char*>(workspace);
     float* gx = reinterpret_cast<float*>(ws);
@@ -566,6 +597,7 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     void* hbuf = ws + gx_b;
     const size_t hb_b = align256(((size_t)T + 1) * batch * H * es);
     unsigned* sync = reinterpret_cast<unsigned*>(ws + gx_b + hb_b);
+    float* hstate = reinterpret_cast<float*>(ws + gx_b + hb_b + kGruSyncBytes);
 
     // Input projection for all steps: Gx[T*batch][3H] = x[T*batch][I] . W^T.
     isam_status_t st = run_gemm(0, 1, T * batch, 3 * H, I, w_type, x, I, W, I, 0, ISAM_F32, gx, 3 * H,
@@ -592,7 +624,7 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     // First-level barrier groups of 8 workgroups (measured fastest), larger
     // when a domain would otherwise need more group counters than it has.
     g.barrier_group = (int)std::max<int64_t>(8, cdiv(H / J, kGruMaxGroupsPerDomain));
-    e = launch_gru_recurrent(g, s);
+    e = step_mode ? launch_gru_steps(g, hstate, s) : launch_gru_recurrent(g, s);
     if (e != hipSuccess) return hip_fail(e, who);
     return ISAM_OK;
 }

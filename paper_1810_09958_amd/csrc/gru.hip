@@ -24,6 +24,9 @@
 //
 // All workgroups must be co-resident (cooperative launch); every barrier
 // wait is bounded and raises an error flag instead of spinning forever.
+#include <mutex>
+#include <vector>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -37,7 +40,7 @@ constexpr int kRedLd = 20;  // floats per row of the cross-wave sums (20: the 4 
 // Upper bound on one barrier wait, in ticks of the 100 MHz constant clock.
 constexpr uint64_t kBarrierTimeoutTicks = 200000000ull;  // 2 s
 
-__device__ __forceinline__ int gru_rows(int J) { return ((3 * J + 15) / 16) * 16; }
+__host__ __device__ __forceinline__ int gru_rows(int J) { return ((3 * J + 15) / 16) * 16; }
 // U rows in LDS: a multiple of 256 bytes, so the chunk swizzle below stays
 // inside the row.
 __host__ __device__ __forceinline__ int64_t gru_row_bytes(int64_t H, int64_t es) { return (H * es + 255) / 256 * 256; }
@@ -258,6 +261,140 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
     if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
 }
 
+// Stepwise form of the same recurrence: the priming, recursive and finish
+// iterations as separate kernels, chained in a graph by the host (Section
+// 3.6's schedule with T fixed per call).  One launch per step t: every
+// workgroup reads its rows of U straight from global memory (they stay in
+// the L2 of its XCD from step to step), h_{t-1} in the operand type from ring
+// slot t and the fp32 state from hstate[t & 1]; it writes h_t to h_seq[t],
+// ring slot t+1, hstate[(t+1) & 1] and, at the last step, h_T.  Kernel
+// boundaries order the steps, so there is no grid barrier and no
+// co-residency requirement; the arithmetic is that of the persistent kernel.
+template <typename T>
+__global__ void gru_step_init_kernel(GruArgs a, float* hstate) {
+    const int64_t n = a.batch * a.H;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {  // ring slot 0 and state 0: h0
+        const float v = a.h0 ? a.h0[i] : 0.0f;
+        hstate[i] = v;
+        if constexpr (sizeof(T) == 2) static_cast<uint16_t*>(a.hbuf)[i] = (uint16_t)f32_to_bf16(v);
+        else static_cast<float*>(a.hbuf)[i] = v;
+    }
+}
+
+// MT (row tiles of 16 U rows: gru_rows(J) / 16) is a template argument so that
+// every load of the step is unconditional: a load whose operand lies outside
+// the matrix reads the buffer's out-of-range offset and returns zeros.  With
+// MT known only at run time, the loads sit behind branches whose joins make
+// the compiler wait for the loads already in flight, one memory round trip
+// per K batch instead of one per step.
+template <typename T, int MT>
+__global__ __launch_bounds__(64 * kWaves) void gru_step_kernel(GruArgs a, float* hstate, int64_t t) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    constexpr int E = 16 / (int)sizeof(T);
+    const int J = a.units_per_wg, BB = a.batch_per_wg;
+    const int64_t H = a.H, B = a.batch;
+    constexpr int RT = MT * 16;
+    const int n_ug = (int)(H / J);
+    const int ug = blockIdx.x % n_ug, bg = blockIdx.x / n_ug;
+    const int64_t j0 = (int64_t)ug * J, b0 = (int64_t)bg * BB;
+    const int nb = (int)min((int64_t)BB, B - b0);
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    float* red = reinterpret_cast<float*>(smem);  // [kWaves][RT][kRedLd]
+
+    // Owned outputs: thread p < J * nb handles (jj, n) = (p % J, p / J).
+    const bool owner = tid < J * nb;
+    const int jj = owner ? tid % J : 0, nn = owner ? tid / J : 0;
+    const int64_t j = j0 + jj, bb = b0 + nn;
+    float h_prev = 0.f, gx_r = 0.f, gx_z = 0.f, gx_n = 0.f;
+    float bias_r = 0.f, bias_z = 0.f, bias_n = 0.f, bias_hn = 0.f;
+    if (owner) {
+        h_prev = hstate[(t & 1) * B * H + bb * H + j];
+        const float* gx = a.gx + (t * B + bb) * 3 * H;
+        gx_r = gx[j];
+        gx_z = gx[H + j];
+        gx_n = gx[2 * H + j];
+        if (a.bias) { bias_r = a.bias[j]; bias_z = a.bias[H + j]; bias_n = a.bias[2 * H + j]; }
+        if (a.bias_hn) bias_hn = a.bias_hn[j];
+    }
+
+    const int KG = (int)((H * (int64_t)sizeof(T) + 63) / 64);  // 64-byte K groups
+    // Wave w owns the contiguous K groups [kg_lo, kg_hi).
+    const int kg_lo = (KG * wid) / kWaves, kg_hi = (KG * (wid + 1)) / kWaves;
+    const int n_col = lane & 15, quarter = lane >> 4;
+    const bool col_ok = n_col < nb;
+    const int64_t hb_row = b0 + n_col;
+    // U row of this lane in row tile m: local row m*16 + n_col = g*J + jj'.
+    int64_t u_row[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const int lr = m * 16 + n_col;
+        u_row[m] = lr < 3 * J ? ((lr / J) * H + j0 + lr % J) : -1;
+    }
+    constexpr int kBatch = 8;  // K groups requested together per lane
+    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)((a.T + 1) * B * H * (int64_t)sizeof(T)));
+    const __amdgpu_buffer_rsrc_t rs_u = make_rsrc(a.U, (uint32_t)(3 * H * H * (int64_t)sizeof(T)));
+    const int64_t hcur_off = t * B * H;  // ring slot t holds h_{t-1}
+    f32x4_t acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kg0 = kg_lo; kg0 < kg_hi; kg0 += kBatch) {
+        uint4 hv[kBatch], uf[kBatch][MT];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int kg = kg0 + u;
+            const int64_t k = (int64_t)(kg * 4 + quarter) * E;
+            const bool kok = kg < kg_hi && k < H;
+            const uint32_t off = (kok && col_ok) ? (uint32_t)((hcur_off + hb_row * H + k) * (int64_t)sizeof(T)) : kOob;
+            hv[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs_h, (int)off, 0, 0));
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const uint32_t uo = (kok && u_row[m] >= 0) ? (uint32_t)((u_row[m] * H + k) * (int64_t)sizeof(T)) : kOob;
+                uf[u][m] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs_u, (int)uo, 0, 0));
+            }
+        }
+        // Keep the scheduler from interleaving the MFMAs into the loads above:
+        // all of the batch's loads are in flight before the first wait.
+        __builtin_amdgcn_sched_barrier(0);
+        // Past kg_hi the operands are zeros, so the MFMAs of the whole batch
+        // run without a branch.
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                if constexpr (sizeof(T) == 2) mfma16_bf16(acc[m], uf[u][m], hv[u]);
+                else mfma16_f32x4(acc[m], uf[u][m], hv[u]);
+            }
+        }
+    }
+    // acc[m] element v of lane l: local row m*16 + 4*(l/16) + v, batch column l%16
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) red[(wid * RT + m * 16 + 4 * quarter + v) * kRedLd + n_col] = acc[m][v];
+    }
+    __syncthreads();
+    if (!owner) return;
+    float gh[3];
+#pragma unroll
+    for (int g = 0; g < 3; ++g) {
+        float sum = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) sum += red[(w * RT + g * J + jj) * kRedLd + nn];
+        gh[g] = sum;
+    }
+    const float r = sigmoidf(gx_r + bias_r + gh[0]);
+    const float z = sigmoidf(gx_z + bias_z + gh[1]);
+    const float n = tanhf(gx_n + bias_n + r * (gh[2] + bias_hn));
+    const float h = (1.0f - z) * n + z * h_prev;
+    if (a.h_seq) a.h_seq[(t * B + bb) * H + j] = h;
+    hstate[((t + 1) & 1) * B * H + bb * H + j] = h;
+    const int64_t hn = (t + 1) * B * H + bb * H + j;  // ring slot t+1
+    if constexpr (sizeof(T) == 2) static_cast<uint16_t*>(a.hbuf)[hn] = (uint16_t)f32_to_bf16(h);
+    else static_cast<float*>(a.hbuf)[hn] = h;
+    if (t + 1 == a.T && a.h_T) a.h_T[bb * H + j] = h;
+}
+
 __global__ void copy_state_kernel(const float* h0, float* hT, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         hT[i] = h0 ? h0[i] : 0.0f;
@@ -307,6 +444,111 @@ hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s) {
     GruArgs args = a;
     void* params[] = {&args};
     return hipLaunchCooperativeKernel(fn, dim3(a.n_wg), dim3(64 * kWaves), params, (unsigned)lds, s);
+}
+
+// Graph of the stepwise recurrence for one call signature: the state init
+// and T step kernels chained as kernel nodes (no stream capture), cached
+// per signature (sizes, tiling and every pointer) so a repeated call replays
+// the same graph with one launch.  The cache is small and guarded by a mutex.
+namespace {
+struct StepGraph {
+    GruArgs a;
+    float* hstate;
+    int dev;
+    hipGraphExec_t exec;
+    uint64_t last_use;
+};
+std::mutex g_step_mu;
+std::vector<StepGraph> g_step_graphs;
+uint64_t g_step_use = 0;
+constexpr size_t kMaxStepGraphs = 32;
+
+bool same_call(const GruArgs& x, const GruArgs& y) {
+    return x.T == y.T && x.batch == y.batch && x.I == y.I && x.H == y.H && x.w_type == y.w_type &&
+           x.gx == y.gx && x.h0 == y.h0 && x.U == y.U && x.bias == y.bias && x.bias_hn == y.bias_hn &&
+           x.h_seq == y.h_seq && x.h_T == y.h_T && x.hbuf == y.hbuf && x.units_per_wg == y.units_per_wg &&
+           x.batch_per_wg == y.batch_per_wg && x.n_wg == y.n_wg;
+}
+
+int state_blocks(const GruArgs& a) {
+    const int64_t n = a.batch * a.H;
+    int64_t b = (n + 255) / 256;
+    return (int)(b > 1024 ? 1024 : (b < 1 ? 1 : b));
+}
+
+hipError_t build_step_graph(const GruArgs& a, float* hstate, hipGraphExec_t* out) {
+    const bool bf = a.w_type == kBF16;
+    const size_t red = (size_t)kWaves * gru_rows(a.units_per_wg) * kRedLd * sizeof(float);
+    hipGraph_t g = nullptr;
+    hipError_t e = hipGraphCreate(&g, 0);
+    if (e != hipSuccess) return e;
+    GruArgs args = a;
+    float* hs = hstate;
+    hipGraphNode_t prev = nullptr, node = nullptr;
+    {
+        void* params[] = {&args, &hs};
+        hipKernelNodeParams kp{};
+        kp.func = bf ? reinterpret_cast<void*>(gru_step_init_kernel<bf16_t>)
+                     : reinterpret_cast<void*>(gru_step_init_kernel<float>);
+        kp.gridDim = dim3(state_blocks(a));
+        kp.blockDim = dim3(256);
+        kp.sharedMemBytes = 0;
+        kp.kernelParams = params;
+        kp.extra = nullptr;
+        e = hipGraphAddKernelNode(&node, g, nullptr, 0, &kp);
+        prev = node;
+    }
+    const int mt = gru_rows(a.units_per_wg) / 16;
+    void* step_fn = nullptr;
+    switch (mt) {
+        case 1: step_fn = bf ? reinterpret_cast<void*>(gru_step_kernel<bf16_t, 1>) : reinterpret_cast<void*>(gru_step_kernel<float, 1>); break;
+        case 2: step_fn = bf ? reinterpret_cast<void*>(gru_step_kernel<bf16_t, 2>) : reinterpret_cast<void*>(gru_step_kernel<float, 2>); break;
+        case 3: step_fn = bf ? reinterpret_cast<void*>(gru_step_kernel<bf16_t, 3>) : reinterpret_cast<void*>(gru_step_kernel<float, 3>); break;
+        default: e = hipErrorInvalidValue;
+    }
+    for (int64_t t = 0; t < a.T && e == hipSuccess; ++t) {
+        int64_t tt = t;
+        void* params[] = {&args, &hs, &tt};
+        hipKernelNodeParams kp{};
+        kp.func = step_fn;
+        kp.gridDim = dim3(a.n_wg);
+        kp.blockDim = dim3(64 * kWaves);
+        kp.sharedMemBytes = (unsigned)red;
+        kp.kernelParams = params;
+        kp.extra = nullptr;
+        e = hipGraphAddKernelNode(&node, g, &prev, 1, &kp);
+        prev = node;
+    }
+    if (e == hipSuccess) e = hipGraphInstantiate(out, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    return e;
+}
+}  // namespace
+
+hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(g_step_mu);
+    StepGraph* hit = nullptr;
+    for (auto& c : g_step_graphs)
+        if (c.dev == dev && c.hstate == hstate && same_call(c.a, a)) hit = &c;
+    if (!hit) {
+        hipGraphExec_t exec = nullptr;
+        e = build_step_graph(a, hstate, &exec);
+        if (e != hipSuccess) return e;
+        if (g_step_graphs.size() >= kMaxStepGraphs) {  // evict the least recently used
+            size_t lru = 0;
+            for (size_t i = 1; i < g_step_graphs.size(); ++i)
+                if (g_step_graphs[i].last_use < g_step_graphs[lru].last_use) lru = i;
+            (void)hipGraphExecDestroy(g_step_graphs[lru].exec);
+            g_step_graphs.erase(g_step_graphs.begin() + (long)lru);
+        }
+        g_step_graphs.push_back(StepGraph{a, hstate, dev, exec, 0});
+        hit = &g_step_graphs.back();
+    }
+    hit->last_use = ++g_step_use;
+    return hipGraphLaunch(hit->exec, s);
 }
 
 }  // namespace isam

@@ -110,6 +110,9 @@ size_t gru_lds_bytes(int w_type, int64_t H, int J);
 int gru_blocks_per_cu(int w_type, size_t lds);
 constexpr int kGruSyncBytes = 32768;  // barrier area at the end of the GRU workspace
 hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s);
+// Stepwise recurrence (state init + one kernel per step, replayed from a
+// cached graph); hstate is a [2][batch][H] fp32 workspace.
+hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s);
 // T == 0: h_T = h0 (or zeros when h0 is null).
 hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStream_t s);
 

@@ -16,6 +16,14 @@ pytestmark = pytest.mark.gpu
 import paper_1810_09958_amd as isam
 
 
+@pytest.fixture(params=["steps", "persistent"])
+def mode(request, monkeypatch):
+    """The two schedules of the recurrence: one kernel per step replayed from a
+    graph, or one persistent kernel with a grid barrier between steps."""
+    monkeypatch.setenv("ISAM_GRU_MODE", request.param)
+    return request.param
+
+
 def _inputs(T, B, I, H, seed=0, scale=1 / 32, with_h0=False, with_bhn=False):
     x = synth.normal(seed, 3, (T, B, I))
     W = synth.uniform(seed, 0, (3 * H, I), -scale, scale)
@@ -46,13 +54,13 @@ def _run(T, B, I, H, dt="bf16", seed=0, with_h0=False, with_bhn=False, scale=1 /
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 @pytest.mark.parametrize("T", [1, 2, 3, 9])
-def test_small_steps(dt, T):
+def test_small_steps(dt, T, mode):
     _run(T, 4, 40, 64, dt, seed=T, with_h0=True, with_bhn=True, scale=1 / 4)
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 @pytest.mark.parametrize("B,H", [(1, 128), (16, 256), (17, 64), (33, 96), (5, 1024)])
-def test_shapes(dt, B, H):
+def test_shapes(dt, B, H, mode):
     _run(5, B, 72, H, dt, seed=B + H, with_h0=(B % 2 == 1), scale=1 / 8)
 
 
@@ -100,7 +108,7 @@ def test_deterministic_run_twice():
 
 
 @pytest.mark.parametrize("variant", ["bf16", "f32"])
-def test_config_full_size_sampled_sequences(variant):
+def test_config_full_size_sampled_sequences(variant, mode):
     d = workloads.gru()
     if variant == "bf16":
         x, W, U = d["x_bf16"], d["W_bf16"], d["U_bf16"]
@@ -116,6 +124,57 @@ def test_config_full_size_sampled_sequences(variant):
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
-def test_paper_step_count_128(dt):
-    # 128 recurrent steps (the paper's sequence length) through one persistent launch
+def test_paper_step_count_128(dt, mode):
+    # 128 recurrent steps (the paper's sequence length): one persistent launch, or
+    # 128 step kernels in one graph
     _run(128, 8, 128, 256, dt, seed=128, with_h0=True, scale=1 / 8)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_schedules_bit_identical(dt, monkeypatch):
+    # Both schedules sum each gate pre-activation in the same order (the K split
+    # over waves depends on H only), so their outputs agree bit for bit.
+    T, B, I, H = 7, 19, 96, 512
+    x, W, U, b, h0, bhn = _inputs(T, B, I, H, seed=77, scale=1 / 8, with_h0=True, with_bhn=True)
+    if dt == "bf16":
+        x, W, U = bits(x), bits(W), bits(U)
+    args = [to_gpu(a) for a in (x, W, U)]
+    kw = dict(bias=to_gpu(b), bias_hn=to_gpu(bhn), h0=to_gpu(h0))
+    out = {}
+    for m in ("steps", "persistent"):
+        monkeypatch.setenv("ISAM_GRU_MODE", m)
+        out[m] = isam.gru_forward(*args, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(out["steps"][0], out["persistent"][0])
+    assert torch.equal(out["steps"][1], out["persistent"][1])
+
+
+def test_step_graph_replay_sees_new_inputs(monkeypatch):
+    # A repeated call with the same buffers replays the cached step graph; new
+    # input values written in place between calls must be used.
+    monkeypatch.setenv("ISAM_GRU_MODE", "steps")
+    T, B, I, H = 5, 4, 64, 256
+    x1, W, U, b, _, _ = _inputs(T, B, I, H, seed=31, scale=1 / 8)
+    x2 = synth.normal(32, 3, (T, B, I))
+    xg, Wg, Ug, bg = to_gpu(bits(x1)), to_gpu(bits(W)), to_gpu(bits(U)), to_gpu(b)
+    hs = torch.empty((T, B, H), device="cuda")
+    hT = torch.empty((B, H), device="cuda")
+    ws = torch.empty(isam.gru_forward_workspace_size(T, B, I, H, isam.ISAM_BF16), device="cuda", dtype=torch.uint8)
+    for xs in (x1, x2, x1):
+        xg.copy_(to_gpu(bits(xs)))
+        isam.gru_forward(xg, Wg, Ug, bias=bg, h_seq=hs, h_T=hT, workspace=ws)
+        torch.cuda.synchronize()
+        ref = oracle.gru(bits(xs), bits(W), bits(U), b, None, None)
+        err = float(np.max(np.abs(hs.cpu().numpy().astype(np.float64) - ref)))
+        assert err <= TOL_BF16, err
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_hidden_too_large_for_lds_runs_stepwise(dt, monkeypatch):
+    # The persistent kernel keeps at least 16 rows of U (three gate rows padded to an
+    # MFMA tile) in one CU's LDS: 192 KB at H = 6144 (bf16) / 3072 (fp32), over the
+    # 160 KB there is.  The stepwise schedule reads U from global memory and has no
+    # such limit, so it is taken even when the persistent one is asked for.
+    monkeypatch.setenv("ISAM_GRU_MODE", "persistent")
+    H = 6144 if dt == "bf16" else 3072
+    _run(3, 2, 64, H, dt, seed=5, with_h0=True, scale=1 / 64)
