@@ -464,6 +464,7 @@ struct StepGraph {
     float* hstate;
     int dev;
     hipGraphExec_t exec;
+    hipEvent_t done;  // recorded after every launch: an evicted graph is destroyed only once idle
     uint64_t last_use;
 };
 std::mutex g_step_mu;
@@ -545,18 +546,29 @@ hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s) {
         hipGraphExec_t exec = nullptr;
         e = build_step_graph(a, hstate, &exec);
         if (e != hipSuccess) return e;
+        hipEvent_t done = nullptr;
+        e = hipEventCreateWithFlags(&done, hipEventDisableTiming);
+        if (e != hipSuccess) {
+            (void)hipGraphExecDestroy(exec);
+            return e;
+        }
         if (g_step_graphs.size() >= kMaxStepGraphs) {  // evict the least recently used
             size_t lru = 0;
             for (size_t i = 1; i < g_step_graphs.size(); ++i)
                 if (g_step_graphs[i].last_use < g_step_graphs[lru].last_use) lru = i;
-            (void)hipGraphExecDestroy(g_step_graphs[lru].exec);
+            StepGraph& old = g_step_graphs[lru];
+            (void)hipEventSynchronize(old.done);  // its last replay may still be running
+            (void)hipGraphExecDestroy(old.exec);
+            (void)hipEventDestroy(old.done);
             g_step_graphs.erase(g_step_graphs.begin() + (long)lru);
         }
-        g_step_graphs.push_back(StepGraph{a, hstate, dev, exec, 0});
+        g_step_graphs.push_back(StepGraph{a, hstate, dev, exec, done, 0});
         hit = &g_step_graphs.back();
     }
     hit->last_use = ++g_step_use;
-    return hipGraphLaunch(hit->exec, s);
+    e = hipGraphLaunch(hit->exec, s);
+    if (e != hipSuccess) return e;
+    return hipEventRecord(hit->done, s);
 }
 
 }  // namespace isam

@@ -178,3 +178,24 @@ def test_hidden_too_large_for_lds_runs_stepwise(dt, monkeypatch):
     monkeypatch.setenv("ISAM_GRU_MODE", "persistent")
     H = 6144 if dt == "bf16" else 3072
     _run(3, 2, 64, H, dt, seed=5, with_h0=True, scale=1 / 64)
+
+
+def test_step_graph_cache_eviction(monkeypatch):
+    # More distinct call signatures than the graph cache holds (32): every call still
+    # matches the oracle, and a signature evicted earlier is rebuilt when it returns.
+    monkeypatch.setenv("ISAM_GRU_MODE", "steps")
+    T, B, I, H = 3, 2, 32, 64
+    x, W, U, b, _, _ = _inputs(T, B, I, H, seed=41, scale=1 / 4)
+    args = [to_gpu(bits(a)) for a in (x, W, U)]
+    ref = oracle.gru(bits(x), bits(W), bits(U), b, None, None)
+    need = isam.gru_forward_workspace_size(T, B, I, H, isam.ISAM_BF16)
+    pool = torch.empty(need + 40 * 256, device="cuda", dtype=torch.uint8)
+    outs = []
+    for i in list(range(36)) + [0, 1]:
+        ws = pool[i * 256: i * 256 + need]
+        hs, _ = isam.gru_forward(*args, bias=to_gpu(b), workspace=ws)
+        outs.append(hs)
+    torch.cuda.synchronize()
+    for hs in outs:
+        err = float(np.max(np.abs(hs.cpu().numpy().astype(np.float64) - ref)))
+        assert err <= TOL_BF16, err
