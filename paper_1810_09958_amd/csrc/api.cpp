@@ -136,6 +136,15 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
         p.k_splits = (int)cdiv(K, p.k_per_split);
         return p;
     }
+    // Small products (few 32x32 output tiles, moderate K): one tile per
+    // workgroup with the waves splitting K (A K-contiguous and aligned, batch 1:
+    // checked at dispatch; the tile kernels are the fallback).
+    const bool small_off = getenv("ISAM_GEMM_CONFIG") && strstr(getenv("ISAM_GEMM_CONFIG"), "small=0");
+    if (allow_skinny && !small_off && gemm_small_fits(M, N, K)) {
+        p.tile = kTile64x64;
+        p.small = 1;
+        return p;
+    }
     // Tile choice (measured on MI355X): 256x256 tiles (8 waves) whenever they
     // fill the CUs; for deep K, 256x256 tiles split along K until they do
     // (the partial sums cost one extra pass over C); otherwise the largest
@@ -273,6 +282,9 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
             p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
             p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
         }
+    } else if (p.small && (!p.vec || trans_a || K == 0)) {
+        p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
+        p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     } else if (p.skinny && (!p.vec || trans_a || trans_b || K == 0)) {
         p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
         p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
@@ -288,9 +300,9 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         if (p.tile != kTile64x64 && p.tile != kTile128x32) p.tile = kTile64x64;
     }
     if (log_enabled())
-        fprintf(stderr, "[isam] %s M=%lld N=%lld K=%lld ta=%d tb=%d ab=%d c=%d tile=%d vec=%d splits=%d kps=%lld group=%d xcd=%d dma=%d\n",
+        fprintf(stderr, "[isam] %s M=%lld N=%lld K=%lld ta=%d tb=%d ab=%d c=%d tile=%d vec=%d splits=%d kps=%lld group=%d xcd=%d dma=%d skinny=%d small=%d\n",
                 who, (long long)M, (long long)N, (long long)K, trans_a, trans_b, ab_type, c_type, p.tile, p.vec,
-                p.k_splits, (long long)p.k_per_split, p.group_m, p.xcd_remap, p.dma);
+                p.k_splits, (long long)p.k_per_split, p.group_m, p.xcd_remap, p.dma, p.skinny, p.small);
     GemmArgs a{};
     a.A = A;
     a.B = B;

@@ -96,9 +96,10 @@ hipError_t launch_splitk_reduce(const GemmArgs& a, int splits, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
-    if (a.batch > 1 && (p.k_splits > 1 || p.skinny)) return hipErrorInvalidValue;
+    if (a.batch > 1 && (p.k_splits > 1 || p.skinny || p.small)) return hipErrorInvalidValue;
     if (p.skinny == 2) return launch_skinny_rows(a, s);
     if (p.skinny == 4) return launch_narrow(a, s);
+    if (p.small) return launch_gemm_small(a, s);
     if (p.skinny) {
         hipError_t e = launch_skinny(a, p.k_splits, s);
         if (e != hipSuccess || p.k_splits <= 1) return e;

@@ -53,7 +53,14 @@ struct GemmPlan {
     int skinny;      // 1: streaming kernel for N <= 32 (k_splits = K slices of skinny_k_slice);
                      // 2: bf16 row-streaming kernel (16 rows per workgroup, whole K, no split);
                      // 4: narrow dot-product kernel (N < 8, not a multiple of the vector width)
+    int small;       // 1: small-product kernel (one 32x32 tile per workgroup, waves split K)
 };
+// Small products: at most kSmallMaxTiles output tiles of 32x32 and K <= kSmallMaxK
+// (A K-contiguous, 16-byte aligned operands, batch 1: checked by the caller).
+constexpr int64_t kSmallMaxTiles = 64;
+constexpr int64_t kSmallMaxK = 1024;
+bool gemm_small_fits(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_small(const GemmArgs& a, hipStream_t s);
 int64_t skinny_k_slice(int ab_type);
 int skinny_rows_per_wg(int ab_type);
 hipError_t launch_skinny(const GemmArgs& a, int splits, hipStream_t s);

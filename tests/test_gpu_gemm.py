@@ -182,3 +182,23 @@ def test_skinny_accumulate_and_fallback_layouts():
     _run_case(513, 32, 5000, "f32", "f32", accumulate=True)
     _run_case(300, 32, 2048, "bf16", "f32", ta=1)      # transposed A: tile kernel
     _run_case(300, 16, 2048, "bf16", "f32", tb=1)      # transposed B: tile kernel
+
+
+# Small products (at most 64 output tiles of 32x32, K <= 1024, A K-contiguous and aligned):
+# one tile per workgroup with the four waves splitting K.  Ragged M and N, K that is not a
+# multiple of the MFMA step (only of the 16-byte piece), both B layouts, accumulate and both
+# output types; the same shapes through the tile kernels (small=0) agree within the tolerance.
+@pytest.mark.parametrize("dt,ct", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16"), ("f32", "bf16")])
+@pytest.mark.parametrize("tb", [0, 1])
+@pytest.mark.parametrize("shape", [(128, 128, 128), (33, 250, 24), (256, 256, 1024), (1, 40, 8), (100, 64, 520)])
+def test_small_products(dt, ct, tb, shape):
+    M, N, K = shape
+    _run_case(M, N, K, dt, ct, tb=tb, seed=M + N + K)
+
+
+@pytest.mark.parametrize("dt,ct", [("f32", "f32"), ("bf16", "bf16")])
+def test_small_products_accumulate_and_tile_path(dt, ct, monkeypatch):
+    _run_case(96, 160, 200, dt, ct, accumulate=True, seed=5)
+    _run_case(96, 160, 200, dt, ct, tb=1, accumulate=True, seed=6)
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "small=0")
+    _run_case(96, 160, 200, dt, ct, accumulate=True, seed=5)
