@@ -275,8 +275,9 @@ def main():
     s1 = workloads.gemm_small_fp32()
     A1, B1 = gpu(s1["A"]), gpu(s1["B"])
     C1 = torch.empty((128, 128), device=dev)
+    ws1 = torch.empty(max(1, isam.gemm_workspace_size(128, 128, 128, 0, 0)), device=dev, dtype=torch.uint8)
     if want("gemm_128x128x128_f32"):
-        comps.append(("gemm_128x128x128_f32", lambda: isam.gemm(A1, B1, C1),
+        comps.append(("gemm_128x128x128_f32", lambda: isam.gemm(A1, B1, C1, workspace=ws1),
                       {"kind": "gemm_f32", "flop": 2.0 * 128 ** 3, "bytes": 3 * 4 * 128 * 128}))
     torch.cuda.synchronize()
     t_setup = time.time() - t_setup
