@@ -24,6 +24,7 @@
 //
 // All workgroups must be co-resident (cooperative launch); every barrier
 // wait is bounded and raises an error flag instead of spinning forever.
+#include <cstdlib>
 #include <mutex>
 #include <vector>
 
@@ -534,7 +535,41 @@ hipError_t build_step_graph(const GruArgs& a, float* hstate, hipGraphExec_t* out
 }
 }  // namespace
 
+// Long sequences are launched step by step instead (a graph of T+1 nodes
+// costs host memory and build time in proportion to T).
+constexpr int64_t kMaxGraphSteps = 4096;
+
+static hipError_t launch_gru_steps_direct(const GruArgs& a, float* hstate, hipStream_t s) {
+    const bool bf = a.w_type == kBF16;
+    const size_t red = (size_t)kWaves * gru_rows(a.units_per_wg) * kRedLd * sizeof(float);
+    if (bf) hipLaunchKernelGGL(gru_step_init_kernel<bf16_t>, dim3(state_blocks(a)), dim3(256), 0, s, a, hstate);
+    else hipLaunchKernelGGL(gru_step_init_kernel<float>, dim3(state_blocks(a)), dim3(256), 0, s, a, hstate);
+    hipError_t e = hipGetLastError();
+    const int mt = gru_rows(a.units_per_wg) / 16;
+    for (int64_t t = 0; t < a.T && e == hipSuccess; ++t) {
+        const dim3 grid(a.n_wg), block(64 * kWaves);
+        switch (mt) {
+            case 1:
+                if (bf) hipLaunchKernelGGL((gru_step_kernel<bf16_t, 1>), grid, block, red, s, a, hstate, t);
+                else hipLaunchKernelGGL((gru_step_kernel<float, 1>), grid, block, red, s, a, hstate, t);
+                break;
+            case 2:
+                if (bf) hipLaunchKernelGGL((gru_step_kernel<bf16_t, 2>), grid, block, red, s, a, hstate, t);
+                else hipLaunchKernelGGL((gru_step_kernel<float, 2>), grid, block, red, s, a, hstate, t);
+                break;
+            case 3:
+                if (bf) hipLaunchKernelGGL((gru_step_kernel<bf16_t, 3>), grid, block, red, s, a, hstate, t);
+                else hipLaunchKernelGGL((gru_step_kernel<float, 3>), grid, block, red, s, a, hstate, t);
+                break;
+            default: return hipErrorInvalidValue;
+        }
+        e = hipGetLastError();
+    }
+    return e;
+}
+
 hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s) {
+    if (a.T > kMaxGraphSteps || getenv("ISAM_GRU_NO_GRAPH")) return launch_gru_steps_direct(a, hstate, s);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;

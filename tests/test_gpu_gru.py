@@ -199,3 +199,37 @@ def test_step_graph_cache_eviction(monkeypatch):
     for hs in outs:
         err = float(np.max(np.abs(hs.cpu().numpy().astype(np.float64) - ref)))
         assert err <= TOL_BF16, err
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_step_kernels_without_graph_match(dt, monkeypatch):
+    # Sequences longer than the graph limit launch the step kernels one by one; the same
+    # kernels give the same bits either way (forced here with ISAM_GRU_NO_GRAPH).
+    monkeypatch.setenv("ISAM_GRU_MODE", "steps")
+    T, B, I, H = 6, 3, 48, 128
+    x, W, U, b, h0, _ = _inputs(T, B, I, H, seed=17, scale=1 / 4, with_h0=True)
+    if dt == "bf16":
+        x, W, U = bits(x), bits(W), bits(U)
+    args = [to_gpu(a) for a in (x, W, U)]
+    g_hs, g_hT = isam.gru_forward(*args, bias=to_gpu(b), h0=to_gpu(h0))
+    monkeypatch.setenv("ISAM_GRU_NO_GRAPH", "1")
+    d_hs, d_hT = isam.gru_forward(*args, bias=to_gpu(b), h0=to_gpu(h0))
+    torch.cuda.synchronize()
+    assert torch.equal(g_hs, d_hs) and torch.equal(g_hT, d_hT)
+    ref = oracle.gru(x, W, U, b, None, h0)
+    err = float(np.max(np.abs(d_hs.cpu().numpy().astype(np.float64) - ref)))
+    assert err <= (TOL_BF16 if dt == "bf16" else TOL_F32), err
+
+
+def test_long_sequence_beyond_graph_limit(monkeypatch):
+    # T = 4097 (> 4096 steps per graph): the step kernels are launched one by one.
+    monkeypatch.setenv("ISAM_GRU_MODE", "steps")
+    T, B, I, H = 4097, 1, 16, 64
+    x, W, U, b, h0, _ = _inputs(T, B, I, H, seed=23, scale=1 / 4, with_h0=True)
+    x, W, U = bits(x), bits(W), bits(U)
+    hs, hT = isam.gru_forward(to_gpu(x), to_gpu(W), to_gpu(U), bias=to_gpu(b), h0=to_gpu(h0))
+    torch.cuda.synchronize()
+    ref = oracle.gru(x, W, U, b, None, h0)
+    err = float(np.max(np.abs(hs.cpu().numpy().astype(np.float64) - ref)))
+    assert err <= TOL_BF16, err
+    assert np.array_equal(hT.cpu().numpy(), hs[-1].cpu().numpy())
