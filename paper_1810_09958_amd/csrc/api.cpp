@@ -124,7 +124,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     // fallback).
     if (allow_skinny && N <= 32 && K > 0 && N % (ab_type == kBF16 ? 8 : 4) == 0 && !skinny_off) {
         p.tile = kTile128x32;
-        if (ab_type == kBF16 && cdiv(M, skinny_stream_rows()) >= cus / 2) {
+        const bool rows_off = getenv("ISAM_GEMM_CONFIG") && strstr(getenv("ISAM_GEMM_CONFIG"), "rows=0");
+        if (!rows_off && cdiv(M, skinny_stream_rows()) >= cus / 2) {
             // Enough 16-row workgroups to cover the CUs: one pass over A, no split.
             p.skinny = 2;
             p.k_splits = 1;

@@ -340,6 +340,143 @@ __global__ __launch_bounds__(64 * kSkWaves) void skinny_rows_kernel(GemmArgs a) 
     }
 }
 
+// fp32 row-streaming variant: the same one-pass structure (16 rows per
+// workgroup, 8 waves splitting K, a private 3-stage pipeline of direct-to-LDS
+// copies per wave, fixed-order cross-wave sum), with 32-deep K chunks (A rows
+// of 128 bytes -- whole lines; B 32 K rows x 32 columns, 128-byte rows) and
+// 16x16x4 fp32 MFMAs fed one value per lane by ds_read_b32: MFMA s of a
+// chunk takes K = 4s + q from lane quarter q for both operands.  LDS layouts
+// per stage: A row r chunk c at c ^ ((r >> 1) & 7); B K row k 16-byte unit u
+// at u ^ (4 * ((k >> 1) & 1)) -- the 64 lanes of every read then fall on 64
+// different banks.  Measured against two other schedules (reads of chunk
+// c+1 issued during chunk c's MFMAs, with 8 waves x 3 stages or 4 waves x 6
+// stages): this one is the fastest (4096x32x4096: 23-25 us against 27-36).
+constexpr int kF32Waves = kSkWaves;
+constexpr int kF32Stages = kStreamStages;
+constexpr int kF32StageA = kRowsPerWg * 128;  // 2 KB
+constexpr int kF32StageB = 32 * 128;          // 4 KB
+constexpr int kF32Stage = kF32StageA + kF32StageB;
+constexpr int kF32CopiesPerChunk = 6;          // 2 A + 4 B copies of 1 KB
+
+__device__ __forceinline__ uint32_t srf_a_off(int r, int k) {
+    return (uint32_t)(r * 128 + ((((k >> 2) ^ sr_a_swz(r))) << 4) + (k & 3) * 4);
+}
+__device__ __forceinline__ uint32_t srf_b_off(int k, int n) {
+    return (uint32_t)(k * 128 + ((((n >> 2) ^ (4 * ((k >> 1) & 1)))) << 4) + (n & 3) * 4);
+}
+
+__global__ __launch_bounds__(64 * kF32Waves) void skinny_rows_f32_kernel(GemmArgs a) {
+    __shared__ __attribute__((aligned(1024))) char smem[kF32Waves * kF32Stages * kF32Stage];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int64_t m0 = (int64_t)blockIdx.x * kRowsPerWg;
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(a.A, (uint32_t)(((a.M - 1) * a.lda + a.K) * 4));
+    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(a.B, (uint32_t)(((a.K - 1) * a.ldb + a.N) * 4));
+    char* ws = smem + wid * kF32Stages * kF32Stage;  // this wave's stages
+
+    // This wave's K range, in 32-deep chunks.
+    const int64_t nchunk_all = (a.K + 31) / 32;
+    const int64_t c_lo = nchunk_all * wid / kF32Waves, c_hi = nchunk_all * (wid + 1) / kF32Waves;
+    const int nc = (int)(c_hi - c_lo);
+
+    // Copy plan: A copy q (0..1) fills rows 8q .. 8q+7 (lane -> row 8q + lane/8,
+    // physical chunk lane%8); B copy q (0..3) fills K rows 8q .. 8q+7 (lane ->
+    // row 8q + lane/8, physical unit lane%8).
+    int64_t a_row_off[2];
+    int a_k[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int r = 8 * q + (lane >> 3), pc = lane & 7;
+        a_k[q] = (pc ^ sr_a_swz(r)) * 4;
+        a_row_off[q] = (m0 + r < a.M) ? (m0 + r) * a.lda : -1;
+    }
+    int b_kr[4], b_n[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int k = 8 * q + (lane >> 3), pu = lane & 7;
+        b_kr[q] = k;
+        b_n[q] = (pu ^ (4 * ((k >> 1) & 1))) * 4;
+    }
+    auto issue = [&](int c) {  // chunk index relative to this wave
+        char* st = ws + (c % kF32Stages) * kF32Stage;
+        const int64_t k0 = (c_lo + c) * 32;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int64_t k = k0 + a_k[q];
+            const uint32_t off = (a_row_off[q] >= 0 && k < a.K) ? (uint32_t)((a_row_off[q] + k) * 4) : kOob;
+            sk_dma16(rsA, __builtin_amdgcn_readfirstlane(sk_lds_addr(st + q * 1024)), off);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t k = k0 + b_kr[q];
+            const uint32_t off = (k < a.K && b_n[q] < a.N) ? (uint32_t)((k * a.ldb + b_n[q]) * 4) : kOob;
+            sk_dma16(rsB, __builtin_amdgcn_readfirstlane(sk_lds_addr(st + kF32StageA + q * 1024)), off);
+        }
+    };
+    const int g = lane >> 4, li = lane & 15;
+    // Operands of one chunk: A value and two B values for each of its 8 MFMA K steps.
+    struct Frags {
+        float av[8], bv[2][8];
+    };
+    auto read_chunk = [&](int c, Frags& f) {
+        const char* st = ws + (c % kF32Stages) * kF32Stage;
+#pragma unroll
+        for (int s8 = 0; s8 < 8; ++s8) {
+            const int k = 4 * s8 + g;
+            f.av[s8] = *reinterpret_cast<const float*>(st + srf_a_off(li, k));
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+                f.bv[nt][s8] = *reinterpret_cast<const float*>(st + kF32StageA + srf_b_off(k, nt * 16 + li));
+        }
+    };
+
+    f32x4_t acc[2];
+    acc[0] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    acc[1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // chunk c is waited for LEAD-1 chunks after its copies were issued
+    constexpr int LEAD = kF32Stages - 1;
+    for (int c = 0; c < LEAD && c < nc; ++c) issue(c);
+    for (int c = 0; c < nc; ++c) {
+        if (c + LEAD - 1 < nc) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((LEAD - 1) * kF32CopiesPerChunk) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        Frags cur;
+        read_chunk(c, cur);
+#pragma unroll
+        for (int s8 = 0; s8 < 8; ++s8)
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.av[s8], cur.bv[nt][s8], acc[nt], 0, 0, 0);
+        // the stage of chunk c-1 (read in the previous iteration) takes chunk c + LEAD
+        if (c + LEAD < nc) issue(c + LEAD);
+    }
+
+    // Sum the waves' 16x32 tiles in wave order (stages no longer needed).
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(smem);  // [wave][16][32]
+    // acc[nt] element v of lane l: row 4*(l/16) + v, column nt*16 + l%16
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) red[(wid * 16 + 4 * g + v) * 32 + nt * 16 + li] = acc[nt][v];
+    __syncthreads();
+    for (int o = tid; o < kRowsPerWg * 32; o += 64 * kF32Waves) {
+        const int row = o >> 5, col = o & 31;
+        float sum = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kF32Waves; ++w) sum += red[(w * 16 + row) * 32 + col];
+        const int64_t gr = m0 + row;
+        if (gr >= a.M || col >= a.N) continue;
+        const int64_t idx = gr * a.ldc + col;
+        if (a.bias) sum += a.bias[col];
+        if (a.c_type == kF32) {
+            float* C = static_cast<float*>(a.C);
+            C[idx] = a.accumulate ? C[idx] + sum : sum;
+        } else {
+            uint16_t* C = static_cast<uint16_t*>(a.C);
+            C[idx] = (uint16_t)f32_to_bf16(a.accumulate ? bf16_to_f32(C[idx]) + sum : sum);
+        }
+    }
+}
+
 // Narrow product (N < 8, any ldb): the batch-1..7 matrix-vector form, where
 // the paper's mapper would pick a dot-product instruction rather than a
 // matrix one (Section 4).  Bound by streaming A once.  A workgroup owns 8
@@ -515,7 +652,8 @@ hipError_t launch_narrow(const GemmArgs& a, hipStream_t s) {
 
 hipError_t launch_skinny_rows(const GemmArgs& a, hipStream_t s) {
     const dim3 grid((unsigned)((a.M + kRowsPerWg - 1) / kRowsPerWg)), block(64 * kSkWaves);
-    hipLaunchKernelGGL(skinny_rows_kernel, grid, block, 0, s, a);
+    if (a.ab_type == kBF16) hipLaunchKernelGGL(skinny_rows_kernel, grid, block, 0, s, a);
+    else hipLaunchKernelGGL(skinny_rows_f32_kernel, grid, dim3(64 * kF32Waves), 0, s, a);
     return hipGetLastError();
 }
 
