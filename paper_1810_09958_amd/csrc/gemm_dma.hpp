@@ -129,20 +129,22 @@ struct DmaCopier {
             }
         }
     }
-    // A copy instruction Q of the K tile starting at k0 into region `dst`.
+    // A copy instruction Q of the K tile starting at k0 into the A region at
+    // LDS address `dst` (a wave-uniform 32-bit LDS address, so no generic-
+    // pointer conversion is redone per copy).
     template <int Q>
-    __device__ __forceinline__ void a_part(int64_t k0, char* dst) const {
+    __device__ __forceinline__ void a_part(int64_t k0, uint32_t dst) const {
         const int64_t k = k0 + a_k[Q];
         const uint32_t off = (a_row_off[Q] >= 0 && k < kend) ? (uint32_t)((a_row_off[Q] + k) * 2) : kOob;
-        dma16(rsA, __builtin_amdgcn_readfirstlane(lds_addr_of(dst + (wid * A_INSTR + Q) * 1024)), off);
+        dma16(rsA, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * A_INSTR + Q) * 1024)), off);
     }
     template <int Q>
-    __device__ __forceinline__ void b_part(int64_t k0, char* dst) const {
+    __device__ __forceinline__ void b_part(int64_t k0, uint32_t dst) const {
         const int64_t k = k0 + b_k[Q];
         uint32_t off;
         if constexpr (TB) off = (b_off[Q] >= 0 && k < kend) ? (uint32_t)((b_off[Q] + k) * 2) : kOob;
         else off = (b_off[Q] >= 0 && k < kend) ? (uint32_t)((k * ldb + b_off[Q]) * 2) : kOob;
-        dma16(rsB, __builtin_amdgcn_readfirstlane(lds_addr_of(dst + (wid * B_INSTR + Q) * 1024)), off);
+        dma16(rsB, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * B_INSTR + Q) * 1024)), off);
     }
 };
 
@@ -281,7 +283,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     constexpr int A_INSTR = Copier::A_INSTR, PER_TILE = Copier::A_INSTR + Copier::B_INSTR;
     static_assert(PER_TILE < 64, "vmcnt range");
     static_assert(NW * 32 * (WTN * 4 + 16) <= STAGES * STAGE, "epilogue staging must fit in LDS");
-    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+    // Two stages, then one idle block that copies of K tiles past the end
+    // are sent to (see below).
+    constexpr int SINK = 1024 * (A_INSTR > Copier::B_INSTR ? A_INSTR : Copier::B_INSTR) * NW;
+    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE + SINK];
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int wm = wid / WN, wn = wid % WN;
@@ -294,12 +299,16 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     const Copier cp(a, m0, n0, kend, wid, lane);
 
     // Copy instruction Q of K tile `tile` (A first, then B) into its stage.
+    // Copies are issued without a branch: those of a K tile past the last one
+    // read nothing (every offset is out of range) and land in the idle sink
+    // block -- in the last iteration their stage may still be being read.
+    const uint32_t smem_base = lds_addr_of(smem);
     auto issue_part = [&](int tile, auto q_c) {
         constexpr int q = decltype(q_c)::value;
-        char* sa = smem + (tile & 1) * STAGE;
+        const uint32_t sa = tile < nk ? smem_base + (uint32_t)((tile & 1) * STAGE) : smem_base + (uint32_t)(STAGES * STAGE);
         const int64_t k0 = kbeg + (int64_t)tile * BK;
         if constexpr (q < A_INSTR) cp.template a_part<q>(k0, sa);
-        else cp.template b_part<q - A_INSTR>(k0, sa + A_BYTES);
+        else cp.template b_part<q - A_INSTR>(k0, tile < nk ? sa + (uint32_t)A_BYTES : sa);
     };
 
     f32x16_t acc[MI][NI];
@@ -326,10 +335,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             __builtin_amdgcn_sched_barrier(0);
         });
     };
-    // MFMAs of f with the N_READS reads of (stage, ks) into g, plus (when
-    // copy) the PER_TILE copies of tile ct, spread evenly over the MFMA slots
+    // MFMAs of f with the N_READS reads of (stage, ks) into g, plus (NC > 0)
+    // the PER_TILE copies of tile ct, spread evenly over the MFMA slots
     // (slot k issues side ops [k*NOPS/S, (k+1)*NOPS/S), reads first).
-    auto step = [&](const F& f, F& g, int stage, int ks, auto nc_c, bool copy, int ct) {
+    auto step = [&](const F& f, F& g, int stage, int ks, auto nc_c, int ct) {
         constexpr int NC = decltype(nc_c)::value;
         mfma_with(f, [&](auto kc) {
             constexpr int k = decltype(kc)::value;
@@ -338,7 +347,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             static_for<hi - lo>([&](auto d) {
                 constexpr int o = lo + decltype(d)::value;
                 if constexpr (o < N_READS) read_part(g, stage, ks, std::integral_constant<int, o>{});
-                else if (copy) issue_part(ct, std::integral_constant<int, o - N_READS>{});
+                else if constexpr (NC > 0) issue_part(ct, std::integral_constant<int, o - N_READS>{});
             });
         });
     };
@@ -359,11 +368,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
         for (int t = 0; t < nk; ++t) {
             const int st = t & 1;
             __builtin_amdgcn_sched_barrier(0);
-            step(f0, f1, st, 1, None{}, false, 0);
+            step(f0, f1, st, 1, None{}, 0);
             __builtin_amdgcn_s_waitcnt(0xc07f);
-            step(f1, f0, st, 2, None{}, false, 0);
+            step(f1, f0, st, 2, None{}, 0);
             __builtin_amdgcn_s_waitcnt(0xc07f);
-            step(f0, f1, st, 3, None{}, false, 0);
+            step(f0, f1, st, 3, None{}, 0);
             __builtin_amdgcn_s_waitcnt(0xc07f);
             if (t + 1 < nk) {
                 vm_wait<0>();  // only tile t+1's copies are in flight here
@@ -372,7 +381,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             // Reads of step 0 of tile t+1 are unconditional (after the last
             // tile they read an idle stage and are unused) so every path
             // reaching the MFMAs has the same LDS requests in flight.
-            step(f1, f0, st ^ 1, 0, std::integral_constant<int, PER_TILE>{}, t + 2 < nk, t + 2);
+            step(f1, f0, st ^ 1, 0, std::integral_constant<int, PER_TILE>{}, t + 2);
             // The next K step's fragments were requested during these MFMAs;
             // waiting here tells the compiler nothing is pending at the loop
             // head, which keeps it from draining reads it does not need.
