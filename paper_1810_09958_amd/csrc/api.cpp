@@ -164,12 +164,15 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
             p.k_per_split = cdiv(cdiv(K, sp), bk) * bk;
             p.k_splits = (int)cdiv(K, p.k_per_split);
         }
+    } else if (K <= 2048 && tiles(kTile128x128) >= cus) {
+        // Shallow K: the 128x128 grid (measured, bf16 NT, K = 1024: 2048x3072
+        // 24 us against 27 for 128x64; 4096x3072 39 us against 55 for 256x128,
+        // whose 384 tiles leave half the CUs idle in the second round).
+        p.tile = kTile128x128;
     } else if (tiles(kTile256x128) >= cus) {
         p.tile = kTile256x128;
     } else if (tiles(kTile128x128) >= cus) {
-        // Shallow K with under two tiles per CU: the 128x64 grid balances
-        // better (measured: 2048x3072x1024 bf16 27 us vs 38 us).
-        p.tile = (K <= 2048 && tiles(kTile128x128) < 2 * (int64_t)cus) ? kTile128x64 : kTile128x128;
+        p.tile = kTile128x128;
     } else if (tiles(kTile128x64) >= cus) {
         p.tile = kTile128x64;
     } else {
