@@ -426,12 +426,13 @@ def cpu_baseline():
     sq = workloads.gemm_square_bf16()
     A, B = sq["A_bf16"], sq["B_bf16"]
     threads = oracle.max_threads()
-    # pilot, then scale the sample to about 12 s of oracle work
-    rows = max(16, threads)
+    # pilot, then scale the sample to 10-15 s of oracle work (the pilot's fixed costs make it
+    # overestimate the per-row time about twofold, hence the 24 s target)
+    rows = max(32, 2 * threads)
     t = time.perf_counter()
     oracle.gemm(np.ascontiguousarray(A[:rows]), B, rows, 8192, 8192, with_norm=False)
     dt = time.perf_counter() - t
-    rows2 = int(min(8192, rows * 12.0 / max(dt, 1e-3)))
+    rows2 = int(min(8192, rows * 24.0 / max(dt, 1e-3)))
     rows2 = max(threads, (rows2 // threads) * threads)
     t = time.perf_counter()
     oracle.gemm(np.ascontiguousarray(A[:rows2]), B, rows2, 8192, 8192, with_norm=False)
