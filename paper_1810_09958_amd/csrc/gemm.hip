@@ -6,7 +6,7 @@ namespace isam {
 
 GemmKernelFn gemm_kernel_bf16(int tile, int ta, int tb, int vec);
 GemmKernelFn gemm_kernel_f32(int tile, int ta, int tb, int vec);
-GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves);
+GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves, bool k_full);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk) {
     static const int dims[kTileCount][2] = {{256, 256}, {256, 128}, {128, 128},
@@ -110,9 +110,11 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     GemmKernelFn fn = nullptr;
     int threads = 256;
     if (p.dma && a.ab_type == kBF16 && !a.trans_a && p.vec) {
-        fn = gemm_dma_kernel_for(p.tile, a.trans_b, p.dma_waves);
+        // every K slice a whole number of 64-deep tiles: copies with base + delta offsets
+        const bool k_full = a.K % 64 == 0 && (p.k_splits <= 1 || p.k_per_split % 64 == 0);
+        fn = gemm_dma_kernel_for(p.tile, a.trans_b, p.dma_waves, k_full);
         if (fn && p.dma_waves == 8 && (p.tile == kTile256x256 || p.tile == kTile256x128)) threads = 512;
-        else fn = gemm_dma_kernel_for(p.tile, a.trans_b, 4);
+        else fn = gemm_dma_kernel_for(p.tile, a.trans_b, 4, k_full);
     }
     if (!fn)
         fn = a.ab_type == kBF16 ? gemm_kernel_bf16(p.tile, a.trans_a, a.trans_b, p.vec)

@@ -4,10 +4,12 @@
 
 namespace isam {
 
-GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves) {
+GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves, bool k_full) {
     if (waves == 8) {
         switch (tile) {
             case kTile256x256:
+                if (k_full)
+                    return trans_b ? gemm_dma_kernel<256, 256, true, 2, 4, true> : gemm_dma_kernel<256, 256, false, 2, 4, true>;
                 return trans_b ? gemm_dma_kernel<256, 256, true, 2, 4> : gemm_dma_kernel<256, 256, false, 2, 4>;
             case kTile256x128:
                 return trans_b ? gemm_dma_kernel<256, 128, true, 4, 2> : gemm_dma_kernel<256, 128, false, 4, 2>;

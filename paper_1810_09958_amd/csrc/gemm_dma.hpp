@@ -96,6 +96,9 @@ struct DmaCopier {
     __amdgpu_buffer_rsrc_t rsA, rsB;
     int64_t a_row_off[A_INSTR], b_off[B_INSTR];
     int a_k[A_INSTR], b_k[B_INSTR];
+    // Byte offsets of each copy for the K tile at k = 0 (kOob outside M / N):
+    // for a K tile wholly inside K the offset is base + a wave-uniform delta.
+    uint32_t a_base[A_INSTR], b_base[B_INSTR];
     int64_t ldb, kend;
     int wid;
 
@@ -111,6 +114,7 @@ struct DmaCopier {
             const int r = unit >> 3, pc = unit & 7;
             a_k[q] = (pc ^ dma_a_swz(r)) * 8;
             a_row_off[q] = (m0 + r < a.M) ? (m0 + r) * a.lda : -1;
+            a_base[q] = a_row_off[q] >= 0 ? (uint32_t)((a_row_off[q] + a_k[q]) * 2) : kOob;
         }
 #pragma unroll
         for (int q = 0; q < B_INSTR; ++q) {
@@ -127,7 +131,19 @@ struct DmaCopier {
                 b_k[q] = k;
                 b_off[q] = (n < a.N) ? n : -1;
             }
+            if constexpr (TB) b_base[q] = b_off[q] >= 0 ? (uint32_t)((b_off[q] + b_k[q]) * 2) : kOob;
+            else b_base[q] = b_off[q] >= 0 ? (uint32_t)((b_k[q] * ldb + b_off[q]) * 2) : kOob;
         }
+    }
+    // Copies of a K tile wholly inside K: offset = base + the tile's delta
+    // (k0 * 2 bytes for A and K-contiguous B, k0 * ldb * 2 for N-contiguous B).
+    template <int Q>
+    __device__ __forceinline__ void a_part_full(uint32_t delta, uint32_t dst) const {
+        dma16(rsA, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * A_INSTR + Q) * 1024)), a_base[Q] + delta);
+    }
+    template <int Q>
+    __device__ __forceinline__ void b_part_full(uint32_t delta, uint32_t dst) const {
+        dma16(rsB, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * B_INSTR + Q) * 1024)), b_base[Q] + delta);
     }
     // A copy instruction Q of the K tile starting at k0 into the A region at
     // LDS address `dst` (a wave-uniform 32-bit LDS address, so no generic-
@@ -273,7 +289,9 @@ __device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc
 //     t, so it may be overwritten)
 //   ks 3:    MFMAs of step 3, reads of step 0 of tile t+1, copies of tile
 //            t+2 into stage t & 1
-template <int BM, int BN, bool TB, int WM = 2, int WN = 2>
+// KFULL: every K slice is a whole number of 64-deep tiles, so the copies take
+// their offsets as base + delta (one add per copy instead of the range checks).
+template <int BM, int BN, bool TB, int WM = 2, int WN = 2, bool KFULL = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
     gemm_batch_offset(a);
     constexpr int NW = WM * WN, STAGES = 2, BK = 64;
@@ -307,8 +325,16 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
         constexpr int q = decltype(q_c)::value;
         const uint32_t sa = tile < nk ? smem_base + (uint32_t)((tile & 1) * STAGE) : smem_base + (uint32_t)(STAGES * STAGE);
         const int64_t k0 = kbeg + (int64_t)tile * BK;
-        if constexpr (q < A_INSTR) cp.template a_part<q>(k0, sa);
-        else cp.template b_part<q - A_INSTR>(k0, tile < nk ? sa + (uint32_t)A_BYTES : sa);
+        const uint32_t sb = tile < nk ? sa + (uint32_t)A_BYTES : sa;
+        if constexpr (KFULL) {
+            // past the last tile the offsets may land anywhere inside the
+            // buffers or past them: the bytes go to the sink
+            if constexpr (q < A_INSTR) cp.template a_part_full<q>((uint32_t)(k0 * 2), sa);
+            else cp.template b_part_full<q - A_INSTR>((uint32_t)(TB ? k0 * 2 : k0 * a.ldb * 2), sb);
+        } else {
+            if constexpr (q < A_INSTR) cp.template a_part<q>(k0, sa);
+            else cp.template b_part<q - A_INSTR>(k0, sb);
+        }
     };
 
     f32x16_t acc[MI][NI];

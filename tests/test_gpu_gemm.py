@@ -202,3 +202,21 @@ def test_small_products_accumulate_and_tile_path(dt, ct, monkeypatch):
     _run_case(96, 160, 200, dt, ct, tb=1, accumulate=True, seed=6)
     monkeypatch.setenv("ISAM_GEMM_CONFIG", "small=0")
     _run_case(96, 160, 200, dt, ct, accumulate=True, seed=5)
+
+
+# The 256x256 direct-to-LDS kernel in both copy modes: K a multiple of 64 (offsets as base +
+# per-tile delta; unsplit at 4096^2, split into K slices at 2048^2) and K with a ragged last tile (range-checked offsets); NN
+# and NT; sampled rows (first, last, spread) against the oracle.
+@pytest.mark.parametrize("K", [1024, 1000, 4160, 4100])
+@pytest.mark.parametrize("tb", [0, 1])
+def test_dma_256_tile_copy_modes(K, tb):
+    M = N = 4096 if K < 2048 else 2048   # 2048^2: 64 tiles, split along K
+    A_h = bits(synth.uniform(K, 20, (M, K), -1, 1))
+    Bm = bits(synth.uniform(K, 21, (K, N), -1, 1))
+    B_h = np.ascontiguousarray(Bm.T) if tb else Bm
+    C = isam.gemm(to_gpu(A_h), to_gpu(B_h), trans_b=bool(tb))
+    torch.cuda.synchronize()
+    rows = workloads.rows_sample(M, 24)
+    ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), Bm, len(rows), N, K)
+    got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
+    assert norm_err(got, ref, S) <= TOL_BF16
