@@ -40,7 +40,7 @@ typedef enum { ISAM_F32 = 0, ISAM_BF16 = 1 } isam_dtype_t;
 typedef enum {
     ISAM_OK = 0,
     ISAM_ERR_INVALID_ARG = 1, /* bad size, pointer, leading dimension, dtype or aliasing */
-    ISAM_ERR_UNSUPPORTED = 2, /* valid request this build does not implement */
+    ISAM_ERR_UNSUPPORTED = 2, /* valid request outside what the library implements */
     ISAM_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the *_workspace_size query */
     ISAM_ERR_HIP = 4          /* a HIP launch failed; isam_last_error() has the HIP message */
 } isam_status_t;
