@@ -84,11 +84,13 @@ def test_gemm_empty_is_noop(L):
 
 
 def test_gemm_workspace_queries(L):
-    # A deep-K, skinny-N fp32 product is split along K and needs partial-sum space;
-    # the bf16 one streams each row block through one workgroup and needs none.
-    ws = L.isam_gemm_workspace_size(0, 0, 4096, 32, 4096, F32, F32)
-    assert ws > 0 and ws % (4096 * 32 * 4) == 0
+    # A skinny-N product with enough 16-row blocks to cover the CUs streams each block
+    # through one workgroup and needs no workspace (bf16 and fp32); with few rows and deep K
+    # it is split along K and needs partial-sum space.
+    assert L.isam_gemm_workspace_size(0, 0, 4096, 32, 4096, F32, F32) == 0
     assert L.isam_gemm_workspace_size(0, 0, 4096, 32, 4096, BF16, F32) == 0
+    ws = L.isam_gemm_workspace_size(0, 0, 512, 32, 8192, F32, F32)
+    assert ws > 0 and ws % (512 * 32 * 4) == 0
     assert L.isam_gemm_workspace_size(0, 0, 8192, 8192, 8192, BF16, BF16) == 0
     assert L.isam_gemm_workspace_size(0, 0, 0, 8, 8, BF16, BF16) == 0
 
