@@ -31,11 +31,20 @@ def _dt(t: torch.Tensor) -> int:
 
 
 def _ptr(t):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    # plain ints: the ctypes signatures convert them (no per-call c_void_p objects)
+    return None if t is None else t.data_ptr()
+
+
+try:
+    _raw_stream = torch._C._cuda_getCurrentRawStream  # current stream handle, no Stream object
+except AttributeError:  # pragma: no cover - older torch
+    _raw_stream = None
 
 
 def _stream():
-    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if _raw_stream is not None:
+        return _raw_stream(torch.cuda.current_device())
+    return torch.cuda.current_stream().cuda_stream
 
 
 def _check_dev(*ts):
