@@ -220,3 +220,19 @@ def test_dma_256_tile_copy_modes(K, tb):
     ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), Bm, len(rows), N, K)
     got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
     assert norm_err(got, ref, S) <= TOL_BF16
+
+
+# The 128x128 direct-to-LDS kernel (shallow K, grid covering the CUs) in both copy modes.
+@pytest.mark.parametrize("K", [1024, 1000])
+@pytest.mark.parametrize("tb", [0, 1])
+def test_dma_128_tile_copy_modes(K, tb):
+    M, N = 2048, 3072
+    A_h = bits(synth.uniform(K, 22, (M, K), -1, 1))
+    Bm = bits(synth.uniform(K, 23, (K, N), -1, 1))
+    B_h = np.ascontiguousarray(Bm.T) if tb else Bm
+    C = isam.gemm(to_gpu(A_h), to_gpu(B_h), trans_b=bool(tb))
+    torch.cuda.synchronize()
+    rows = workloads.rows_sample(M, 24)
+    ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), Bm, len(rows), N, K)
+    got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
+    assert norm_err(got, ref, S) <= TOL_BF16
