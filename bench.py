@@ -259,6 +259,21 @@ def main():
                     sets, {"kind": "dwsep", "flop": 2.0 * 100352 * (9 * 128 + 128 * 256),
                            # fused minimum: X read once, y written once (+ the small filters)
                            "bytes": es * (32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + oes * 100352 * 256})
+    # The same convolution unfused (depthwise kernel writes Y, then the pointwise GEMM reads it):
+    # times the standalone depthwise stencil and the pointwise product as separate launches.
+    if want("dwsep_32x56x56x128_256_bf16_out_bf16_unfused"):
+        X0, Dw, P = gpu(d["X_bf16"]), gpu(d["D_bf16"]), gpu(d["P_bf16"])
+        sets = n_sets(2 * (3 * 32 * 56 * 56 * 128 + 100352 * 256))
+        Xs = [X0] + [X0.clone() for _ in range(sets - 1)]
+        ys = [torch.empty((32, 56, 56, 256), device=dev, dtype=torch.bfloat16) for _ in range(sets)]
+        wsu = [torch.empty(isam.dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, 1, 1),
+                           device=dev, dtype=torch.uint8) for _ in range(sets)]
+        add_rotated("dwsep_32x56x56x128_256_bf16_out_bf16_unfused",
+                    lambda i, Xs=Xs, Dw=Dw, P=P, ys=ys, wsu=wsu: (lambda: isam.dwsep_conv(Xs[i], Dw, P, out=ys[i], workspace=wsu[i])),
+                    sets, {"kind": "dwsep", "flop": 2.0 * 100352 * (9 * 128 + 128 * 256),
+                           "env": {"ISAM_DWSEP_FUSED": "0"},
+                           # X read, Y written and read back, y written (+ the small filters)
+                           "bytes": 2 * (3 * 32 * 56 * 56 * 128 + 9 * 128 + 128 * 256) + 2 * 100352 * 256})
     del d
 
     # -- 1D convolution (second listing) as implicit GEMM --------------------------------

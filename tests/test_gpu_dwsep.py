@@ -52,6 +52,27 @@ def test_one_pixel_image():
     _case(1, 1, 1, 8, 8, pad=1)
 
 
+# Unfused path (fusion switched off): the standalone 3x3 stride-1 depthwise kernel, then the
+# pointwise GEMM.  The LDS-staged kernel owns RS rows x SW columns per workgroup (RS: the
+# default per dtype, 8 and 3 rows): ragged last
+# row segment and column strip, one channel vector per pixel up to a whole workgroup of them,
+# a one-pixel image; more channel vectors than one workgroup holds take the register-window
+# kernel, as does every shape with the LDS-staged kernel switched off (ISAM_DW_RS=0).
+@pytest.mark.parametrize("dt,ot", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16")])
+@pytest.mark.parametrize("shape", [(2, 9, 11, 16, 24), (3, 17, 5, 64, 40), (1, 19, 57, 128, 16),
+                                   (2, 6, 7, 8, 8), (1, 1, 1, 8, 8), (1, 10, 3, 1024, 8),
+                                   (1, 5, 4, 4096, 8)])
+@pytest.mark.parametrize("rs", ["default", "8", "3", "0"])
+def test_unfused_depthwise_kernel(dt, ot, shape, rs, monkeypatch):
+    monkeypatch.setenv("ISAM_DWSEP_FUSED", "0")
+    if rs == "default":
+        monkeypatch.delenv("ISAM_DW_RS", raising=False)
+    else:
+        monkeypatch.setenv("ISAM_DW_RS", rs)
+    b, H, W, C, Co = shape
+    _case(b, H, W, C, Co, dt=dt, ot=ot, seed=H + W + C)
+
+
 @pytest.mark.parametrize("variant", ["f32", "bf16", "bf16_out_bf16"])
 def test_config_full_size_sampled_images(variant):
     d = workloads.dwsep()
@@ -67,6 +88,14 @@ def test_config_full_size_sampled_images(variant):
     got = to_host_f64(y[torch.as_tensor(imgs, device="cuda")])
     tol = TOL_F32 if variant == "f32" else TOL_BF16
     assert norm_err(got, Z, S) <= tol
+
+
+@pytest.mark.parametrize("variant", ["f32", "bf16_out_bf16"])
+def test_config_full_size_unfused(variant, monkeypatch):
+    # the full image batch through the standalone depthwise kernel and the pointwise GEMM
+    monkeypatch.setenv("ISAM_DWSEP_FUSED", "0")
+    monkeypatch.delenv("ISAM_DW_RS", raising=False)
+    test_config_full_size_sampled_images(variant)
 
 
 @pytest.mark.parametrize("ot", ["f32", "bf16"])
