@@ -5,7 +5,8 @@
 // interface (Section 4): every tiling, split and rasterisation choice is made
 // in one place (the plan_* functions below) from the problem shape and the
 // device's compute-unit count, and can be overridden for tuning with the
-// environment variable ISAM_GEMM_CONFIG="tile=<0-5>,splits=<n>,group=<n>,xcd=<0|1>,dma=<0|1>".
+// environment variable ISAM_GEMM_CONFIG="tile=<0-5>,splits=<n>,group=<n>,xcd=<0|1>,dma=<0|1>"
+// (and small=0, rows=0, skinny=0, stream=0|1 for the special-shape kernels).
 // ISAM_LOG=1 prints each chosen plan to stderr.
 #include <hip/hip_runtime.h>
 
@@ -334,6 +335,23 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
     a.stride_a = stride_a;
     a.stride_b = stride_b;
     a.stride_c = stride_c;
+    // Very shallow bf16 products with at least one 32-row tile per CU take the
+    // streaming kernel (B in registers, A streamed once through LDS by producer
+    // waves; measured, bf16 out: 100352x256x128 24.8 us against 35.2 for the
+    // 128x128 tiles, 100352x128x64 14.6 against 19.0, 200704x64x32 19.4
+    // against 30.9, 8192x256x128 7.5 against 8.3); ISAM_GEMM_CONFIG stream=0 /
+    // stream=1 switch it off / force it where it fits.
+    {
+        const char* env = getenv("ISAM_GEMM_CONFIG");
+        const bool off = env && strstr(env, "stream=0"), force = env && strstr(env, "stream=1");
+        if (!off && batch == 1 && !p.skinny && !p.small && gemm_stream_fits(a) &&
+            (force || (K <= kStreamMaxK && cdiv(M, 32) >= (int64_t)device_cus()))) {
+            if (log_enabled()) fprintf(stderr, "[isam] %s streaming kernel\n", who);
+            hipError_t e = launch_gemm_stream(a, device_cus(), stream);
+            if (e != hipSuccess) return hip_fail(e, who);
+            return ISAM_OK;
+        }
+    }
     hipError_t e = launch_gemm(a, p, stream);
     if (e != hipSuccess) return hip_fail(e, who);
     return ISAM_OK;

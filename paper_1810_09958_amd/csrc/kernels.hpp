@@ -60,6 +60,10 @@ struct GemmPlan {
 constexpr int64_t kSmallMaxTiles = 64;
 constexpr int64_t kSmallMaxK = 1024;
 bool gemm_small_fits(int64_t M, int64_t N, int64_t K);
+// Very shallow bf16 products (K <= 256, N <= 256, NN): B in registers, A streamed.
+bool gemm_stream_fits(const GemmArgs& a);
+constexpr int64_t kStreamMaxK = 256;  // planner: deepest K routed to it by default
+hipError_t launch_gemm_stream(const GemmArgs& a, int cus, hipStream_t s);
 hipError_t launch_gemm_small(const GemmArgs& a, hipStream_t s);
 int64_t skinny_k_slice(int ab_type);
 int skinny_rows_per_wg(int ab_type);

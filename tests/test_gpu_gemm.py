@@ -236,3 +236,29 @@ def test_dma_128_tile_copy_modes(K, tb):
     ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), Bm, len(rows), N, K)
     got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
     assert norm_err(got, ref, S) <= TOL_BF16
+
+
+# Very shallow bf16 products (K <= 256, N <= 256 with N % 4 == 0, A and B not transposed): the
+# streaming kernel (B in registers, A through an LDS ring).  Forced on small shapes with
+# stream=1: ragged last 32-row tile, K not a multiple of the 16-deep MFMA step, N not a multiple
+# of a wave's 32 columns, padded leading dimensions, fp32 and bf16 output, accumulate; then
+# chosen by the planner on its own for a shape with enough row tiles, against the tile path.
+@pytest.mark.parametrize("ct", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(33, 8, 8), (100, 40, 72), (257, 256, 128), (64, 100, 200),
+                                   (95, 256, 256), (1, 4, 64), (300, 12, 24)])
+def test_stream_kernel_forced(ct, shape, monkeypatch):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "stream=1")
+    M, N, K = shape
+    _run_case(M, N, K, "bf16", ct, seed=M + N + K)
+    _run_case(M, N, K, "bf16", ct, accumulate=True, seed=M + N + K + 1)
+    _run_case(M, N, K, "bf16", ct, seed=M + N + K + 2, pad_ld=8)
+
+
+@pytest.mark.parametrize("shape", [(32768, 64, 64), (40001, 256, 128), (33000, 200, 256)])
+def test_stream_kernel_planned(shape, monkeypatch):
+    M, N, K = shape
+    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    e_stream = _run_case(M, N, K, "bf16", "f32", seed=M)
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "stream=0")
+    e_tile = _run_case(M, N, K, "bf16", "f32", seed=M)
+    assert e_stream <= TOL_BF16 and e_tile <= TOL_BF16
