@@ -417,11 +417,7 @@ hipError_t launch_depthwise(const DwArgs& a, hipStream_t s) {
         if (lds <= 64 * 1024) {
             const int64_t nseg = (a.Ho + RS - 1) / RS;
             const dim3 grid((unsigned)(a.batch * nseg * nstrip)), block(kDwLdsThreads);
-            const void* fn;
-            if (a.in_type == kBF16) fn = a.y_type == kBF16 ? (const void*)dw3x3_lds_kernel<bf16_t, bf16_t> : (const void*)dw3x3_lds_kernel<bf16_t, float>;
-            else fn = a.y_type == kBF16 ? (const void*)dw3x3_lds_kernel<float, bf16_t> : (const void*)dw3x3_lds_kernel<float, float>;
-            hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) return e;
+            // at most 64 KB of dynamic LDS: within the default limit, no attribute needed
             if (a.in_type == kBF16) {
                 if (a.y_type == kBF16) hipLaunchKernelGGL((dw3x3_lds_kernel<bf16_t, bf16_t>), grid, block, lds, s, a, RS, SW);
                 else hipLaunchKernelGGL((dw3x3_lds_kernel<bf16_t, float>), grid, block, lds, s, a, RS, SW);
