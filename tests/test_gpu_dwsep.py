@@ -61,7 +61,7 @@ def test_one_pixel_image():
 @pytest.mark.parametrize("dt,ot", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16")])
 @pytest.mark.parametrize("shape", [(2, 9, 11, 16, 24), (3, 17, 5, 64, 40), (1, 19, 57, 128, 16),
                                    (2, 6, 7, 8, 8), (1, 1, 1, 8, 8), (1, 10, 3, 1024, 8),
-                                   (1, 5, 4, 4096, 8)])
+                                   (1, 5, 4, 4096, 8), (2, 3, 1000, 8, 4), (1, 23, 300, 32, 8)])
 @pytest.mark.parametrize("rs", ["default", "8", "3", "0"])
 def test_unfused_depthwise_kernel(dt, ot, shape, rs, monkeypatch):
     monkeypatch.setenv("ISAM_DWSEP_FUSED", "0")
