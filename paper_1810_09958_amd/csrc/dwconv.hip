@@ -279,7 +279,11 @@ __global__ __launch_bounds__(kDwLdsThreads) void dw3x3_lds_kernel(DwArgs a, int 
     const int CV = (int)(a.C / E);
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int64_t nstrip = (a.Wo + SW - 1) / SW, nseg = (a.Ho + RS - 1) / RS;
+    // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
+    // contiguous range of blocks, so blocks that share halo rows and columns
+    // run on one L2 at about the same time.
     int64_t u = blockIdx.x;
+    if (gridDim.x % 8 == 0) u = (u % 8) * (gridDim.x / 8) + u / 8;
     const int64_t strip = u % nstrip;
     u /= nstrip;
     const int64_t seg = u % nseg;
