@@ -266,8 +266,10 @@ def main():
         sets = n_sets(2 * (3 * 32 * 56 * 56 * 128 + 100352 * 256))
         Xs = [X0] + [X0.clone() for _ in range(sets - 1)]
         ys = [torch.empty((32, 56, 56, 256), device=dev, dtype=torch.bfloat16) for _ in range(sets)]
-        wsu = [torch.empty(isam.dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, 1, 1),
-                           device=dev, dtype=torch.uint8) for _ in range(sets)]
+        os.environ["ISAM_DWSEP_FUSED"] = "0"   # size of the unfused path: Y in the workspace
+        wsu_bytes = isam.dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, 1, 1)
+        del os.environ["ISAM_DWSEP_FUSED"]
+        wsu = [torch.empty(wsu_bytes, device=dev, dtype=torch.uint8) for _ in range(sets)]
         add_rotated("dwsep_32x56x56x128_256_bf16_out_bf16_unfused",
                     lambda i, Xs=Xs, Dw=Dw, P=P, ys=ys, wsu=wsu: (lambda: isam.dwsep_conv(Xs[i], Dw, P, out=ys[i], workspace=wsu[i])),
                     sets, {"kind": "dwsep", "flop": 2.0 * 100352 * (9 * 128 + 128 * 256),

@@ -92,6 +92,35 @@ int device_cus() {
     return cache[dev];
 }
 
+// Largest LDS allocation of one workgroup on the current device, cached;
+// 160 KiB (gfx950) when no device is visible.
+int device_lds_max() {
+    static std::mutex mu;
+    static int cache[64];
+    static bool have[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+        (void)hipGetLastError();
+        return 160 * 1024;
+    }
+    std::unique_lock<std::mutex> lk(mu, std::defer_lock);
+    try {
+        lk.lock();
+    } catch (...) {
+        return 160 * 1024;
+    }
+    if (!have[dev]) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || v <= 0) {
+            (void)hipGetLastError();
+            v = 160 * 1024;
+        }
+        cache[dev] = v;
+        have[dev] = true;
+    }
+    return cache[dev];
+}
+
 // ---------------------------------------------------------------------------
 // GEMM plan
 // ---------------------------------------------------------------------------
@@ -306,6 +335,16 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         p.k_per_split = K;
         p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     }
+    if (p.k_splits > 1) {
+        // The split-K partial sums must not land on an operand.
+        const int64_t es = (int64_t)dsize(ab_type);
+        const size_t a_b = (size_t)((trans_a ? (K - 1) * lda + M : (M - 1) * lda + K) * es);
+        const size_t b_b = (size_t)((trans_b ? (N - 1) * ldb + K : (K - 1) * ldb + N) * es);
+        const size_t c_b = (size_t)((M - 1) * ldc + N) * dsize(c_type);
+        const size_t w_b = gemm_ws_bytes(p, M, N);
+        if (overlaps(workspace, w_b, A, a_b) || overlaps(workspace, w_b, B, b_b) || overlaps(workspace, w_b, C, c_b))
+            return fail(ISAM_ERR_INVALID_ARG, "%s: workspace overlaps A, B or C", who);
+    }
     if (!p.vec) {
         // The element-wise loader is instantiated for the small tiles only.
         if (p.tile != kTile64x64 && p.tile != kTile128x32) p.tile = kTile64x64;
@@ -403,14 +442,56 @@ static size_t dwsep_ws(int64_t batch, int64_t Ho, int64_t Wo, int64_t C_in, int6
     return y + gemm_ws_bytes(p, M, C_out);
 }
 
+// Which separable-convolution path runs: 1 = fused bf16 kernel, 2 = fused
+// fp32 kernel (both keep the depthwise result on chip and need no
+// workspace), 0 = depthwise kernel into the workspace, then the pointwise
+// GEMM.  The fused kernels need 16-byte aligned x, dw_filter, pw_weight and
+// y; ISAM_DWSEP_FUSED=0 turns them off.
+static int dwsep_path(const DwArgs& d, int64_t C_out, int out_type, const void* pw, const void* y) {
+    const char* env = getenv("ISAM_DWSEP_FUSED");
+    if (env && env[0] == '0') return 0;
+    if (((uintptr_t)y & 15) || ((uintptr_t)pw & 15)) return 0;
+    const int lds_max = device_lds_max();
+    if (dwsep_fused_rows(d, C_out, lds_max) > 0) return 1;
+    if (out_type == ISAM_F32 && dwsep_fused_f32_ok(d, C_out, lds_max)) return 2;
+    return 0;
+}
+
+static DwArgs dw_args(int64_t batch, int64_t H, int64_t W, int64_t C_in, int64_t depth_mult, int64_t kh,
+                      int64_t kw, int64_t stride, int64_t pad, int64_t Ho, int64_t Wo, int in_type,
+                      const void* x, const void* dw_filter, void* Y) {
+    DwArgs d{};
+    d.x = x;
+    d.w = dw_filter;
+    d.y = Y;
+    d.batch = batch;
+    d.H = H;
+    d.W = W;
+    d.C = C_in;
+    d.cm = depth_mult;
+    d.kh = kh;
+    d.kw = kw;
+    d.stride = stride;
+    d.pad = pad;
+    d.Ho = Ho;
+    d.Wo = Wo;
+    d.in_type = in_type;
+    d.y_type = in_type;
+    return d;
+}
+
 size_t isam_dwsep_conv_workspace_size(int64_t batch, int64_t H, int64_t W, int64_t C_in,
                                       int64_t depth_mult, int64_t kh, int64_t kw, int64_t stride,
                                       int64_t pad, int64_t C_out, int in_type, int out_type) {
-    (void)out_type;
     int64_t Ho, Wo;
     if (batch <= 0 || C_in <= 0 || depth_mult <= 0 || C_out <= 0 || kh <= 0 || kw <= 0 || pad < 0 ||
-        !valid_dtype(in_type) || !dw_out_dims(H, W, kh, kw, stride, pad, &Ho, &Wo))
+        !valid_dtype(in_type) || !valid_dtype(out_type) || !dw_out_dims(H, W, kh, kw, stride, pad, &Ho, &Wo))
         return 0;
+    // The fused paths need no workspace (the answer assumes 16-byte aligned
+    // tensors, as every torch allocation is).
+    const DwArgs d = dw_args(batch, H, W, C_in, depth_mult, kh, kw, stride, pad, Ho, Wo, in_type, nullptr,
+                             nullptr, nullptr);
+    if (dwsep_path(d, C_out, out_type, nullptr, nullptr)) return 0;
     return dwsep_ws(batch, Ho, Wo, C_in, depth_mult, C_out, in_type);
 }
 
@@ -443,53 +524,30 @@ isam_status_t isam_dwsep_conv(int64_t batch, int64_t H, int64_t W, int64_t C_in,
         overlaps(y, yb, dw_filter, (size_t)(kh * kw * Cm) * es) ||
         overlaps(y, yb, pw_weight, (size_t)(Cm * C_out) * es))
         return fail(ISAM_ERR_INVALID_ARG, "%s: y overlaps an input", who);
-    const size_t need = dwsep_ws(batch, Ho, Wo, C_in, depth_mult, C_out, in_type);
-    const size_t y_bytes = align256((size_t)Y_el * es);
-    if (!workspace || workspace_bytes < y_bytes)
-        return fail(ISAM_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu required", who, workspace_bytes, need);
-    if (overlaps(workspace, workspace_bytes, y, yb) || overlaps(workspace, workspace_bytes, x, (size_t)x_el * es))
-        return fail(ISAM_ERR_INVALID_ARG, "%s: workspace overlaps a tensor", who);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    DwArgs d{};
-    d.x = x;
-    d.w = dw_filter;
-    d.y = workspace;
-    d.batch = batch;
-    d.H = H;
-    d.W = W;
-    d.C = C_in;
-    d.cm = depth_mult;
-    d.kh = kh;
-    d.kw = kw;
-    d.stride = stride;
-    d.pad = pad;
-    d.Ho = Ho;
-    d.Wo = Wo;
-    d.in_type = in_type;
-    d.y_type = in_type;
+    const size_t y_bytes = align256((size_t)Y_el * es);
+    DwArgs d = dw_args(batch, H, W, C_in, depth_mult, kh, kw, stride, pad, Ho, Wo, in_type, x, dw_filter, workspace);
     // Fused paths: the depthwise result stays in LDS and feeds the MFMA
     // product directly (bf16 input, or fp32 input and output; 3x3 stride 1
-    // pad 1 shapes that fit).
-    const bool fused_off = getenv("ISAM_DWSEP_FUSED") && getenv("ISAM_DWSEP_FUSED")[0] == '0';
-    if (!fused_off && !((uintptr_t)y & 15) && !((uintptr_t)pw_weight & 15)) {
-        int dev = 0, lds_max = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) {
-            const int R = dwsep_fused_rows(d, C_out, lds_max);
-            if (R > 0) {
-                if (log_enabled()) fprintf(stderr, "[isam] dwsep fused R=%d\n", R);
-                hipError_t e = launch_dwsep_fused(d, pw_weight, y, C_out, out_type, lds_max, device_cus(), s);
-                return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
-            }
-            if (out_type == ISAM_F32 && dwsep_fused_f32_ok(d, C_out, lds_max)) {
-                if (log_enabled()) fprintf(stderr, "[isam] dwsep fused fp32\n");
-                hipError_t e = launch_dwsep_fused_f32(d, pw_weight, y, C_out, device_cus(), s);
-                return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
-            }
-        } else {
-            (void)hipGetLastError();
-        }
+    // pad 1 shapes that fit).  No workspace is touched.
+    const int path = dwsep_path(d, C_out, out_type, pw_weight, y);
+    if (path == 1) {
+        if (log_enabled()) fprintf(stderr, "[isam] dwsep fused bf16\n");
+        hipError_t e = launch_dwsep_fused(d, pw_weight, y, C_out, out_type, device_lds_max(), device_cus(), s);
+        return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
     }
+    if (path == 2) {
+        if (log_enabled()) fprintf(stderr, "[isam] dwsep fused fp32\n");
+        hipError_t e = launch_dwsep_fused_f32(d, pw_weight, y, C_out, device_cus(), s);
+        return e == hipSuccess ? ISAM_OK : hip_fail(e, who);
+    }
+    const size_t need = dwsep_ws(batch, Ho, Wo, C_in, depth_mult, C_out, in_type);
+    if (!workspace || workspace_bytes < y_bytes)
+        return fail(ISAM_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu required", who, workspace_bytes, need);
+    if (overlaps(workspace, workspace_bytes, y, yb) || overlaps(workspace, workspace_bytes, x, (size_t)x_el * es) ||
+        overlaps(workspace, workspace_bytes, dw_filter, (size_t)(kh * kw * Cm) * es) ||
+        overlaps(workspace, workspace_bytes, pw_weight, (size_t)(Cm * C_out) * es))
+        return fail(ISAM_ERR_INVALID_ARG, "%s: workspace overlaps a tensor", who);
     hipError_t e = launch_depthwise(d, s);
     if (e != hipSuccess) return hip_fail(e, who);
     char* gws = static_cast<char*>(workspace) + y_bytes;
@@ -503,7 +561,8 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
     (void)input_size;
     if (T < 0 || batch <= 0 || hidden_size <= 0 || !valid_dtype(w_type)) return 0;
     const size_t gx = align256((size_t)T * (size_t)batch * 3 * (size_t)hidden_size * sizeof(float));
-    const size_t hb = align256(((size_t)T + 1) * (size_t)batch * (size_t)hidden_size * dsize(w_type));
+    const size_t hb = align256(((size_t)T + 1) * (size_t)gru_slot_elems(batch, hidden_size, (int64_t)dsize(w_type)) *
+                               dsize(w_type));
     const size_t hs = align256(2 * (size_t)batch * (size_t)hidden_size * sizeof(float));
     return gx + hb + kGruSyncBytes + hs;
 }
@@ -541,7 +600,7 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     const size_t xb = (size_t)T * batch * I * es, wb = (size_t)3 * H * I * es, ub = (size_t)3 * H * H * es;
     if ((int64_t)xb > kMaxExtent || (int64_t)wb > kMaxExtent || (int64_t)ub > kMaxExtent ||
         (int64_t)((size_t)T * batch * 3 * H * sizeof(float)) > kMaxExtent ||
-        (int64_t)(((size_t)T + 1) * batch * H * es) > kMaxExtent)
+        (int64_t)(((size_t)T + 1) * (size_t)gru_slot_elems(batch, H, (int64_t)es) * es) > kMaxExtent)
         return fail(ISAM_ERR_UNSUPPORTED, "%s: a tensor spans more than 2^31 bytes", who);
     const void* ins[6] = {x, W, U, h0, bias, bias_hn};
     const size_t inb[6] = {xb, wb, ub, state, (size_t)3 * H * sizeof(float), (size_t)H * sizeof(float)};
@@ -635,7 +694,8 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     float* gx = reinterpret_cast<float*>(ws);
     const size_t gx_b = align256((size_t)T * batch * 3 * H * sizeof(float));
     void* hbuf = ws + gx_b;
-    const size_t hb_b = align256(((size_t)T + 1) * batch * H * es);
+    const int64_t slot = gru_slot_elems(batch, H, (int64_t)es);
+    const size_t hb_b = align256(((size_t)T + 1) * (size_t)slot * es);
     unsigned* sync = reinterpret_cast<unsigned*>(ws + gx_b + hb_b);
     float* hstate = reinterpret_cast<float*>(ws + gx_b + hb_b + kGruSyncBytes);
 
@@ -657,7 +717,15 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     g.h_seq = h_seq;
     g.h_T = h_T;
     g.hbuf = hbuf;
+    g.slot = slot;
     g.sync = sync;
+    g.timeout_ticks = kGruTimeoutTicks;
+    // Test hook: a barrier target one arrival beyond the grid is never met, so
+    // every wait ends at a 100 us bound and the outputs come back as NaN.
+    if (const char* st_env = getenv("ISAM_GRU_TEST_STALL"); st_env && st_env[0] == '1') {
+        g.stall = 1;
+        g.timeout_ticks = 10000;
+    }
     g.units_per_wg = J;
     g.batch_per_wg = BB;
     g.n_wg = n_wg;

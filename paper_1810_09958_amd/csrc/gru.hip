@@ -24,6 +24,7 @@
 //
 // All workgroups must be co-resident (cooperative launch); every barrier
 // wait is bounded and raises an error flag instead of spinning forever.
+#include <algorithm>
 #include <cstdlib>
 #include <mutex>
 #include <vector>
@@ -38,8 +39,6 @@ constexpr int kWaves = 4;
 constexpr int kSyncWords = kGruSyncBytes / 4;
 constexpr int kRedLd = 20;  // floats per row of the cross-wave sums (20: the 4 row groups written by
                             // one store instruction fall on different banks)
-// Upper bound on one barrier wait, in ticks of the 100 MHz constant clock.
-constexpr uint64_t kBarrierTimeoutTicks = 200000000ull;  // 2 s
 
 __host__ __device__ __forceinline__ int gru_rows(int J) { return ((3 * J + 15) / 16) * 16; }
 // U rows in LDS: a multiple of 256 bytes, so the chunk swizzle below stays
@@ -55,13 +54,21 @@ __device__ __forceinline__ int u_chunk(int r, int c) { return c ^ (2 * (r & 7));
 // h_{t-1} travels between workgroups (and XCDs, whose L2 caches are not
 // coherent with each other) through a ring of T+1 slots, one per step: h_t is
 // written to slot t+1 with device-scope (sc1) stores, which write through to
-// the device coherence point, and __syncthreads() waits for each thread's
-// stores to complete (vmcnt(0)) before the workgroup signals arrival.  After
-// the barrier, slot t+1 is read with ordinary (L2-cached) loads: no
-// workgroup has touched that slot earlier in the launch, so no L2 can hold a
-// stale copy of it, and the first reader on each XCD brings it into that
-// XCD's L2 for the other 31 workgroups there -- each step's state leaves
-// memory once per XCD instead of once per workgroup.
+// the device coherence point.  A store counts as complete (vmcnt) only once
+// that write is acknowledged, and s_barrier does not wait for the stores of
+// the other waves, so every wave waits for vmcnt(0) itself before the
+// workgroup barrier that precedes the arrival atomic: no workgroup signals
+// arrival while any of its h stores is still in flight.
+//
+// After the barrier, slot t+1 is read with ordinary (L2-cached) loads.  No
+// workgroup reads any line of slot t+1 before barrier t: slots are padded to
+// whole 256-byte blocks, so the lines of slot t (read during step t) never hold
+// bytes of slot t+1, and a line of slot t+1 enters an XCD's L2 only through
+// the write-through stores of that XCD's own workgroups, which carry no stale
+// bytes.  The first reader on each XCD then brings the slot into that XCD's L2
+// for the other workgroups there -- each step's state leaves memory once per
+// XCD instead of once per workgroup.  The kernel boundary (whose acquire
+// invalidates the caches) separates launches that reuse the ring.
 //
 // The barrier is two-level to limit serialised atomics on one address:
 // workgroups arrive on a counter of their group (a.barrier_group members:
@@ -69,7 +76,8 @@ __device__ __forceinline__ int u_chunk(int r, int c) { return c ^ (2 * (r & 7));
 // of a group bumps the domain counter, and every workgroup polls the domain
 // counter.  All counters are monotonic over the steps of one launch (zeroed
 // by the init kernel).  Each wait is bounded in time; a timeout sets the
-// sticky error word, after which every wait returns at once.
+// sticky error word, after which every wait returns at once, and the check
+// kernel launched behind the recurrence then fills h_seq and h_T with NaN.
 
 constexpr int kSyncError = 0;           // word offsets; counters sit 64 bytes apart
 constexpr int kSyncDomainWords = 512;   // per batch group: global counter + group counters
@@ -77,10 +85,13 @@ constexpr int kCpolDevice = 16;         // sc1: device-scope coherence
 
 // Workgroups of one batch group form a barrier domain: batch groups are
 // independent sequences, so they never wait for each other.
-__device__ __forceinline__ void grid_barrier(unsigned* sync, int64_t step, int domain, int member, int n_members,
-                                             int kGroup) {
+__device__ __forceinline__ void grid_barrier(const GruArgs& a, int64_t step, int domain, int member, int n_members) {
+    // Every wave's h stores must be complete before the workgroup can arrive.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (threadIdx.x == 0) {
+        unsigned* sync = a.sync;
+        const int kGroup = a.barrier_group;
         unsigned* dom = sync + kSyncDomainWords * (1 + domain);
         const int g = member / kGroup;
         const int n_groups = (n_members + kGroup - 1) / kGroup;
@@ -89,12 +100,12 @@ __device__ __forceinline__ void grid_barrier(unsigned* sync, int64_t step, int d
                                                     __HIP_MEMORY_SCOPE_AGENT);
         if (old + 1 == (unsigned)(step + 1) * gsize)
             __hip_atomic_fetch_add(dom, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned target = (unsigned)(step + 1) * (unsigned)n_groups;
+        const unsigned target = (unsigned)(step + 1) * (unsigned)n_groups + (unsigned)a.stall;
         const uint64_t start = wall_clock64();
         while (__hip_atomic_load(dom, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target &&
                __hip_atomic_load(sync + kSyncError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
             __builtin_amdgcn_s_sleep(2);
-            if (wall_clock64() - start > kBarrierTimeoutTicks) {
+            if (wall_clock64() - start > a.timeout_ticks) {
                 __hip_atomic_fetch_or(sync + kSyncError, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 break;
             }
@@ -193,9 +204,9 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
     fetch_gx(0);
 
     constexpr int kBatch = 8;  // h chunks requested together per lane
-    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)((a.T + 1) * B * H * (int64_t)sizeof(T)));
+    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)((a.T + 1) * a.slot * (int64_t)sizeof(T)));
     for (int64_t t = 0; t < a.T; ++t) {
-        const int64_t hcur_off = t * B * H;  // element offset of h_{t-1}: ring slot t
+        const int64_t hcur_off = t * a.slot;  // element offset of h_{t-1}: ring slot t
         f32x4_t acc[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) acc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -258,14 +269,14 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
             const float h = (1.0f - z) * n + z * h_prev;
             h_prev = h;
             if (a.h_seq) a.h_seq[(t * B + bb) * H + j] = h;
-            const int64_t hn = (t + 1) * B * H + bb * H + j;  // ring slot t+1
+            const int64_t hn = (t + 1) * a.slot + bb * H + j;  // ring slot t+1
             if constexpr (sizeof(T) == 2)
                 __builtin_amdgcn_raw_buffer_store_b16((unsigned short)f32_to_bf16(h), rs_h, (int)(hn * 2), 0, kCpolDevice);
             else
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(h), rs_h, (int)(hn * 4), 0, kCpolDevice);
         }
         fetch_gx(t + 1);
-        if (t + 1 < a.T) grid_barrier(a.sync, t, bg, ug, n_ug, a.barrier_group);
+        if (t + 1 < a.T) grid_barrier(a, t, bg, ug, n_ug);
     }
     if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
 }
@@ -341,9 +352,9 @@ __global__ __launch_bounds__(64 * kWaves) void gru_step_kernel(GruArgs a, float*
         u_row[m] = lr < 3 * J ? ((lr / J) * H + j0 + lr % J) : -1;
     }
     constexpr int kBatch = 8;  // K groups requested together per lane
-    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)((a.T + 1) * B * H * (int64_t)sizeof(T)));
+    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)((a.T + 1) * a.slot * (int64_t)sizeof(T)));
     const __amdgpu_buffer_rsrc_t rs_u = make_rsrc(a.U, (uint32_t)(3 * H * H * (int64_t)sizeof(T)));
-    const int64_t hcur_off = t * B * H;  // ring slot t holds h_{t-1}
+    const int64_t hcur_off = t * a.slot;  // ring slot t holds h_{t-1}
     f32x4_t acc[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) acc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -398,10 +409,22 @@ __global__ __launch_bounds__(64 * kWaves) void gru_step_kernel(GruArgs a, float*
     const float h = (1.0f - z) * n + z * h_prev;
     if (a.h_seq) a.h_seq[(t * B + bb) * H + j] = h;
     hstate[((t + 1) & 1) * B * H + bb * H + j] = h;
-    const int64_t hn = (t + 1) * B * H + bb * H + j;  // ring slot t+1
+    const int64_t hn = (t + 1) * a.slot + bb * H + j;  // ring slot t+1
     if constexpr (sizeof(T) == 2) static_cast<uint16_t*>(a.hbuf)[hn] = (uint16_t)f32_to_bf16(h);
     else static_cast<float*>(a.hbuf)[hn] = h;
     if (t + 1 == a.T && a.h_T) a.h_T[bb * H + j] = h;
+}
+
+// Finish check behind the persistent recurrence: if any barrier wait ran into
+// its bound (sticky error word set), the results are not trustworthy, so every
+// output element is overwritten with NaN.  The kernel boundary orders this
+// after every store of the recurrence.
+__global__ void gru_error_fill_kernel(const unsigned* sync, float* h_seq, int64_t n_seq, float* h_T, int64_t n_T) {
+    if (__hip_atomic_load(sync + kSyncError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) return;
+    const float nan = __uint_as_float(0x7fc00000u);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_seq; i += stride) h_seq[i] = nan;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_T; i += stride) h_T[i] = nan;
 }
 
 __global__ void copy_state_kernel(const float* h0, float* hT, int64_t n) {
@@ -431,6 +454,14 @@ hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStre
     return hipGetLastError();
 }
 
+hipError_t launch_gru_error_fill(const GruArgs& a, hipStream_t s) {
+    const int64_t n_seq = a.h_seq ? a.T * a.batch * a.H : 0, n_T = a.h_T ? a.batch * a.H : 0;
+    int blocks = (int)((std::max(n_seq, n_T) + 255) / 256);
+    blocks = blocks > 1024 ? 1024 : (blocks < 1 ? 1 : blocks);
+    hipLaunchKernelGGL(gru_error_fill_kernel, dim3(blocks), dim3(256), 0, s, a.sync, a.h_seq, n_seq, a.h_T, n_T);
+    return hipGetLastError();
+}
+
 size_t gru_lds_bytes(int w_type, int64_t H, int J) {
     const int RT = ((3 * J + 15) / 16) * 16;
     const int64_t es = w_type == kBF16 ? 2 : 4;
@@ -452,7 +483,9 @@ hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     GruArgs args = a;
     void* params[] = {&args};
-    return hipLaunchCooperativeKernel(fn, dim3(a.n_wg), dim3(64 * kWaves), params, (unsigned)lds, s);
+    e = hipLaunchCooperativeKernel(fn, dim3(a.n_wg), dim3(64 * kWaves), params, (unsigned)lds, s);
+    if (e != hipSuccess) return e;
+    return launch_gru_error_fill(a, s);
 }
 
 // Graph of the stepwise recurrence for one call signature: the state init

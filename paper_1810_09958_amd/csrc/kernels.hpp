@@ -105,8 +105,13 @@ struct GruArgs {
     const float* bias_hn;   // [H] or null
     float* h_seq;           // [T][batch][H] or null
     float* h_T;             // [batch][H] or null
-    void* hbuf;             // [T+1][batch][H] in w_type: ring of per-step MFMA copies of h
+    void* hbuf;             // [T+1] slots of `slot` elements in w_type: ring of per-step MFMA
+                            // copies of h, slot t holding h_{t-1} as [batch][H]
+    int64_t slot;           // elements per ring slot: batch*H rounded up to a multiple of 256 bytes
     unsigned* sync;         // barrier counters and error word (kGruSyncBytes, zeroed by the launch)
+    uint64_t timeout_ticks; // bound on one barrier wait, in ticks of the 100 MHz constant clock
+    int stall;              // 1: barrier targets one arrival beyond the grid (never met), so every
+                            // wait runs into the bound; exercises the timeout path
     int units_per_wg;       // J
     int batch_per_wg;       // BB
     int n_wg;
@@ -120,7 +125,14 @@ size_t gru_lds_bytes(int w_type, int64_t H, int J);
 // Resident workgroups of the recurrent kernel per compute unit at this LDS size.
 int gru_blocks_per_cu(int w_type, size_t lds);
 constexpr int kGruSyncBytes = 32768;  // barrier area at the end of the GRU workspace
+// Ring slot stride in elements: whole 256-byte blocks, so no cache line holds
+// parts of two slots.
+inline int64_t gru_slot_elems(int64_t batch, int64_t H, int64_t es) { return (batch * H * es + 255) / 256 * 256 / es; }
 hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s);
+// NaN into h_seq and h_T if the recurrence's sticky error word is set.
+hipError_t launch_gru_error_fill(const GruArgs& a, hipStream_t s);
+// Bound on one barrier wait of the persistent recurrence (2 s at 100 MHz).
+constexpr uint64_t kGruTimeoutTicks = 200000000ull;
 // Stepwise recurrence (state init + one kernel per step, replayed from a
 // cached graph); hstate is a [2][batch][H] fp32 workspace.
 hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s);

@@ -78,6 +78,18 @@ def test_gemm_validation(L, kw, code):
     assert L.isam_last_error() != b""
 
 
+def test_gemm_splitk_workspace_must_not_overlap_operands(L):
+    # 512 x 32 x 8192 fp32 is planned with split-K partial sums in the workspace: a workspace
+    # that overlaps C, A or B is rejected before anything is launched.
+    M, N, K = 512, 32, 8192
+    need = L.isam_gemm_workspace_size(0, 0, M, N, K, F32, F32)
+    assert need > 0
+    A, B, C = (ctypes.c_void_p(v) for v in (0x100000000, 0x200000000, 0x300000000))
+    for ws in (C, A, B, ctypes.c_void_p(0x300000000 - need + 4)):
+        assert gemm(L, M=M, N=N, K=K, A=A, lda=K, B=B, ldb=N, C=C, ldc=N, ws=ws, wsb=need) == INVALID
+        assert b"workspace overlaps" in L.isam_last_error()
+
+
 def test_gemm_empty_is_noop(L):
     assert gemm(L, M=0, A=None, B=None, C=None) == OK
     assert gemm(L, N=0, A=None, B=None, C=None) == OK
@@ -114,8 +126,15 @@ def test_dwsep_validation(L, kw, code):
 
 
 def test_dwsep_workspace_query(L):
-    n = L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, BF16, F32)
-    assert n >= 32 * 56 * 56 * 128 * 2
+    # The fused kernels (3x3, stride 1, pad 1 at these channel counts) keep the depthwise
+    # result on chip and need no workspace; other shapes hold Y in the workspace.
+    assert L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, BF16, F32) == 0
+    assert L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, BF16, BF16) == 0
+    assert L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, F32, F32) == 0
+    n = L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 2, 1, 256, BF16, F32)
+    assert n >= 32 * 28 * 28 * 128 * 2
+    n = L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 1, 1, 256, F32, BF16)
+    assert n >= 32 * 56 * 56 * 128 * 4
     assert L.isam_dwsep_conv_workspace_size(32, 56, 56, 128, 1, 3, 3, 0, 1, 256, BF16, F32) == 0
     assert dw(L, batch=0, x=None, y=None) == OK
 

@@ -73,21 +73,33 @@ def test_unfused_depthwise_kernel(dt, ot, shape, rs, monkeypatch):
     _case(b, H, W, C, Co, dt=dt, ot=ot, seed=H + W + C)
 
 
-@pytest.mark.parametrize("variant", ["f32", "bf16", "bf16_out_bf16"])
-def test_config_full_size_sampled_images(variant):
-    d = workloads.dwsep()
-    if variant == "f32":
-        X, D, P = d["X"], d["D"], d["P"]
-    else:
-        X, D, P = d["X_bf16"], d["D_bf16"], d["P_bf16"]
+_FULL = {}
+
+
+def _full_ref(dt):
+    """Oracle output of the whole 32-image separable-convolution workload, once per dtype."""
+    if dt not in _FULL:
+        d = workloads.dwsep()
+        X, D, P = (d["X"], d["D"], d["P"]) if dt == "f32" else (d["X_bf16"], d["D_bf16"], d["P_bf16"])
+        Z, S = oracle.dwsep(X, D, P)
+        _FULL[dt] = (X, D, P, Z, S)
+    return _FULL[dt]
+
+
+def _check_full(variant):
+    X, D, P, Z, S = _full_ref("f32" if variant == "f32" else "bf16")
     ot = torch.bfloat16 if variant == "bf16_out_bf16" else torch.float32
     y = isam.dwsep_conv(to_gpu(X), to_gpu(D), to_gpu(P), out_dtype=ot)
     torch.cuda.synchronize()
-    imgs = [0, 13, 31]   # images are independent: the oracle runs on a subset of the batch
-    Z, S = oracle.dwsep(np.ascontiguousarray(X[imgs]), D, P)
-    got = to_host_f64(y[torch.as_tensor(imgs, device="cuda")])
     tol = TOL_F32 if variant == "f32" else TOL_BF16
-    assert norm_err(got, Z, S) <= tol
+    err = norm_err(to_host_f64(y), Z, S)
+    assert err <= tol, f"{variant}: {err:.3e}"
+
+
+@pytest.mark.parametrize("variant", ["f32", "bf16", "bf16_out_bf16"])
+def test_config_full_size_all_images(variant):
+    # all 32 images, every output element, through the default (fused) path
+    _check_full(variant)
 
 
 @pytest.mark.parametrize("variant", ["f32", "bf16_out_bf16"])
@@ -95,7 +107,57 @@ def test_config_full_size_unfused(variant, monkeypatch):
     # the full image batch through the standalone depthwise kernel and the pointwise GEMM
     monkeypatch.setenv("ISAM_DWSEP_FUSED", "0")
     monkeypatch.delenv("ISAM_DW_RS", raising=False)
-    test_config_full_size_sampled_images(variant)
+    _check_full(variant)
+
+
+@pytest.mark.parametrize("dt,ot", [("bf16", "f32"), ("bf16", "bf16"), ("f32", "f32")])
+def test_fused_path_needs_no_workspace(dt, ot):
+    # The fused kernels keep the depthwise result on chip: the size query returns 0 and the
+    # call runs with no workspace at all.
+    b, H, W, C, Co = 2, 6, 56, 128, 256
+    it = isam.ISAM_BF16 if dt == "bf16" else isam.ISAM_F32
+    otc = isam.ISAM_BF16 if ot == "bf16" else isam.ISAM_F32
+    assert isam.dwsep_conv_workspace_size(b, H, W, C, 1, 3, 3, 1, 1, Co, it, otc) == 0
+    X = synth.normal(5, 0, (b, H, W, C))
+    D = synth.uniform(5, 1, (3, 3, C, 1), -1 / 3, 1 / 3)
+    P = synth.uniform(5, 2, (C, Co), -1 / 11, 1 / 11)
+    if dt == "bf16":
+        X, D, P = bits(X), bits(D), bits(P)
+    odt = torch.bfloat16 if ot == "bf16" else torch.float32
+    y = torch.empty((b, H, W, Co), device="cuda", dtype=odt)
+    Xg, Dg, Pg = to_gpu(X), to_gpu(D), to_gpu(P)   # held until the kernel has run
+    rc = isam.lib().isam_dwsep_conv(b, H, W, C, 1, 3, 3, 1, 1, Co, it, Xg.data_ptr(), Dg.data_ptr(),
+                                    Pg.data_ptr(), otc, y.data_ptr(), None, 0, isam._stream())
+    assert rc == 0, isam.lib().isam_last_error()
+    torch.cuda.synchronize()
+    Z, S = oracle.dwsep(X, D, P)
+    assert norm_err(to_host_f64(y), Z, S) <= (TOL_F32 if ot == "f32" and dt == "f32" else TOL_BF16)
+
+
+@pytest.mark.parametrize("dt,ot,fused", [("bf16", "f32", "1"), ("bf16", "bf16", "1"), ("f32", "f32", "1"),
+                                         ("bf16", "bf16", "0"), ("f32", "f32", "0")])
+def test_output_guard_bands(dt, ot, fused, monkeypatch):
+    # y placed inside a larger sentinel-filled buffer: the fused bf16 and fp32 kernels and the
+    # unfused pair write nothing outside [b][H][W][C_out].
+    monkeypatch.setenv("ISAM_DWSEP_FUSED", fused)
+    b, H, W, C, Co = 3, 7, 56, 128, 96
+    X = synth.normal(6, 0, (b, H, W, C))
+    D = synth.uniform(6, 1, (3, 3, C, 1), -1 / 3, 1 / 3)
+    P = synth.uniform(6, 2, (C, Co), -1 / 11, 1 / 11)
+    if dt == "bf16":
+        X, D, P = bits(X), bits(D), bits(P)
+    odt = torch.bfloat16 if ot == "bf16" else torch.float32
+    g = 4096
+    n = b * H * W * Co
+    buf = torch.full((n + 2 * g,), -768.0, device="cuda", dtype=odt)
+    y = buf[g: g + n].view(b, H, W, Co)
+    isam.dwsep_conv(to_gpu(X), to_gpu(D), to_gpu(P), out=y)
+    torch.cuda.synchronize()
+    h = buf.float().cpu().numpy()
+    assert np.all(h[:g] == -768.0) and np.all(h[g + n:] == -768.0)
+    Z, S = oracle.dwsep(X, D, P)
+    assert norm_err(h[g: g + n].reshape(b, H, W, Co).astype(np.float64), Z, S) <= \
+        (TOL_F32 if ot == "f32" and dt == "f32" else TOL_BF16)
 
 
 @pytest.mark.parametrize("ot", ["f32", "bf16"])

@@ -141,19 +141,111 @@ def test_config_skinny_full(variant):
     assert err <= (TOL_BF16 if variant == "bf16" else TOL_F32), err
 
 
+_LARGE_REF = {}
+
+
+def _large_ref(which):
+    """Oracle result and normaliser of a whole large bf16 product, computed once per module
+    (about 20 s for 8192^3 on the GPU machine's host cores)."""
+    if which not in _LARGE_REF:
+        _LARGE_REF.clear()   # hold one (2 x 512 MiB for 8192^2) at a time
+        d = workloads.gemm_square_bf16() if which == "square" else workloads.gemm_rect_bf16()
+        A_h, B_h = d["A_bf16"], d["B_bf16"]
+        M, K = A_h.shape
+        N = B_h.shape[1]
+        ref, S = oracle.gemm(A_h, B_h, M, N, K)
+        _LARGE_REF[which] = (A_h, B_h, ref, S)
+    return _LARGE_REF[which]
+
+
 @pytest.mark.parametrize("which", ["square", "rect"])
-@pytest.mark.parametrize("ct", ["bf16", "f32"])
-def test_config_large_bf16_sampled_rows(which, ct):
-    d = workloads.gemm_square_bf16() if which == "square" else workloads.gemm_rect_bf16()
-    A_h, B_h = d["A_bf16"], d["B_bf16"]
-    M, K = A_h.shape
-    N = B_h.shape[1]
-    C = isam.gemm(to_gpu(A_h), to_gpu(B_h), out_dtype=torch.bfloat16 if ct == "bf16" else torch.float32)
+def test_config_large_bf16_every_element(which):
+    # 8192^3 and 8192 x 1024 x 16384 in the launch configuration the benchmark times, fp32 and
+    # bf16 output, every element against the oracle.
+    A_h, B_h, ref, S = _large_ref(which)
+    A, B = to_gpu(A_h), to_gpu(B_h)
+    for out_dtype in (torch.float32, torch.bfloat16):
+        C = isam.gemm(A, B, out_dtype=out_dtype)
+        torch.cuda.synchronize()
+        err = norm_err(to_host_f64(C), ref, S)
+        assert err <= TOL_BF16, f"{which} {out_dtype}: {err:.3e}"
+        del C
+
+
+# Every direct-to-LDS kernel instance, forced on small shapes and checked on every element:
+# 256x256 tiles with 8 waves (the large-GEMM kernel) and with 4, 256x128 with 8 and 4, and
+# 128x128; B K-contiguous (NT) and N-contiguous (NN); K a multiple of the 64-deep tile (copy
+# offsets as base + per-tile delta) and with a ragged last tile; fp32 and bf16 output;
+# unsplit and split into two K slices (partial sums + fixed-order reduction).
+DMA_INSTANCES = [("0", "8"), ("0", "4"), ("1", "8"), ("1", "4"), ("2", "4")]
+
+
+@pytest.mark.parametrize("tile,waves", DMA_INSTANCES)
+@pytest.mark.parametrize("tb", [0, 1])
+@pytest.mark.parametrize("K", [640, 600])
+@pytest.mark.parametrize("splits", [1, 2])
+def test_dma_instances_every_element(tile, waves, tb, K, splits, monkeypatch):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", f"tile={tile},dma=1,dmaw={waves},splits={splits}")
+    for ct in ("f32", "bf16"):
+        _run_case(512, 768, K, "bf16", ct, tb=tb, seed=K + splits + int(tile))
+    _run_case(512, 768, K, "bf16", "f32", tb=tb, accumulate=True, seed=K + 7)
+
+
+def _guarded_gemm(M, N, K, dt, ct, pad_cols, seed, tb=0, env=None, monkeypatch=None):
+    """C written into a [M][N + pad_cols] window of a larger sentinel-filled buffer: checks
+    that nothing outside the M x N block changes and that the block matches the oracle."""
+    if env is not None:
+        monkeypatch.setenv("ISAM_GEMM_CONFIG", env)
+    Am = synth.uniform(seed, 30, (M, K), -1, 1)
+    Bm = synth.uniform(seed, 31, (K, N), -1, 1)
+    B_host = np.ascontiguousarray(Bm.T) if tb else Bm
+    if dt == "bf16":
+        Am, B_host = bits(Am), bits(B_host)
+        Bm = bits(Bm)
+    A, B = to_gpu(Am), to_gpu(B_host)
+    ldc = N + pad_cols
+    g = 4096
+    tdt = torch.bfloat16 if ct == "bf16" else torch.float32
+    sentinel = -12345.0
+    buf = torch.full((M * ldc + 2 * g,), sentinel, device="cuda", dtype=tdt)
+    C = buf[g: g + M * ldc].view(M, ldc)[:, :N]
+    isam.gemm(A, B, C, trans_b=bool(tb))
     torch.cuda.synchronize()
-    rows = workloads.rows_sample(M, 48)
-    ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), B_h, len(rows), N, K)
-    got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
-    assert norm_err(got, ref, S) <= TOL_BF16
+    h = buf.float().cpu().numpy()
+    sv = float(torch.tensor(sentinel, dtype=tdt).float())
+    assert np.all(h[:g] == sv) and np.all(h[g + M * ldc:] == sv), "write before or after C"
+    body = h[g: g + M * ldc].reshape(M, ldc)
+    assert np.all(body[:, N:] == sv), "write into the row padding of C"
+    ref, S = oracle.gemm(Am, Bm, M, N, K)
+    tol = TOL_F32 if (dt == "f32" and ct == "f32") else TOL_BF16
+    assert norm_err(body[:, :N].astype(np.float64), ref, S) <= tol
+
+
+GUARD_CASES = ["dma256", "dma256_split", "dma128", "skinny_rows", "skinny_split", "narrow", "stream",
+               "tile_f32", "small"]
+
+
+@pytest.mark.parametrize("ct", ["f32", "bf16"])
+@pytest.mark.parametrize("case", GUARD_CASES)
+def test_guard_bands_every_kernel(ct, case, monkeypatch):
+    # Each GEMM kernel writes exactly its M x N block: the direct-to-LDS kernels (256x256
+    # whole and split along K, 128x128), the skinny kernels (one pass and split-K), the
+    # narrow dot-product kernel, the streaming kernel, the fp32 tile kernel and the small-
+    # product kernel, with C rows padded (ldc > N).
+    cases = {
+        "dma256": dict(M=520, N=776, K=640, dt="bf16", env="tile=0,dma=1,dmaw=8"),
+        "dma256_split": dict(M=520, N=776, K=640, dt="bf16", env="tile=0,dma=1,dmaw=8,splits=2"),
+        "dma128": dict(M=520, N=776, K=600, dt="bf16", env="tile=2,dma=1"),
+        "skinny_rows": dict(M=4100, N=32, K=1000, dt="bf16", env=None),
+        "skinny_split": dict(M=300, N=24, K=6000, dt="f32", env=None),
+        "narrow": dict(M=1000, N=3, K=2000, dt="bf16", env=None),
+        "stream": dict(M=300, N=72, K=96, dt="bf16", env="stream=1"),
+        "tile_f32": dict(M=300, N=200, K=130, dt="f32", env=None),
+        "small": dict(M=100, N=64, K=520, dt="f32", env=None),
+    }
+    c = cases[case]
+    _guarded_gemm(c["M"], c["N"], c["K"], c["dt"], ct, pad_cols=8, seed=100 + GUARD_CASES.index(case),
+                  env=c["env"], monkeypatch=monkeypatch)
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
