@@ -144,6 +144,25 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
                                        int64_t hidden_size, int w_type);
 
 /*
+ * isam_gru_forward without a workspace argument and without any allocation,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Arguments,
+ * results and errors are those of isam_gru_forward (bit for bit the same
+ * outputs); the workspace is instead a static 64 MiB device array of the
+ * library (one per device, held until the process ends), so sizes whose
+ * isam_gru_forward_workspace_size exceeds 64 MiB are rejected with
+ * ISAM_ERR_WORKSPACE (T = 64, batch 32, hidden 1024 needs about 28 MiB).  The
+ * stepwise schedule launches its kernels one by one here (no graph is built).
+ * Every call on one device shares that array: calls that overlap in time on
+ * the same device race and must be serialised by the caller (one stream, or
+ * events).  No hipMalloc, hipFree or allocating library call is made.
+ */
+isam_status_t isam_gru_forward_noalloc(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
+                                       int w_type, const void* x, const float* h0, const void* W,
+                                       const void* U, const float* bias, const float* bias_hn,
+                                       float* h_seq, float* h_T, void* stream);
+
+/*
  * 1D convolution of the paper's second listing (Section 2), valid positions,
  * stride 1:
  *   C[i][x][ko] (+)= sum_{d < D} sum_{ki < Ki} A[i][x+d][ki] * B[d][ki][ko]

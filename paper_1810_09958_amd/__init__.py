@@ -16,7 +16,7 @@ import torch
 
 from ._lib import (ISAM_BF16, ISAM_F32, IsamError, lib, lib_path)
 
-__all__ = ["gemm", "conv1d", "dwsep_conv", "gru_forward", "gemm_workspace_size",
+__all__ = ["gemm", "conv1d", "dwsep_conv", "gru_forward", "gru_forward_noalloc", "gemm_workspace_size",
            "dwsep_conv_workspace_size", "gru_forward_workspace_size", "IsamError",
            "lib", "lib_path", "ISAM_F32", "ISAM_BF16", "version"]
 
@@ -203,4 +203,23 @@ def gru_forward(x: torch.Tensor, W: torch.Tensor, U: torch.Tensor, *, bias=None,
                                 _ptr(bias_hn), _ptr(h_seq), _ptr(h_T), _ptr(workspace),
                                 workspace.numel(), _stream())
     _call(rc, "isam_gru_forward")
+    return h_seq, h_T
+
+
+def gru_forward_noalloc(x: torch.Tensor, W: torch.Tensor, U: torch.Tensor, h_seq: torch.Tensor,
+                        h_T: torch.Tensor, *, bias=None, bias_hn=None, h0=None):
+    """GRU forward through isam_gru_forward_noalloc: the library's static device scratch
+    serves as workspace and nothing is allocated (h_seq and h_T are caller-provided; either
+    may be None, not both).  Calls that overlap in time on one device race."""
+    _check_dev(x, W, U, bias, bias_hn, h0, h_seq, h_T)
+    for t in (x, W, U, bias, bias_hn, h0, h_seq, h_T):
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    if not (x.dtype == W.dtype == U.dtype):
+        raise TypeError("x, W, U must share a dtype")
+    T, B, I = x.shape
+    H = U.shape[1]
+    rc = lib().isam_gru_forward_noalloc(T, B, I, H, _dt(W), _ptr(x), _ptr(h0), _ptr(W), _ptr(U), _ptr(bias),
+                                        _ptr(bias_hn), _ptr(h_seq), _ptr(h_T), _stream())
+    _call(rc, "isam_gru_forward_noalloc")
     return h_seq, h_T

@@ -16,6 +16,7 @@ SIGNATURES = {
     "isam_dwsep_conv_workspace_size": (sz, [i64] * 10 + [ci, ci]),
     "isam_gru_forward": (ci, [i64, i64, i64, i64, ci, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
     "isam_gru_forward_workspace_size": (sz, [i64, i64, i64, i64, ci]),
+    "isam_gru_forward_noalloc": (ci, [i64, i64, i64, i64, ci, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
     "isam_conv1d": (ci, [i64, i64, i64, i64, i64, ci, vp, vp, ci, ci, vp, vp]),
     "isam_status_string": (ctypes.c_char_p, [ci]),
     "isam_last_error": (ctypes.c_char_p, []),

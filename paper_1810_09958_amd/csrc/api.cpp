@@ -569,13 +569,16 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
 
 }  // extern "C"
 
-extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
-                                          int w_type, const void* x, const float* h0, const void* W,
-                                          const void* U, const float* bias, const float* bias_hn,
-                                          float* h_seq, float* h_T, void* workspace,
-                                          size_t workspace_bytes, void* stream) {
-    g_last_error.clear();
-    const char* who = "isam_gru_forward";
+// Shared body of isam_gru_forward and isam_gru_forward_noalloc.  `workspace`
+// NULL with `scratch_fn` set: after validation, the workspace is the library's
+// static scratch (scratch_fn returns its address on the current device), and
+// the stepwise schedule launches its kernels directly instead of building a
+// graph, so nothing is allocated.
+static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
+                                      int w_type, const void* x, const float* h0, const void* W,
+                                      const void* U, const float* bias, const float* bias_hn,
+                                      float* h_seq, float* h_T, void* workspace, size_t workspace_bytes,
+                                      void* stream, const char* who, bool no_alloc) {
     if (T < 0 || batch < 0 || input_size <= 0 || hidden_size <= 0)
         return fail(ISAM_ERR_INVALID_ARG, "%s: T, batch >= 0 and input_size, hidden_size > 0 required", who);
     if (!valid_dtype(w_type)) return fail(ISAM_ERR_INVALID_ARG, "%s: w_type must be 0 or 1", who);
@@ -609,6 +612,14 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
             return fail(ISAM_ERR_INVALID_ARG, "%s: an output overlaps an input", who);
     }
     const size_t need = isam_gru_forward_workspace_size(T, batch, I, H, w_type);
+    if (no_alloc) {
+        if (need > kGruScratchBytes)
+            return fail(ISAM_ERR_WORKSPACE, "%s: these sizes need %zu bytes of scratch; the static scratch holds %zu",
+                        who, need, (size_t)kGruScratchBytes);
+        hipError_t se = gru_scratch(&workspace);
+        if (se != hipSuccess) return hip_fail(se, who);
+        workspace_bytes = kGruScratchBytes;
+    }
     if (!workspace || workspace_bytes < need)
         return fail(ISAM_ERR_WORKSPACE, "%s: workspace of %zu bytes < %zu required", who, workspace_bytes, need);
     if ((h_seq && overlaps(workspace, need, h_seq, (size_t)T * state)) || (h_T && overlaps(workspace, need, h_T, state)))
@@ -732,9 +743,28 @@ extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t inpu
     // First-level barrier groups of 8 workgroups (measured fastest), larger
     // when a domain would otherwise need more group counters than it has.
     g.barrier_group = (int)std::max<int64_t>(8, cdiv(H / J, kGruMaxGroupsPerDomain));
-    e = step_mode ? launch_gru_steps(g, hstate, s) : launch_gru_recurrent(g, s);
+    e = step_mode ? launch_gru_steps(g, hstate, s, /*use_graph=*/!no_alloc) : launch_gru_recurrent(g, s);
     if (e != hipSuccess) return hip_fail(e, who);
     return ISAM_OK;
+}
+
+extern "C" isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
+                                          int w_type, const void* x, const float* h0, const void* W,
+                                          const void* U, const float* bias, const float* bias_hn,
+                                          float* h_seq, float* h_T, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+    g_last_error.clear();
+    return gru_forward_impl(T, batch, input_size, hidden_size, w_type, x, h0, W, U, bias, bias_hn, h_seq, h_T,
+                            workspace, workspace_bytes, stream, "isam_gru_forward", false);
+}
+
+extern "C" isam_status_t isam_gru_forward_noalloc(int64_t T, int64_t batch, int64_t input_size,
+                                                  int64_t hidden_size, int w_type, const void* x, const float* h0,
+                                                  const void* W, const void* U, const float* bias,
+                                                  const float* bias_hn, float* h_seq, float* h_T, void* stream) {
+    g_last_error.clear();
+    return gru_forward_impl(T, batch, input_size, hidden_size, w_type, x, h0, W, U, bias, bias_hn, h_seq, h_T,
+                            nullptr, 0, stream, "isam_gru_forward_noalloc", true);
 }
 
 extern "C" isam_status_t isam_conv1d(int64_t batch, int64_t L, int64_t Ki, int64_t D, int64_t Ko, int ab_type,

@@ -601,8 +601,8 @@ static hipError_t launch_gru_steps_direct(const GruArgs& a, float* hstate, hipSt
     return e;
 }
 
-hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s) {
-    if (a.T > kMaxGraphSteps || getenv("ISAM_GRU_NO_GRAPH")) return launch_gru_steps_direct(a, hstate, s);
+hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s, bool use_graph) {
+    if (!use_graph || a.T > kMaxGraphSteps || getenv("ISAM_GRU_NO_GRAPH")) return launch_gru_steps_direct(a, hstate, s);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -637,6 +637,40 @@ hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s) {
     e = hipGraphLaunch(hit->exec, s);
     if (e != hipSuccess) return e;
     return hipEventRecord(hit->done, s);
+}
+
+// Workspace of isam_gru_forward_noalloc: a static device array, so that
+// callers that cannot allocate (code under graph capture, tight serving loops)
+// need not pass one.  Each device holds its own copy for the life of the
+// process.  In host code `scratch` names a host-side stand-in, never a device
+// address: its device address is looked up once per device with
+// hipGetSymbolAddress and only that address is handed to kernels.  Every call
+// on a device shares the array, so calls that overlap in time on one device
+// race.
+static __device__ __align__(256) unsigned char scratch[kGruScratchBytes];
+
+hipError_t gru_scratch(void** ptr) {
+    static std::mutex mu;
+    static void* addr[64];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::unique_lock<std::mutex> lock(mu, std::defer_lock);
+    try {
+        lock.lock();
+    } catch (...) {
+        return hipErrorUnknown;
+    }
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
 }
 
 }  // namespace isam

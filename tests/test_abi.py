@@ -182,3 +182,16 @@ def test_conv1d_noops(L):
     assert conv1d(L, nb=0, A=None, B=None, C=None) == OK
     assert conv1d(L, Ko=0, A=None, B=None, C=None) == OK
     assert conv1d(L, Ln=2, D=3, A=None, B=None, C=None) == OK   # no valid position
+
+
+def test_gru_noalloc_rejects_sizes_beyond_its_scratch(L):
+    # T = 1024, batch 32, hidden 1024 needs ~410 MB of workspace, more than the 64 MiB static
+    # scratch of the allocation-free entry point: rejected before any HIP call.
+    need = L.isam_gru_forward_workspace_size(1024, 32, 1024, 1024, BF16)
+    assert need > 64 << 20
+    rc = L.isam_gru_forward_noalloc(1024, 32, 1024, 1024, BF16, FAKE, None, ctypes.c_void_p(0x30000),
+                                    ctypes.c_void_p(0x50000), None, None, ctypes.c_void_p(0x700000000),
+                                    None, None)
+    assert rc == WORKSPACE
+    assert b"static scratch" in L.isam_last_error()
+    assert L.isam_gru_forward_workspace_size(64, 32, 1024, 1024, BF16) <= 64 << 20
