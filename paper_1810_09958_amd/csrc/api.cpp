@@ -652,13 +652,42 @@ static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_si
     bool step_mode = (batch <= 16 && u_mb <= 16.0) || (batch <= 4 && u_mb <= 32.0);
     if (mode_env && strcmp(mode_env, "persistent") == 0) step_mode = false;
     if (mode_env && strcmp(mode_env, "steps") == 0) step_mode = true;
+    // Batch-group schedule (bf16, hidden 256..1024 in steps of 256): G barrier
+    // domains of P = H/32 workgroups, each domain a slice of at most 16 batch
+    // columns with the whole of U in its workgroups' registers.  As many
+    // domains as the batch, the CUs and the barrier area allow.
+    // Workgroups are dealt to the XCDs round-robin (32 CUs each on gfx950), so
+    // a domain of P workgroups taken at a stride of the XCD count lands on
+    // one XCD; the grid is X * P * ceil(G / X) workgroups.
+    int groups = 0, group_wgs = 0;
+    const int xcds = cus % 32 == 0 ? cus / 32 : 1;
+    const bool group_allowed = !(mode_env && (strcmp(mode_env, "persistent") == 0 || strcmp(mode_env, "steps") == 0));
+    if (group_allowed && w_type == ISAM_BF16 && gru_group_supported(H)) {
+        const int P = (int)(H / kGruGroupUnits);
+        const int64_t resident = (int64_t)cus * gru_group_blocks_per_cu(H);
+        const int64_t max_domains = kGruBarrierBytes / 4 / 512 - 1;
+        for (int64_t g = std::min<int64_t>(batch, max_domains); g >= 1; --g) {
+            const int64_t wgs = (int64_t)xcds * P * cdiv(g, xcds);
+            if (wgs <= resident && wgs <= kGruMaxWgs) {
+                if (cdiv(batch, g) <= 16) { groups = (int)g; group_wgs = (int)wgs; }
+                break;
+            }
+        }
+    }
+    if (mode_env && strcmp(mode_env, "group") == 0 && !groups)
+        return fail(ISAM_ERR_UNSUPPORTED, "%s: ISAM_GRU_MODE=group needs bf16 weights, hidden 256/512/768/1024 and "
+                    "at most 16 batch columns per domain", who);
     // Units per workgroup: the smallest power of two whose grid fits one
     // workgroup per CU (measured faster than packing two per CU); if none
     // does, the smallest that fits at the occupancy limit.  Batch groups
     // have separate barriers.
     int J = 0;
     int n_wg = 0;
-    if (!step_mode) {
+    if (groups) {
+        step_mode = false;
+        J = kGruGroupUnits;
+        n_wg = group_wgs;
+    } else if (!step_mode) {
         for (int pass = 0; pass < 2 && !J; ++pass) {
             for (int cand = 1; cand <= 16; cand *= 2) {
                 if (H % cand) continue;
@@ -680,7 +709,7 @@ static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_si
                 n_wg = (int)((H / v) * n_bg);
             }
         }
-        if (!J || n_bg > kGruSyncBytes / 4 / 512 - 1) step_mode = true;  // one 512-word barrier domain per batch group
+        if (!J || n_bg > kGruBarrierBytes / 4 / 512 - 1) step_mode = true;  // one 512-word barrier domain per batch group
     }
     if (step_mode) {
         // No residency constraint: the smallest power of two whose grid fits
@@ -698,8 +727,9 @@ static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_si
         n_wg = (int)((H / J) * n_bg);
     }
     if (log_enabled())
-        fprintf(stderr, "[isam] gru T=%lld B=%lld I=%lld H=%lld w=%d mode=%s J=%d BB=%d wgs=%d\n", (long long)T,
-                (long long)batch, (long long)I, (long long)H, w_type, step_mode ? "steps" : "persistent", J, BB, n_wg);
+        fprintf(stderr, "[isam] gru T=%lld B=%lld I=%lld H=%lld w=%d mode=%s J=%d BB=%d wgs=%d groups=%d\n", (long long)T,
+                (long long)batch, (long long)I, (long long)H, w_type,
+                groups ? "group" : (step_mode ? "steps" : "persistent"), J, BB, n_wg, groups);
 
     char* ws = static_cast<char*>(workspace);
     float* gx = reinterpret_cast<float*>(ws);
@@ -743,7 +773,20 @@ static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_si
     // First-level barrier groups of 8 workgroups (measured fastest), larger
     // when a domain would otherwise need more group counters than it has.
     g.barrier_group = (int)std::max<int64_t>(8, cdiv(H / J, kGruMaxGroupsPerDomain));
-    e = step_mode ? launch_gru_steps(g, hstate, s, /*use_graph=*/!no_alloc) : launch_gru_recurrent(g, s);
+    g.groups = groups;
+    g.xcds = xcds;
+    if (groups) {
+        g.barrier_group = 16;  // two first-level counters for 32 members (measured best of 4..32)
+        if (const char* bg_env = getenv("ISAM_GRU_BGROUP")) {  // tuning override
+            const int v = atoi(bg_env);
+            if (v >= 1 && cdiv(n_wg / groups, v) <= kGruMaxGroupsPerDomain) g.barrier_group = v;
+        }
+        if (const char* sc_env = getenv("ISAM_GRU_GROUP_SCOPE"); sc_env && strcmp(sc_env, "device") == 0)
+            g.device_scope = 1;
+        e = launch_gru_group(g, s);
+    } else {
+        e = step_mode ? launch_gru_steps(g, hstate, s, /*use_graph=*/!no_alloc) : launch_gru_recurrent(g, s);
+    }
     if (e != hipSuccess) return hip_fail(e, who);
     return ISAM_OK;
 }

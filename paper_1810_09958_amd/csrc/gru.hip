@@ -281,6 +281,232 @@ __global__ __launch_bounds__(64 * kWaves) void gru_recurrent_kernel(GruArgs a) {
     if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
 }
 
+// Batch-group form of the persistent recurrence (bf16 weights).  The batch
+// columns are independent sequences, so the grid is split into `groups`
+// barrier domains: domain g owns a contiguous slice of at most 16 columns and
+// runs on P = n_wg / groups workgroups, each owning 32 hidden units (the 96 rows
+// of U of their three gates).  Against one domain per 16 columns spread over
+// the whole chip this trades more matrix-core work per workgroup (cheap at
+// these sizes) for a barrier among P workgroups instead of 128 and an h
+// exchange of the domain's own columns only (8 KiB per workgroup and step at
+// 4 columns and hidden 1024, instead of 32 KiB).  Workgroup g + groups * r is
+// member r of domain g, so under the round-robin dispatch of workgroups to XCDs
+// a domain sits on one XCD.
+//
+// Exchange.  At launch every workgroup publishes its XCC id (device scope) and
+// the domain passes one device-scope barrier; then each member reads the ids of
+// its domain.  If all members share one XCD (the normal case), h and the step
+// flags travel through that XCD's L2: stores with workgroup scope (sc0) reach
+// the L2, and loads with system scope (sc0 sc1) miss the per-CU L1 and return
+// the L2's copy; the step barrier is one flag word per member (no atomics,
+// which are performed beyond the L2) -- member r stores t+1 into word r after
+// every wave's stores have completed, and one wave polls the P words.  If the
+// members are spread over XCDs, everything goes through device-scope stores,
+// loads and the atomic barrier instead.  The choice is made per domain from
+// data every member reads alike, so it is uniform within the domain.
+//
+// Priming: each of the 8 waves loads its K range (H / 8 values) of all 96 rows
+// of U into registers, where it stays for the whole launch -- the weights live
+// on the register files between steps, as in the paper's recurrent schedule.
+// Recursive step: every wave reads the domain's h_{t-1} for its K range from
+// ring slot t, runs 6 x KS MFMAs of 16x16x32, and the 8 partial tiles are
+// summed through LDS in wave order; the owner threads (unit, column) apply the
+// gates, write h_seq (fp32) and ring slot t+1 (bf16), then the domain barrier.
+// Finish: h_T.
+constexpr int kGWaves = 8;
+constexpr int kGRows = 3 * kGruGroupUnits;  // 96 rows of U per workgroup
+constexpr int kGMT = kGRows / 16;           // 6 row tiles of 16
+constexpr int kCpolGroup = 1;               // sc0: workgroup scope
+constexpr int kCpolSystem = 17;             // sc0 sc1: system scope
+
+// Poll the P flag words of a domain (one wave) until each holds at least
+// `target`; bounded like the grid barrier, and stops early on the error word.
+__device__ __forceinline__ void flag_wait(const GruArgs& a, __amdgpu_buffer_rsrc_t rs_sync, uint32_t flag_off,
+                                          int P, unsigned target) {
+    const int l = threadIdx.x;  // wave 0
+    const uint64_t start = wall_clock64();
+    for (unsigned it = 1;; ++it) {
+        const unsigned v = (unsigned)__builtin_amdgcn_raw_buffer_load_b32(rs_sync, (int)(flag_off + 4u * (unsigned)(l % P)), 0,
+                                                                        kCpolSystem);
+        if (__builtin_amdgcn_ballot_w64(l < P && v < target) == 0) break;
+        // the sticky error word lives beyond the L2: look at it now and then only
+        if ((it & 255u) == 0 && __hip_atomic_load(a.sync + kSyncError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+            break;
+        if (wall_clock64() - start > a.timeout_ticks) {
+            if (l == 0) __hip_atomic_fetch_or(a.sync + kSyncError, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+    }
+}
+
+template <int KS, bool LOCAL>
+__device__ __forceinline__ void group_steps(const GruArgs& a, const uint4 (&uf)[kGMT][KS], float* red, int g, int rank,
+                                            int P, int64_t c0, int nb, float h_prev, float bias_r, float bias_z,
+                                            float bias_n, float bias_hn) {
+    constexpr int cp_st = LOCAL ? kCpolGroup : kCpolDevice;
+    constexpr int cp_ld = LOCAL ? kCpolSystem : kCpolDevice;
+    const int64_t H = a.H, B = a.batch;
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int n_col = lane & 15, quarter = lane >> 4;
+    const bool owner = tid < kGruGroupUnits * nb;
+    const int jj = owner ? tid % kGruGroupUnits : 0, nn = owner ? tid / kGruGroupUnits : 0;
+    const int64_t j = (int64_t)rank * kGruGroupUnits + jj, bb = c0 + nn;
+    float gx_r = 0.f, gx_z = 0.f, gx_n = 0.f;
+    auto fetch_gx = [&](int64_t t) {
+        if (owner && t < a.T) {
+            const float* gx = a.gx + (t * B + bb) * 3 * H;
+            gx_r = gx[j];
+            gx_z = gx[H + j];
+            gx_n = gx[2 * H + j];
+        }
+    };
+    fetch_gx(0);
+    const bool col_ok = n_col < nb;
+    const int64_t h_row = (c0 + n_col) * H;
+    const __amdgpu_buffer_rsrc_t rs_h = make_rsrc(a.hbuf, (uint32_t)((a.T + 1) * a.slot * 2));
+    const __amdgpu_buffer_rsrc_t rs_sync = make_rsrc(a.sync, (uint32_t)kGruSyncBytes);
+    const uint32_t flag_off = (uint32_t)(kGruFlagWord + 64 * g) * 4u;
+    for (int64_t t = 0; t < a.T; ++t) {
+        uint4 hv[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            const int64_t k = (int64_t)(wid * KS + s) * 32 + quarter * 8;
+            const uint32_t off = col_ok ? (uint32_t)((t * a.slot + h_row + k) * 2) : kOob;
+            hv[s] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs_h, (int)off, 0, cp_ld));
+        }
+        // every h load of the step in flight before the first wait
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4_t acc[kGMT];
+#pragma unroll
+        for (int m = 0; m < kGMT; ++m) acc[m] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+#pragma unroll
+            for (int m = 0; m < kGMT; ++m) mfma16_bf16(acc[m], uf[m][s], hv[s]);
+        }
+        // acc[m] element v of lane l: local row m*16 + 4*(l/16) + v, column l%16
+#pragma unroll
+        for (int m = 0; m < kGMT; ++m) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) red[(wid * kGRows + m * 16 + 4 * quarter + v) * kRedLd + n_col] = acc[m][v];
+        }
+        __syncthreads();
+        if (owner) {
+            float gh[3];
+#pragma unroll
+            for (int q = 0; q < 3; ++q) {
+                float sum = 0.0f;
+#pragma unroll
+                for (int w = 0; w < kGWaves; ++w) sum += red[(w * kGRows + q * kGruGroupUnits + jj) * kRedLd + nn];
+                gh[q] = sum;
+            }
+            const float r = gate_sigmoid(gx_r + bias_r + gh[0]);
+            const float z = gate_sigmoid(gx_z + bias_z + gh[1]);
+            const float n = gate_tanh(gx_n + bias_n + r * (gh[2] + bias_hn));
+            const float h = (1.0f - z) * n + z * h_prev;
+            h_prev = h;
+            if (a.h_seq) a.h_seq[(t * B + bb) * H + j] = h;
+            const int64_t hn = (t + 1) * a.slot + bb * H + j;  // ring slot t+1
+            __builtin_amdgcn_raw_buffer_store_b16((unsigned short)f32_to_bf16(h), rs_h, (int)(hn * 2), 0, cp_st);
+        }
+        fetch_gx(t + 1);
+        if (t + 1 < a.T) {
+            if constexpr (LOCAL) {
+                // every wave's slot stores complete (in the L2) before the flag
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                __syncthreads();
+                if (tid == 0)
+                    __builtin_amdgcn_raw_buffer_store_b32((unsigned)(t + 1), rs_sync, (int)(flag_off + 4u * (uint32_t)rank), 0,
+                                                          kCpolGroup);
+                if (wid == 0) flag_wait(a, rs_sync, flag_off, P, (unsigned)(t + 1) + (unsigned)a.stall);
+                __syncthreads();
+            } else {
+                grid_barrier(a, t + 1, g, rank, P);  // round 0 was the placement check
+            }
+        } else {
+            __syncthreads();
+        }
+    }
+    if (owner && a.h_T) a.h_T[bb * H + j] = h_prev;
+}
+
+template <int KS>
+__global__ __launch_bounds__(64 * kGWaves) void gru_group_kernel(GruArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    float* red = reinterpret_cast<float*>(smem);  // [kGWaves][kGRows][kRedLd]
+    __shared__ int s_local;
+    const int64_t H = a.H, B = a.batch;
+    // Workgroup b is slot i = b / X of XCD lane x = b % X (X = a.xcds, the
+    // round-robin width of the dispatcher); slots are cut into layers of P,
+    // and domain g = x + X * layer takes rank i % P.  Slots of domains past
+    // the last one have no work.
+    const int G = a.groups, P = (int)(H / kGruGroupUnits), X = a.xcds;
+    const int xl = (int)(blockIdx.x % (unsigned)X), slot = (int)(blockIdx.x / (unsigned)X);
+    const int layer = slot / P, rank = slot % P;
+    const int g = xl + X * layer;
+    if (g >= G) return;
+    const int64_t c0 = (B * g) / G, c1 = (B * (g + 1)) / G;
+    const int nb = (int)(c1 - c0);
+    const int64_t j0 = (int64_t)rank * kGruGroupUnits;
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int n_col = lane & 15, quarter = lane >> 4;
+
+    // Placement: publish this workgroup's XCC id, one device-scope barrier of
+    // the domain, then compare the ids of all members.
+    const __amdgpu_buffer_rsrc_t rs_sync = make_rsrc(a.sync, (uint32_t)kGruSyncBytes);
+    if (tid == 0) {
+        const unsigned xcc = __builtin_amdgcn_s_getreg((20) | (0 << 6) | (31 << 11)) & 0xfu;  // HW_REG_XCC_ID
+        __builtin_amdgcn_raw_buffer_store_b32(xcc, rs_sync, (int)((kGruXccWord + blockIdx.x) * 4u), 0, kCpolDevice);
+    }
+    grid_barrier(a, 0, g, rank, P);
+    if (wid == 0) {
+        unsigned id = 0, id0 = 0;
+        for (int r0 = 0; r0 < P; r0 += 64) {
+            const int r = r0 + lane;
+            const unsigned v = r < P ? (unsigned)__builtin_amdgcn_raw_buffer_load_b32(
+                                           rs_sync, (int)((kGruXccWord + xl + X * (layer * P + r)) * 4u), 0, kCpolDevice)
+                                     : 0u;
+            if (r0 == 0) id0 = __builtin_amdgcn_readfirstlane(v);
+            id |= (r < P && v != id0) ? 1u : 0u;
+        }
+        const bool same = __builtin_amdgcn_ballot_w64(id != 0) == 0;
+        if (lane == 0) s_local = (same && !a.device_scope) ? 1 : 0;
+    }
+
+    // Priming: U fragments of this wave.  Local row lr = m*16 + n_col is unit
+    // lr % 32 of gate lr / 32; K-step s of wave w covers K [(w*KS + s)*32, +32),
+    // of which this lane carries the 8 values at quarter*8.
+    uint4 uf[kGMT][KS];
+    {
+        const __amdgpu_buffer_rsrc_t rs_u = make_rsrc(a.U, (uint32_t)(3 * H * H * 2));
+#pragma unroll
+        for (int m = 0; m < kGMT; ++m) {
+            const int lr = m * 16 + n_col;
+            const int64_t row = (int64_t)(lr / kGruGroupUnits) * H + j0 + lr % kGruGroupUnits;
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                const int64_t k = (int64_t)(wid * KS + s) * 32 + quarter * 8;
+                uf[m][s] = buf_load16(rs_u, (uint32_t)((row * H + k) * 2));
+            }
+        }
+    }
+    const bool owner = tid < kGruGroupUnits * nb;
+    const int jj = owner ? tid % kGruGroupUnits : 0, nn = owner ? tid / kGruGroupUnits : 0;
+    const int64_t j = j0 + jj, bb = c0 + nn;
+    float h_prev = 0.0f;
+    float bias_r = 0.f, bias_z = 0.f, bias_n = 0.f, bias_hn = 0.f;
+    if (owner) {
+        if (a.h0) h_prev = a.h0[bb * H + j];
+        if (a.bias) { bias_r = a.bias[j]; bias_z = a.bias[H + j]; bias_n = a.bias[2 * H + j]; }
+        if (a.bias_hn) bias_hn = a.bias_hn[j];
+    }
+    __syncthreads();
+    if (s_local)
+        group_steps<KS, true>(a, uf, red, g, rank, P, c0, nb, h_prev, bias_r, bias_z, bias_n, bias_hn);
+    else
+        group_steps<KS, false>(a, uf, red, g, rank, P, c0, nb, h_prev, bias_r, bias_z, bias_n, bias_hn);
+}
+
 // Stepwise form of the same recurrence: the priming, recursive and finish
 // iterations as separate kernels, chained in a graph by the host (Section
 // 3.6's schedule with T fixed per call).  One launch per step t: every
@@ -460,6 +686,58 @@ hipError_t launch_gru_error_fill(const GruArgs& a, hipStream_t s) {
     blocks = blocks > 1024 ? 1024 : (blocks < 1 ? 1 : blocks);
     hipLaunchKernelGGL(gru_error_fill_kernel, dim3(blocks), dim3(256), 0, s, a.sync, a.h_seq, n_seq, a.h_T, n_T);
     return hipGetLastError();
+}
+
+bool gru_group_supported(int64_t H) { return H % 256 == 0 && H >= 256 && H <= 1024; }
+
+size_t gru_group_lds_bytes() { return (size_t)kGWaves * kGRows * kRedLd * sizeof(float); }
+
+hipError_t launch_gru_group(const GruArgs& a, hipStream_t s) {
+    void* fn = nullptr;
+    switch (a.H / 256) {
+        case 1: fn = reinterpret_cast<void*>(gru_group_kernel<1>); break;
+        case 2: fn = reinterpret_cast<void*>(gru_group_kernel<2>); break;
+        case 3: fn = reinterpret_cast<void*>(gru_group_kernel<3>); break;
+        case 4: fn = reinterpret_cast<void*>(gru_group_kernel<4>); break;
+        default: return hipErrorInvalidValue;
+    }
+    const int P = (int)(a.H / kGruGroupUnits);
+    if (a.w_type != kBF16 || a.groups <= 0 || a.xcds <= 0 || (a.batch + a.groups - 1) / a.groups > 16 ||
+        a.n_wg != a.xcds * P * ((a.groups + a.xcds - 1) / a.xcds) || a.n_wg > kGruMaxWgs)
+        return hipErrorInvalidValue;
+    const size_t lds = gru_group_lds_bytes();
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    int64_t n = a.batch * a.H;
+    int blocks = (int)((n + 255) / 256);
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(gru_init_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    GruArgs args = a;
+    void* params[] = {&args};
+    e = hipLaunchCooperativeKernel(fn, dim3(a.n_wg), dim3(64 * kGWaves), params, (unsigned)lds, s);
+    if (e != hipSuccess) return e;
+    return launch_gru_error_fill(a, s);
+}
+
+int gru_group_blocks_per_cu(int64_t H) {
+    void* fn = nullptr;
+    switch (H / 256) {
+        case 1: fn = reinterpret_cast<void*>(gru_group_kernel<1>); break;
+        case 2: fn = reinterpret_cast<void*>(gru_group_kernel<2>); break;
+        case 3: fn = reinterpret_cast<void*>(gru_group_kernel<3>); break;
+        case 4: fn = reinterpret_cast<void*>(gru_group_kernel<4>); break;
+        default: return 0;
+    }
+    int n = 0;
+    const size_t lds = gru_group_lds_bytes();
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, 64 * kGWaves, lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return n;
 }
 
 size_t gru_lds_bytes(int w_type, int64_t H, int J) {

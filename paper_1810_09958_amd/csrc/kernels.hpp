@@ -116,6 +116,10 @@ struct GruArgs {
     int batch_per_wg;       // BB
     int n_wg;
     int barrier_group;      // workgroups per first-level barrier counter
+    int groups;             // batch-group schedule: barrier domains (batch groups); 0 otherwise
+    int device_scope;       // batch-group schedule: 1 = exchange through device scope even when a
+                            // domain sits on one XCD
+    int xcds;               // batch-group schedule: width of the round-robin dispatch over XCDs
 };
 // Barrier layout of the GRU kernel: per batch group a domain of 512 words
 // holds the domain counter and up to 31 first-level group counters (64
@@ -124,11 +128,29 @@ constexpr int kGruMaxGroupsPerDomain = 31;
 size_t gru_lds_bytes(int w_type, int64_t H, int J);
 // Resident workgroups of the recurrent kernel per compute unit at this LDS size.
 int gru_blocks_per_cu(int w_type, size_t lds);
-constexpr int kGruSyncBytes = 32768;  // barrier area at the end of the GRU workspace
+// Barrier area of the GRU workspace: the domain counters of the grid barrier
+// in the first 32 KiB, then per-domain flag words (64 per domain) and the XCC
+// id of every workgroup (batch-group schedule).
+constexpr int kGruBarrierBytes = 32768;
+constexpr int kGruSyncBytes = 65536;
+constexpr int kGruFlagWord = 8192;    // flags of domain d: words kGruFlagWord + 64 d ..
+constexpr int kGruXccWord = 12288;    // XCC id of workgroup b: word kGruXccWord + b
+constexpr int kGruMaxWgs = 4096;
 // Ring slot stride in elements: whole 256-byte blocks, so no cache line holds
 // parts of two slots.
 inline int64_t gru_slot_elems(int64_t batch, int64_t H, int64_t es) { return (batch * H * es + 255) / 256 * 256 / es; }
 hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s);
+// Batch-group persistent recurrence (bf16): `groups` independent barrier
+// domains, each a set of n_wg / groups workgroups that own kGruGroupUnits
+// hidden units apiece with their rows of U held in registers, and each a
+// contiguous slice of the batch.  Needs H = 256 * KS (KS in 1..4), at most 16
+// batch columns per group and every workgroup resident.
+constexpr int kGruGroupUnits = 32;
+bool gru_group_supported(int64_t H);
+size_t gru_group_lds_bytes();
+hipError_t launch_gru_group(const GruArgs& a, hipStream_t s);
+// Resident workgroups of the batch-group kernel per compute unit (0: none).
+int gru_group_blocks_per_cu(int64_t H);
 // NaN into h_seq and h_T if the recurrence's sticky error word is set.
 hipError_t launch_gru_error_fill(const GruArgs& a, hipStream_t s);
 // Bound on one barrier wait of the persistent recurrence (2 s at 100 MHz).

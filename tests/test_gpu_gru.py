@@ -16,11 +16,15 @@ pytestmark = pytest.mark.gpu
 import paper_1810_09958_amd as isam
 
 
-@pytest.fixture(params=["steps", "persistent"])
+@pytest.fixture(params=["steps", "persistent", "default"])
 def mode(request, monkeypatch):
-    """The two schedules of the recurrence: one kernel per step replayed from a
-    graph, or one persistent kernel with a grid barrier between steps."""
-    monkeypatch.setenv("ISAM_GRU_MODE", request.param)
+    """The schedules of the recurrence: one kernel per step replayed from a graph, one
+    persistent kernel with a grid barrier between steps, and the library's own choice
+    (the batch-group persistent kernel for bf16 weights and hidden 256..1024)."""
+    if request.param == "default":
+        monkeypatch.delenv("ISAM_GRU_MODE", raising=False)
+    else:
+        monkeypatch.setenv("ISAM_GRU_MODE", request.param)
     return request.param
 
 
@@ -316,3 +320,99 @@ def test_output_guard_bands(dt, mode):
         assert np.all(h[:g] == -777.0) and np.all(h[g + n:] == -777.0)
     err = float(np.max(np.abs(hs.cpu().numpy().astype(np.float64) - oracle.gru(x, W, U, b, None, h0))))
     assert err <= (TOL_BF16 if dt == "bf16" else TOL_F32), err
+
+
+# Batch-group schedule (bf16 weights, hidden 256/512/768/1024): independent barrier domains of
+# H/32 workgroups, each owning a slice of at most 16 batch columns, U rows in registers.
+@pytest.fixture(params=["xcd", "device"])
+def group_scope(request, monkeypatch):
+    """The two exchanges of the batch-group kernel: through the L2 of the XCD a domain
+    sits on (taken when all its workgroups share one), or device scope throughout."""
+    if request.param == "device":
+        monkeypatch.setenv("ISAM_GRU_GROUP_SCOPE", "device")
+    else:
+        monkeypatch.delenv("ISAM_GRU_GROUP_SCOPE", raising=False)
+    return request.param
+
+
+@pytest.mark.parametrize("H", [256, 512, 768, 1024])
+@pytest.mark.parametrize("B", [1, 3, 4, 17, 32, 33, 128])
+def test_group_schedule_shapes(H, B, group_scope, monkeypatch):
+    monkeypatch.setenv("ISAM_GRU_MODE", "group")
+    _run(5 if B < 100 else 3, B, 72, H, "bf16", seed=B + H, with_h0=True, with_bhn=(B % 2 == 1), scale=1 / 8)
+
+
+@pytest.mark.parametrize("T", [1, 2, 9])
+def test_group_schedule_steps(T, group_scope, monkeypatch):
+    monkeypatch.setenv("ISAM_GRU_MODE", "group")
+    _run(T, 8, 40, 256, "bf16", seed=50 + T, with_h0=True, with_bhn=True, scale=1 / 4)
+
+
+def test_group_schedule_poisoned_workspace_and_repeat(group_scope, monkeypatch):
+    # NaN-filled workspace before each call, two calls with different inputs on one workspace.
+    monkeypatch.setenv("ISAM_GRU_MODE", "group")
+    T, B, I, H = 7, 33, 64, 768
+    need = isam.gru_forward_workspace_size(T, B, I, H, isam.ISAM_BF16)
+    ws = torch.empty(need, device="cuda", dtype=torch.uint8)
+    for seed in (61, 62):
+        x, W, U, b, h0, bhn = _inputs(T, B, I, H, seed=seed, scale=1 / 8, with_h0=True, with_bhn=True)
+        x, W, U = bits(x), bits(W), bits(U)
+        ws.fill_(0xFF)
+        hs, hT = isam.gru_forward(to_gpu(x), to_gpu(W), to_gpu(U), bias=to_gpu(b), bias_hn=to_gpu(bhn),
+                                  h0=to_gpu(h0), workspace=ws)
+        torch.cuda.synchronize()
+        got = hs.cpu().numpy().astype(np.float64)
+        assert np.all(np.isfinite(got))
+        err = float(np.max(np.abs(got - oracle.gru(x, W, U, b, bhn, h0))))
+        assert err <= TOL_BF16, f"seed {seed}: {err:.3e}"
+        assert np.array_equal(hT.cpu().numpy(), hs[-1].cpu().numpy())
+
+
+def test_group_schedule_barrier_timeout_returns_nan(group_scope, monkeypatch):
+    monkeypatch.setenv("ISAM_GRU_MODE", "group")
+    T, B, I, H = 4, 4, 32, 256
+    x, W, U, b, _, _ = _inputs(T, B, I, H, seed=63, scale=1 / 4)
+    x, W, U = bits(x), bits(W), bits(U)
+    args = [to_gpu(a) for a in (x, W, U)]
+    need = isam.gru_forward_workspace_size(T, B, I, H, isam.ISAM_BF16)
+    ws = torch.empty(need, device="cuda", dtype=torch.uint8)
+    monkeypatch.setenv("ISAM_GRU_TEST_STALL", "1")
+    hs, hT = isam.gru_forward(*args, bias=to_gpu(b), workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.all(torch.isnan(hs)).item() and torch.all(torch.isnan(hT)).item()
+    monkeypatch.delenv("ISAM_GRU_TEST_STALL")
+    hs, hT = isam.gru_forward(*args, bias=to_gpu(b), workspace=ws)
+    torch.cuda.synchronize()
+    err = float(np.max(np.abs(hs.cpu().numpy().astype(np.float64) - oracle.gru(x, W, U, b, None, None))))
+    assert err <= TOL_BF16, err
+
+
+def test_group_schedule_deterministic_and_guarded(group_scope, monkeypatch):
+    monkeypatch.setenv("ISAM_GRU_MODE", "group")
+    T, B, I, H = 6, 20, 48, 512
+    x, W, U, b, h0, _ = _inputs(T, B, I, H, seed=64, scale=1 / 8, with_h0=True)
+    x, W, U = bits(x), bits(W), bits(U)
+    args = [to_gpu(a) for a in (x, W, U)]
+    g = 1024
+    outs = []
+    for _ in range(2):
+        buf_s = torch.full((T * B * H + 2 * g,), -777.0, device="cuda")
+        buf_t = torch.full((B * H + 2 * g,), -777.0, device="cuda")
+        hs = buf_s[g: g + T * B * H].view(T, B, H)
+        hT = buf_t[g: g + B * H].view(B, H)
+        isam.gru_forward(*args, bias=to_gpu(b), h0=to_gpu(h0), h_seq=hs, h_T=hT)
+        torch.cuda.synchronize()
+        for buf, n in ((buf_s, T * B * H), (buf_t, B * H)):
+            h = buf.cpu().numpy()
+            assert np.all(h[:g] == -777.0) and np.all(h[g + n:] == -777.0)
+        outs.append(hs.clone())
+    assert torch.equal(outs[0], outs[1])
+    err = float(np.max(np.abs(outs[0].cpu().numpy().astype(np.float64) - oracle.gru(x, W, U, b, None, h0))))
+    assert err <= TOL_BF16, err
+
+
+def test_group_mode_rejects_unsupported(monkeypatch):
+    monkeypatch.setenv("ISAM_GRU_MODE", "group")
+    x, W, U, b, _, _ = _inputs(3, 2, 16, 96, seed=65)
+    with pytest.raises(isam.IsamError):
+        isam.gru_forward(to_gpu(bits(x)), to_gpu(bits(W)), to_gpu(bits(U)), bias=to_gpu(b))
