@@ -22,8 +22,10 @@
  *   - Outputs must not overlap inputs (detected by address range).
  *   - Each operand's addressed extent must be below 2^31 bytes
  *     (ISAM_ERR_UNSUPPORTED otherwise).
- *   - Entry points are thread-safe; the only global state is a cache of
- *     device properties.
+ *   - Entry points are thread-safe.  The library keeps no state between
+ *     calls other than per-device caches filled once and never changed: CU
+ *     count, LDS size, and the address of the static scratch that
+ *     isam_gru_forward_noalloc uses.
  */
 #ifndef ISAM_H
 #define ISAM_H
@@ -123,16 +125,21 @@ size_t isam_dwsep_conv_workspace_size(int64_t batch, int64_t H, int64_t W, int64
  * hidden must be a multiple of 8 (bf16) or 4 (fp32).  The bf16 path rounds
  * h_{t-1} to bf16 only as the matrix-core operand; the state stays fp32.
  * T == 0: h_T = h0 (or zeros).  batch == 0: no-op.
- * Two schedules compute the same values bit for bit: a persistent kernel with
- * U held in on-chip memory and a grid barrier per step, or the priming,
- * recursive and finish iterations as separate kernels (one per step) replayed
- * from a graph that the library builds and caches per call signature (sizes
- * and every pointer, workspace included; up to 32 signatures).  The faster one
- * for the shape runs by default; the environment variable ISAM_GRU_MODE
- * (persistent | steps) overrides, and the stepwise schedule runs whenever the
- * persistent kernel cannot keep all its workgroups resident, so any hidden size
- * that meets the multiple rule is supported.  Calls on one workspace must not
- * overlap in time.
+ * Schedules (the faster one for the shape runs; the environment variable
+ * ISAM_GRU_MODE = group | persistent | steps overrides):
+ *   - batch-group (bf16 weights, hidden 256, 512, 768 or 1024, at most 16
+ *     batch columns per domain): independent barrier domains of hidden/32
+ *     workgroups, one batch slice each, U rows held in registers;
+ *   - persistent: one kernel with U held in on-chip memory and a grid barrier
+ *     per step;
+ *   - stepwise: the priming, recursive and finish iterations as separate
+ *     kernels, one per step, launched in order (no co-residency needed, so
+ *     any hidden size that meets the multiple rule is supported).
+ * The persistent and stepwise schedules give the same values bit for bit.  A
+ * persistent barrier wait that exceeds 2 s (never, for a launch whose
+ * workgroups are all resident, as cooperative launches guarantee) ends the
+ * recurrence early and fills h_seq and h_T with NaN.  Calls on one workspace
+ * must not overlap in time.
  */
 isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
                                int w_type, const void* x, const float* h0, const void* W,
@@ -151,8 +158,7 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
  * outputs); the workspace is instead a static 64 MiB device array of the
  * library (one per device, held until the process ends), so sizes whose
  * isam_gru_forward_workspace_size exceeds 64 MiB are rejected with
- * ISAM_ERR_WORKSPACE (T = 64, batch 32, hidden 1024 needs about 28 MiB).  The
- * stepwise schedule launches its kernels one by one here (no graph is built).
+ * ISAM_ERR_WORKSPACE (T = 64, batch 32, hidden 1024 needs about 28 MiB).
  * Every call on one device shares that array: calls that overlap in time on
  * the same device race and must be serialised by the caller (one stream, or
  * events).  No hipMalloc, hipFree or allocating library call is made.

@@ -569,11 +569,9 @@ size_t isam_gru_forward_workspace_size(int64_t T, int64_t batch, int64_t input_s
 
 }  // extern "C"
 
-// Shared body of isam_gru_forward and isam_gru_forward_noalloc.  `workspace`
-// NULL with `scratch_fn` set: after validation, the workspace is the library's
-// static scratch (scratch_fn returns its address on the current device), and
-// the stepwise schedule launches its kernels directly instead of building a
-// graph, so nothing is allocated.
+// Shared body of isam_gru_forward and isam_gru_forward_noalloc.  With
+// no_alloc, the workspace is the library's static scratch on the current
+// device (looked up after validation), so nothing is allocated.
 static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
                                       int w_type, const void* x, const float* h0, const void* W,
                                       const void* U, const float* bias, const float* bias_hn,
@@ -637,16 +635,16 @@ static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_si
     int lds_max = 0;
     e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (e != hipSuccess) return hip_fail(e, who);
-    // Two schedules of the same step arithmetic: one persistent kernel with U
-    // resident in LDS and a grid barrier between steps, or one kernel per step
-    // replayed from a graph, which re-reads U from the memory-side cache every
-    // step (the L2 does not keep it across kernel boundaries) but pays no grid
-    // barrier.  Measured on MI355X (T = 64, I = 1024): the stepwise schedule
-    // is faster up to batch 16 while U is at most 16 MB (H = 1024 bf16: 257
-    // vs 369 us at batch 1, 326 vs 337 at 16; 391 vs 320 at 32), and up to
-    // batch 4 while U is at most 32 MB; the persistent one elsewhere.
-    // ISAM_GRU_MODE=persistent|steps overrides; the stepwise schedule also
-    // runs whenever the persistent kernel has no resident tiling.
+    // Three schedules.  The batch-group kernel below, where it applies; else
+    // one persistent kernel with U resident in LDS and a grid barrier between
+    // steps, or one kernel per step, which re-reads U from the memory-side
+    // cache every step (the L2 does not keep it across kernel boundaries) but
+    // pays no grid barrier.  Measured on MI355X (T = 64, I = 1024): the
+    // stepwise schedule is faster up to batch 16 while U is at most 16 MB
+    // (fp32 H = 1024 batch 4: 375 vs 508 us), and up to batch 4 while U is at
+    // most 32 MB (bf16 H = 2048 batch 4: 430 vs 511 us); the persistent one
+    // elsewhere.  ISAM_GRU_MODE=group|persistent|steps overrides; the stepwise
+    // schedule also runs whenever the persistent kernel has no resident tiling.
     const char* mode_env = getenv("ISAM_GRU_MODE");
     const double u_mb = 3.0 * (double)H * (double)H * (double)es / (1 << 20);
     bool step_mode = (batch <= 16 && u_mb <= 16.0) || (batch <= 4 && u_mb <= 32.0);
@@ -785,7 +783,7 @@ static isam_status_t gru_forward_impl(int64_t T, int64_t batch, int64_t input_si
             g.device_scope = 1;
         e = launch_gru_group(g, s);
     } else {
-        e = step_mode ? launch_gru_steps(g, hstate, s, /*use_graph=*/!no_alloc) : launch_gru_recurrent(g, s);
+        e = step_mode ? launch_gru_steps(g, hstate, s) : launch_gru_recurrent(g, s);
     }
     if (e != hipSuccess) return hip_fail(e, who);
     return ISAM_OK;

@@ -27,7 +27,6 @@
 #include <algorithm>
 #include <cstdlib>
 #include <mutex>
-#include <vector>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -508,8 +507,8 @@ __global__ __launch_bounds__(64 * kGWaves) void gru_group_kernel(GruArgs a) {
 }
 
 // Stepwise form of the same recurrence: the priming, recursive and finish
-// iterations as separate kernels, chained in a graph by the host (Section
-// 3.6's schedule with T fixed per call).  One launch per step t: every
+// iterations as separate kernels launched in order by the host (Section 3.6's
+// schedule with T fixed per call).  One launch per step t: every
 // workgroup reads its rows of U straight from global memory (they stay in
 // the L2 of its XCD from step to step), h_{t-1} in the operand type from ring
 // slot t and the fp32 state from hstate[t & 1]; it writes h_t to h_seq[t],
@@ -766,91 +765,18 @@ hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s) {
     return launch_gru_error_fill(a, s);
 }
 
-// Graph of the stepwise recurrence for one call signature: the state init
-// and T step kernels chained as kernel nodes (no stream capture), cached
-// per signature (sizes, tiling and every pointer) so a repeated call replays
-// the same graph with one launch.  The cache is small and guarded by a mutex.
-namespace {
-struct StepGraph {
-    GruArgs a;
-    float* hstate;
-    int dev;
-    hipGraphExec_t exec;
-    hipEvent_t done;  // recorded after every launch: an evicted graph is destroyed only once idle
-    uint64_t last_use;
-};
-std::mutex g_step_mu;
-std::vector<StepGraph> g_step_graphs;
-uint64_t g_step_use = 0;
-constexpr size_t kMaxStepGraphs = 32;
-
-bool same_call(const GruArgs& x, const GruArgs& y) {
-    return x.T == y.T && x.batch == y.batch && x.I == y.I && x.H == y.H && x.w_type == y.w_type &&
-           x.gx == y.gx && x.h0 == y.h0 && x.U == y.U && x.bias == y.bias && x.bias_hn == y.bias_hn &&
-           x.h_seq == y.h_seq && x.h_T == y.h_T && x.hbuf == y.hbuf && x.units_per_wg == y.units_per_wg &&
-           x.batch_per_wg == y.batch_per_wg && x.n_wg == y.n_wg;
-}
-
-int state_blocks(const GruArgs& a) {
+// Stepwise schedule: the state init and T step kernels launched in order on
+// the caller's stream (kernel boundaries order the steps).  The host enqueues
+// faster than the steps run (about 2.7 us of host time per launch against
+// 4-10 us per step), so no graph is built and the library keeps no state
+// between calls.
+static int state_blocks(const GruArgs& a) {
     const int64_t n = a.batch * a.H;
     int64_t b = (n + 255) / 256;
     return (int)(b > 1024 ? 1024 : (b < 1 ? 1 : b));
 }
 
-hipError_t build_step_graph(const GruArgs& a, float* hstate, hipGraphExec_t* out) {
-    const bool bf = a.w_type == kBF16;
-    const size_t red = (size_t)kWaves * gru_rows(a.units_per_wg) * kRedLd * sizeof(float);
-    hipGraph_t g = nullptr;
-    hipError_t e = hipGraphCreate(&g, 0);
-    if (e != hipSuccess) return e;
-    GruArgs args = a;
-    float* hs = hstate;
-    hipGraphNode_t prev = nullptr, node = nullptr;
-    {
-        void* params[] = {&args, &hs};
-        hipKernelNodeParams kp{};
-        kp.func = bf ? reinterpret_cast<void*>(gru_step_init_kernel<bf16_t>)
-                     : reinterpret_cast<void*>(gru_step_init_kernel<float>);
-        kp.gridDim = dim3(state_blocks(a));
-        kp.blockDim = dim3(256);
-        kp.sharedMemBytes = 0;
-        kp.kernelParams = params;
-        kp.extra = nullptr;
-        e = hipGraphAddKernelNode(&node, g, nullptr, 0, &kp);
-        prev = node;
-    }
-    const int mt = gru_rows(a.units_per_wg) / 16;
-    void* step_fn = nullptr;
-    switch (mt) {
-        case 1: step_fn = bf ? reinterpret_cast<void*>(gru_step_kernel<bf16_t, 1>) : reinterpret_cast<void*>(gru_step_kernel<float, 1>); break;
-        case 2: step_fn = bf ? reinterpret_cast<void*>(gru_step_kernel<bf16_t, 2>) : reinterpret_cast<void*>(gru_step_kernel<float, 2>); break;
-        case 3: step_fn = bf ? reinterpret_cast<void*>(gru_step_kernel<bf16_t, 3>) : reinterpret_cast<void*>(gru_step_kernel<float, 3>); break;
-        default: e = hipErrorInvalidValue;
-    }
-    for (int64_t t = 0; t < a.T && e == hipSuccess; ++t) {
-        int64_t tt = t;
-        void* params[] = {&args, &hs, &tt};
-        hipKernelNodeParams kp{};
-        kp.func = step_fn;
-        kp.gridDim = dim3(a.n_wg);
-        kp.blockDim = dim3(64 * kWaves);
-        kp.sharedMemBytes = (unsigned)red;
-        kp.kernelParams = params;
-        kp.extra = nullptr;
-        e = hipGraphAddKernelNode(&node, g, &prev, 1, &kp);
-        prev = node;
-    }
-    if (e == hipSuccess) e = hipGraphInstantiate(out, g, nullptr, nullptr, 0);
-    (void)hipGraphDestroy(g);
-    return e;
-}
-}  // namespace
-
-// Long sequences are launched step by step instead (a graph of T+1 nodes
-// costs host memory and build time in proportion to T).
-constexpr int64_t kMaxGraphSteps = 4096;
-
-static hipError_t launch_gru_steps_direct(const GruArgs& a, float* hstate, hipStream_t s) {
+hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s) {
     const bool bf = a.w_type == kBF16;
     const size_t red = (size_t)kWaves * gru_rows(a.units_per_wg) * kRedLd * sizeof(float);
     if (bf) hipLaunchKernelGGL(gru_step_init_kernel<bf16_t>, dim3(state_blocks(a)), dim3(256), 0, s, a, hstate);
@@ -877,44 +803,6 @@ static hipError_t launch_gru_steps_direct(const GruArgs& a, float* hstate, hipSt
         e = hipGetLastError();
     }
     return e;
-}
-
-hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s, bool use_graph) {
-    if (!use_graph || a.T > kMaxGraphSteps || getenv("ISAM_GRU_NO_GRAPH")) return launch_gru_steps_direct(a, hstate, s);
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    std::lock_guard<std::mutex> lock(g_step_mu);
-    StepGraph* hit = nullptr;
-    for (auto& c : g_step_graphs)
-        if (c.dev == dev && c.hstate == hstate && same_call(c.a, a)) hit = &c;
-    if (!hit) {
-        hipGraphExec_t exec = nullptr;
-        e = build_step_graph(a, hstate, &exec);
-        if (e != hipSuccess) return e;
-        hipEvent_t done = nullptr;
-        e = hipEventCreateWithFlags(&done, hipEventDisableTiming);
-        if (e != hipSuccess) {
-            (void)hipGraphExecDestroy(exec);
-            return e;
-        }
-        if (g_step_graphs.size() >= kMaxStepGraphs) {  // evict the least recently used
-            size_t lru = 0;
-            for (size_t i = 1; i < g_step_graphs.size(); ++i)
-                if (g_step_graphs[i].last_use < g_step_graphs[lru].last_use) lru = i;
-            StepGraph& old = g_step_graphs[lru];
-            (void)hipEventSynchronize(old.done);  // its last replay may still be running
-            (void)hipGraphExecDestroy(old.exec);
-            (void)hipEventDestroy(old.done);
-            g_step_graphs.erase(g_step_graphs.begin() + (long)lru);
-        }
-        g_step_graphs.push_back(StepGraph{a, hstate, dev, exec, done, 0});
-        hit = &g_step_graphs.back();
-    }
-    hit->last_use = ++g_step_use;
-    e = hipGraphLaunch(hit->exec, s);
-    if (e != hipSuccess) return e;
-    return hipEventRecord(hit->done, s);
 }
 
 // Workspace of isam_gru_forward_noalloc: a static device array, so that

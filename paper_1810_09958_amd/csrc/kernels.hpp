@@ -155,10 +155,9 @@ int gru_group_blocks_per_cu(int64_t H);
 hipError_t launch_gru_error_fill(const GruArgs& a, hipStream_t s);
 // Bound on one barrier wait of the persistent recurrence (2 s at 100 MHz).
 constexpr uint64_t kGruTimeoutTicks = 200000000ull;
-// Stepwise recurrence (state init + one kernel per step, replayed from a
-// cached graph, or launched one by one when use_graph is false); hstate is a
-// [2][batch][H] fp32 workspace.
-hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s, bool use_graph);
+// Stepwise recurrence (state init + one kernel per step, launched in order);
+// hstate is a [2][batch][H] fp32 workspace.
+hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s);
 // Static scratch of the allocation-free GRU entry point: its device address on
 // the current device (looked up once per device).
 constexpr size_t kGruScratchBytes = size_t(64) << 20;

@@ -18,8 +18,8 @@ import paper_1810_09958_amd as isam
 
 @pytest.fixture(params=["steps", "persistent", "default"])
 def mode(request, monkeypatch):
-    """The schedules of the recurrence: one kernel per step replayed from a graph, one
-    persistent kernel with a grid barrier between steps, and the library's own choice
+    """The schedules of the recurrence: one kernel per step, one persistent kernel with a
+    grid barrier between steps, and the library's own choice
     (the batch-group persistent kernel for bf16 weights and hidden 256..1024)."""
     if request.param == "default":
         monkeypatch.delenv("ISAM_GRU_MODE", raising=False)
@@ -139,7 +139,7 @@ def test_config_full_size_all_sequences(variant, mode):
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_paper_step_count_128(dt, mode):
     # 128 recurrent steps (the paper's sequence length): one persistent launch, or
-    # 128 step kernels in one graph
+    # 128 step kernels
     _run(128, 8, 128, 256, dt, seed=128, with_h0=True, scale=1 / 8)
 
 
@@ -162,10 +162,9 @@ def test_schedules_bit_identical(dt, monkeypatch):
     assert torch.equal(out["steps"][1], out["persistent"][1])
 
 
-def test_step_graph_replay_sees_new_inputs(monkeypatch):
-    # A repeated call with the same buffers replays the cached step graph; new
-    # input values written in place between calls must be used.
-    monkeypatch.setenv("ISAM_GRU_MODE", "steps")
+def test_repeated_calls_see_new_inputs(mode):
+    # Repeated calls on the same buffers: new input values written in place between calls
+    # must be used (nothing about a call is kept from one call to the next).
     T, B, I, H = 5, 4, 64, 256
     x1, W, U, b, _, _ = _inputs(T, B, I, H, seed=31, scale=1 / 8)
     x2 = synth.normal(32, 3, (T, B, I))
@@ -193,9 +192,9 @@ def test_hidden_too_large_for_lds_runs_stepwise(dt, monkeypatch):
     _run(3, 2, 64, H, dt, seed=5, with_h0=True, scale=1 / 64)
 
 
-def test_step_graph_cache_eviction(monkeypatch):
-    # More distinct call signatures than the graph cache holds (32): every call still
-    # matches the oracle, and a signature evicted earlier is rebuilt when it returns.
+def test_many_workspaces(monkeypatch):
+    # Calls on 38 workspace placements in a row on one stream (so they run one after the
+    # other), all queued before one sync: every result matches the oracle.
     monkeypatch.setenv("ISAM_GRU_MODE", "steps")
     T, B, I, H = 3, 2, 32, 64
     x, W, U, b, _, _ = _inputs(T, B, I, H, seed=41, scale=1 / 4)
@@ -214,28 +213,8 @@ def test_step_graph_cache_eviction(monkeypatch):
         assert err <= TOL_BF16, err
 
 
-@pytest.mark.parametrize("dt", ["bf16", "f32"])
-def test_step_kernels_without_graph_match(dt, monkeypatch):
-    # Sequences longer than the graph limit launch the step kernels one by one; the same
-    # kernels give the same bits either way (forced here with ISAM_GRU_NO_GRAPH).
-    monkeypatch.setenv("ISAM_GRU_MODE", "steps")
-    T, B, I, H = 6, 3, 48, 128
-    x, W, U, b, h0, _ = _inputs(T, B, I, H, seed=17, scale=1 / 4, with_h0=True)
-    if dt == "bf16":
-        x, W, U = bits(x), bits(W), bits(U)
-    args = [to_gpu(a) for a in (x, W, U)]
-    g_hs, g_hT = isam.gru_forward(*args, bias=to_gpu(b), h0=to_gpu(h0))
-    monkeypatch.setenv("ISAM_GRU_NO_GRAPH", "1")
-    d_hs, d_hT = isam.gru_forward(*args, bias=to_gpu(b), h0=to_gpu(h0))
-    torch.cuda.synchronize()
-    assert torch.equal(g_hs, d_hs) and torch.equal(g_hT, d_hT)
-    ref = oracle.gru(x, W, U, b, None, h0)
-    err = float(np.max(np.abs(d_hs.cpu().numpy().astype(np.float64) - ref)))
-    assert err <= (TOL_BF16 if dt == "bf16" else TOL_F32), err
-
-
-def test_long_sequence_beyond_graph_limit(monkeypatch):
-    # T = 4097 (> 4096 steps per graph): the step kernels are launched one by one.
+def test_long_sequence_stepwise(monkeypatch):
+    # T = 4097 steps of the stepwise schedule.
     monkeypatch.setenv("ISAM_GRU_MODE", "steps")
     T, B, I, H = 4097, 1, 16, 64
     x, W, U, b, h0, _ = _inputs(T, B, I, H, seed=23, scale=1 / 4, with_h0=True)
