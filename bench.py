@@ -18,7 +18,10 @@ large bf16 GEMMs (total FLOP / total time); GRU timesteps/s, separable-conv GB/s
 rest are reported under "components".  `roofline` covers the dominant kernel (the square
 bf16 GEMM, bf16 output); `cpu_baseline` times the CPU oracle on a bounded sample.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+After the timing, every configuration runs once more and is compared with the CPU oracle
+("parity": maximum normalised error, tolerance, pass/fail, oracle seconds and threads).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-parity]
 """
 from __future__ import annotations
 
@@ -46,6 +49,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parity", action="store_true", help="skip the per-configuration check against the oracle")
     ap.add_argument("--only", default="", help="comma list of component names to run (profiling)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="time plain device copies / fills of known size (HBM reference, counter scaling)")
@@ -406,7 +410,99 @@ def main():
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
+    if not args.no_parity:
+        out["parity"] = parity_per_config(isam, gpu)
     print(json.dumps(out), flush=True)
+
+
+def parity_per_config(isam, gpu):
+    """Each benchmark configuration once more through the library (the same launch
+    configuration the timing uses), against the CPU oracle: maximum normalised error
+    (|gpu - oracle| / sum|a||b|; for the GRU the absolute error of h, whose scale is 1),
+    the tolerance, pass/fail, what was compared, and the oracle's seconds on this host
+    (with the thread count).  The large GEMMs compare 256 rows x all columns; their full
+    oracle time is extrapolated from that sample."""
+    import torch
+    import oracle
+    from synth import workloads
+
+    threads = oracle.max_threads()
+    res = {}
+
+    def nerr(out, ref, S):
+        out = np.asarray(out, np.float64)
+        if not np.all(np.isfinite(out)):
+            return float("inf")
+        m = S > 0
+        e = float(np.max(np.abs(out - ref)[m] / S[m])) if np.any(m) else 0.0
+        if np.any(~m) and not np.array_equal(out[~m], ref[~m]):
+            e = float("inf")
+        return e
+
+    def record(name, err, tol, checked, t_oracle, scale=1.0):
+        res[name] = {"max_norm_err": err, "tol": tol, "pass": bool(err <= tol), "checked": checked,
+                     "oracle_s": round(t_oracle, 3), "cores": threads}
+        if scale != 1.0:
+            res[name]["oracle_full_s_extrapolated"] = round(t_oracle * scale, 1)
+
+    def host(t):
+        return t.detach().float().cpu().numpy().astype(np.float64)
+
+    # fp32 GEMM 128^3
+    d = workloads.gemm_small_fp32()
+    C = isam.gemm(gpu(d["A"]), gpu(d["B"]))
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    ref, S = oracle.gemm(d["A"], d["B"], 128, 128, 128)
+    record("gemm_128x128x128_f32", nerr(host(C), ref, S), 1e-5, "all elements", time.perf_counter() - t)
+    # skinny 4096 x 32 x 4096, bf16 and fp32
+    d = workloads.skinny()
+    for tag, A, B, tol in (("bf16", d["A_bf16"], d["B_bf16"], 1e-2), ("f32", d["A"], d["B"], 1e-5)):
+        C = isam.gemm(gpu(A), gpu(B))
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        ref, S = oracle.gemm(A, B, 4096, 32, 4096)
+        record(f"skinny_4096x32x4096_{tag}", nerr(host(C), ref, S), tol, "all elements", time.perf_counter() - t)
+    # GRU T64 B32 I=H=1024, bf16 weights
+    d = workloads.gru()
+    hs, _ = isam.gru_forward(gpu(d["x_bf16"]), gpu(d["W_bf16"]), gpu(d["U_bf16"]), bias=gpu(d["bias"]))
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    ref = oracle.gru(d["x_bf16"], d["W_bf16"], d["U_bf16"], d["bias"], None, None)
+    got = host(hs)
+    err = float(np.max(np.abs(got - ref))) if np.all(np.isfinite(got)) else float("inf")
+    record("gru_T64_B32_H1024_bf16", err, 1e-2, "every step of all 32 sequences (absolute error of h)",
+           time.perf_counter() - t)
+    # separable conv 32x56x56x128 -> 256
+    d = workloads.dwsep()
+    for tag, X, D, P, odt, tol in (("bf16_out_f32", d["X_bf16"], d["D_bf16"], d["P_bf16"], torch.float32, 1e-2),
+                                   ("bf16_out_bf16", d["X_bf16"], d["D_bf16"], d["P_bf16"], torch.bfloat16, 1e-2),
+                                   ("f32", d["X"], d["D"], d["P"], torch.float32, 1e-5)):
+        y = isam.dwsep_conv(gpu(X), gpu(D), gpu(P), out_dtype=odt)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        Z, S = oracle.dwsep(X, D, P)
+        record(f"dwsep_32x56x56x128_256_{tag}", nerr(host(y), Z, S), tol, "all elements", time.perf_counter() - t)
+    del d
+    # large bf16 GEMMs: 256 sampled rows (first and last included) x all columns
+    for tag, d in (("8192x8192x8192", workloads.gemm_square_bf16()), ("8192x1024x16384", workloads.gemm_rect_bf16())):
+        A_h, B_h = d["A_bf16"], d["B_bf16"]
+        M, K = A_h.shape
+        N = B_h.shape[1]
+        rows = workloads.rows_sample(M, 256)
+        Ag, Bg = gpu(A_h), gpu(B_h)
+        t = time.perf_counter()
+        ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), B_h, len(rows), N, K)
+        t_or = time.perf_counter() - t
+        idx = torch.as_tensor(rows, device=Ag.device)
+        for odt, otag in ((torch.bfloat16, "bf16"), (torch.float32, "f32")):
+            C = isam.gemm(Ag, Bg, out_dtype=odt)
+            torch.cuda.synchronize()
+            record(f"gemm_{tag}_bf16_out_{otag}", nerr(host(C[idx]), ref, S), 1e-2,
+                   f"{len(rows)} of {M} rows x all {N} columns", t_or, scale=M / len(rows))
+            del C
+        del Ag, Bg
+    return res
 
 
 def sources_hash(names) -> str:
