@@ -260,9 +260,14 @@ __global__ __launch_bounds__(64 * kSkWaves) void skinny_rows_kernel(GemmArgs a) 
         b_kr[q] = k;
         b_n[q] = blk * 16 + (pu & 1) * 8;
     }
-    auto issue = [&](int c) {  // chunk index relative to this wave
+    // Workgroups start their walk over the wave's chunks at different
+    // positions (rotation by workgroup index), so the 32 workgroups of an XCD
+    // do not all read the same lines of B from its L2 at the same moment.
+    const int rot = nc > 0 ? (int)((blockIdx.x >> 3) % (unsigned)nc) : 0;  // workgroups are dealt to 8 XCDs in turn
+    auto issue = [&](int c) {  // position c in this wave's walk
         char* st = ws + (c % kStreamStages) * kStage;
-        const int64_t k0 = (c_lo + c) * 64;
+        const int cc = c + rot < nc ? c + rot : c + rot - nc;
+        const int64_t k0 = (c_lo + cc) * 64;
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
             const int64_t k = k0 + a_k[q];
