@@ -24,15 +24,22 @@ _LIB = os.path.join(_HERE, "libisam_ref.so")
 F32, BF16 = 0, 1
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (OpenMP, -O2, no fast-math, no FP contraction)."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
-        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+_SAN_LIB = os.path.join(_HERE, "libisam_ref_san.so")
+
+
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (OpenMP, -O2, no fast-math, no FP contraction); with
+    sanitize, a separate copy under AddressSanitizer and UndefinedBehaviorSanitizer (load it
+    with gcc's libasan and libubsan preloaded and ISAM_REF_LIB pointing at it)."""
+    out = _SAN_LIB if sanitize else _LIB
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp"
+        san = ["-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer"] if sanitize else []
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", *san,
                "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
         subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB)
-    return _LIB
+        os.replace(tmp, out)
+    return out
 
 
 _lib = None
@@ -41,9 +48,10 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
+        path = os.environ.get("ISAM_REF_LIB") or _LIB
+        if path == _LIB and not os.path.exists(_LIB):
             build(force=False)
-        L = ctypes.CDLL(_LIB)
+        L = ctypes.CDLL(path)
         i64, vp, dp, fp = ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
         ci = ctypes.c_int
         L.isam_ref_gemm.argtypes = [ci, ci, i64, i64, i64, ci, vp, i64, vp, i64, dp, dp, dp, ci]

@@ -31,7 +31,8 @@ class IsamError(RuntimeError):
 
 
 def lib_path() -> str:
-    return os.path.join(HERE, "libisam.so")
+    """The in-tree libisam.so, or the file ISAM_LIB names (e.g. the sanitizer build)."""
+    return os.environ.get("ISAM_LIB") or os.path.join(HERE, "libisam.so")
 
 
 _lib = None

@@ -66,5 +66,32 @@ def build(jobs: int = 8, verbose: bool = False) -> str:
     return LIB
 
 
+SAN_LIB = os.path.join(BUILD, "libisam_san.so")
+
+
+def build_sanitized() -> str:
+    """A copy of the library whose host code (argument validation, planning and dispatch in
+    api.cpp) is built with g++ under AddressSanitizer and UndefinedBehaviorSanitizer, linked
+    with the device objects of the regular build.  For the CPU test tier: load it with gcc's
+    libasan and libubsan preloaded and ISAM_LIB pointing at it."""
+    if not all(os.path.exists(os.path.join(BUILD, src + ".o")) for src in SOURCES):
+        build()
+    obj = os.path.join(BUILD, "api.cpp.san.o")
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(hipcc())))
+    san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer"]
+    subprocess.run(["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-D__HIP_PLATFORM_AMD__",
+                    "-I", os.path.join(rocm, "include"), "-I", os.path.join(HERE, "..", "include"), *san,
+                    "-c", os.path.join(CSRC, "api.cpp"), "-o", obj], check=True)
+    objs = [obj] + [os.path.join(BUILD, src + ".o") for src in SOURCES if src != "api.cpp"]
+    tmp = SAN_LIB + ".tmp"
+    subprocess.run(["g++", "-shared", "-o", tmp, *objs, "-L", os.path.join(rocm, "lib"),
+                    "-Wl,-rpath," + os.path.join(rocm, "lib"), "-lamdhip64", *san], check=True)
+    os.replace(tmp, SAN_LIB)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--sanitized" in sys.argv:
+        print(build_sanitized())
+    else:
+        print(build(verbose="-v" in sys.argv))
