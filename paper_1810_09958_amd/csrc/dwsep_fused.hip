@@ -112,7 +112,8 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
                                                                    int64_t C_out, int n_slots, int row_instr) {
     extern __shared__ __attribute__((aligned(1024))) char smem[];
     constexpr int UPW = C / (8 * NP);  // 16-byte channel units per producer wave
-    constexpr int CPP = 64 / UPW;    // columns per producer pass
+    constexpr int SLOTS = 64 / UPW;  // column runs per producer wave (lanes per channel unit)
+    constexpr int CPL = kFPix / SLOTS;  // columns per run: SLOTS * CPL = 64 >= W, one pass
     constexpr int KS = C / 16;       // MFMA K steps
     constexpr int kA = a_tile_bytes<C>();
     const int W = (int)d.W, H = (int)d.H;
@@ -133,8 +134,9 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
     const bool producer = wid < NP;
     const int pw4 = producer ? wid : wid - NP;  // producer index / consumer index
 
-    // Producer lane: channel unit ug (8 channels) of columns jl, jl + CPP, ...
-    // Its taps are fixed: (di, 0) and (di, 1) paired as bf16x2, (di, 2) fp32.
+    // Producer lane: channel unit ug (8 channels) of the CPL adjacent columns
+    // jl*CPL .. jl*CPL + CPL-1.  Its taps are fixed: (di, 0) and (di, 1)
+    // paired as bf16x2, (di, 2) fp32.
     const int ul = lane % UPW, jl = lane / UPW, ug = pw4 * UPW + ul;
     uint32_t w01[3][8];
     float w2[3][8];
@@ -202,7 +204,9 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
         for (int di = 0; di < 3; ++di)
 #pragma unroll
             for (int c = 0; c < 8; ++c) asm volatile("" : : "v"(w01[di][c]), "v"(w2[di][c]));
-        while (nx_tile < n_local && issued < n_slots) issue_row();
+        // Only the next tile's rows now: every workgroup requests its first
+        // rows at the same moment, and a shorter burst lands them sooner.
+        while (nx_tile < n_local && issued < min(n_slots, 2 * R + 2)) issue_row();
     } else {
         // Stage this wave's P slice [C][64] (columns past C_out read as zero),
         // then read its fragments; no other wave touches this staging area.
@@ -254,28 +258,32 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
                 if (sl >= n_slots) sl -= n_slots;
                 rowp[k] = ring + sl * slot_bytes;
             }
-            // Column passes of CPP columns each.
-            uint4 v[R + 2][3];
-            auto load_pass = [&](int cp, uint4 (&dst)[R + 2][3]) {
-                // columns j-1 .. j+1 sit at units (j + dj) * UPW (the halo
-                // makes every read unconditional); idle lanes read column W-1
-                const int j = min(cp * CPP + jl, W - 1);
+            // One pass: the lane reads columns j0-1 .. j0+CPL of each of the
+            // R+2 rows (the halo columns make every read unconditional; a run
+            // past the image reads column W-1 and is not stored), all reads
+            // in flight at once, then computes its CPL x R outputs: each
+            // loaded column serves up to three outputs instead of being read
+            // once per output.
+            const int j0 = jl * CPL;
+            uint4 v[R + 2][CPL + 2];
 #pragma unroll
-                for (int k = 0; k < R + 2; ++k)
+            for (int k = 0; k < R + 2; ++k)
 #pragma unroll
-                    for (int dj = 0; dj < 3; ++dj)
-                        dst[k][dj] = *reinterpret_cast<const uint4*>(rowp[k] + ((j + dj) * UPW + ul) * 16);
-            };
-            auto compute_pass = [&](int cp, const uint4 (&src)[R + 2][3]) {
-                const int j = cp * CPP + jl;
-                if (j >= W) return;
+                for (int dj = 0; dj < CPL + 2; ++dj) {
+                    const int x = min(j0 + dj, W + 1);  // unit column x holds image column x-1
+                    v[k][dj] = *reinterpret_cast<const uint4*>(rowp[k] + (x * UPW + ul) * 16);
+                }
+#pragma unroll
+            for (int cl = 0; cl < CPL; ++cl) {
+                const int j = j0 + cl;
+                if (j >= W) break;
                 uint32_t pr[R + 2][8];  // per row: (x=j-1, x=j) pairs per channel
                 float sg[R + 2][8];     // per row: x=j+1 per channel
 #pragma unroll
                 for (int k = 0; k < R + 2; ++k) {
-                    const uint32_t b0[4] = {src[k][0].x, src[k][0].y, src[k][0].z, src[k][0].w},
-                                   b1[4] = {src[k][1].x, src[k][1].y, src[k][1].z, src[k][1].w},
-                                   b2[4] = {src[k][2].x, src[k][2].y, src[k][2].z, src[k][2].w};
+                    const uint4 c0 = v[k][cl], c1 = v[k][cl + 1], c2 = v[k][cl + 2];
+                    const uint32_t b0[4] = {c0.x, c0.y, c0.z, c0.w}, b1[4] = {c1.x, c1.y, c1.z, c1.w},
+                                   b2[4] = {c2.x, c2.y, c2.z, c2.w};
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         pr[k][2 * q] = __builtin_amdgcn_perm(b1[q], b0[q], 0x05040100u);
@@ -302,10 +310,6 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
                         make_uint4(f_pack_bf16(acc[0], acc[1]), f_pack_bf16(acc[2], acc[3]),
                                    f_pack_bf16(acc[4], acc[5]), f_pack_bf16(acc[6], acc[7]));
                 }
-            };
-            for (int cp = 0; cp * CPP < W; ++cp) {
-                load_pass(cp, v);
-                compute_pass(cp, v);
             }
             f_lds_wait();
             f_barrier();  // A tile t complete
@@ -340,6 +344,47 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
             const int img = tg / tiles_per_img, i0 = (tg % tiles_per_img) * R;
             const int valid_px = min(R, H - i0) * W;
             const int64_t m0 = ((int64_t)img * H + i0) * W;
+            // Output through the wave's part of the P staging area (free
+            // after the prologue), 32 pixels at a time: a pixel's 64 channels
+            // of this wave are one contiguous piece of the output row (128
+            // bytes bf16, 256 fp32), so every store instruction writes whole
+            // pieces instead of 32 scattered 8- or 16-byte ones.  16-byte chunk
+            // c of staged pixel p sits at chunk c ^ (p & (CH-1)).
+            constexpr int RB = 64 * (int)sizeof(TO), CH = RB / 16;
+            constexpr bool kStaged = 32 * RB * kConsumers <= 2 * kA;
+            if constexpr (kStaged) {
+                char* stg = sT + cb * (32 * RB);
+                static_for<2>([&](auto jjc) {
+                    constexpr int jj = decltype(jjc)::value;
+                    const int p = lane & 31;
+                    static_for<2>([&](auto ic) {
+                        constexpr int i = decltype(ic)::value;
+                        static_for<4>([&](auto v4c) {
+                            constexpr int v4 = decltype(v4c)::value;
+                            const int byte = (i * 32 + 8 * v4 + 4 * (lane >> 5)) * (int)sizeof(TO);
+                            char* dst = stg + p * RB + ((((byte >> 4) ^ (p & (CH - 1)))) << 4) + (byte & 15);
+                            const float x0 = acc[i][jj][4 * v4], x1 = acc[i][jj][4 * v4 + 1];
+                            const float x2 = acc[i][jj][4 * v4 + 2], x3 = acc[i][jj][4 * v4 + 3];
+                            if constexpr (sizeof(TO) == 4)
+                                *reinterpret_cast<float4*>(dst) = make_float4(x0, x1, x2, x3);
+                            else
+                                *reinterpret_cast<uint2*>(dst) = make_uint2(f_pack_bf16(x0, x1), f_pack_bf16(x2, x3));
+                        });
+                    });
+                    f_lds_wait();  // this wave's staging writes before its reads (no other wave uses the area)
+#pragma unroll
+                    for (int r = 0; r < 32 * CH / 64; ++r) {
+                        const int q = r * 64 + lane, pp = q / CH, c = q % CH;
+                        const uint4 val = *reinterpret_cast<const uint4*>(stg + pp * RB + ((c ^ (pp & (CH - 1))) << 4));
+                        const int px = jj * 32 + pp;
+                        const int64_t co = cb * 64 + c * (16 / (int)sizeof(TO));
+                        const bool ok = px < valid_px && co < C_out;
+                        const int64_t idx = (m0 + px) * C_out + co;
+                        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, val), rsO,
+                                                               ok ? (int)(idx * (int64_t)sizeof(TO)) : (int)kOob, 0, 0);
+                    }
+                });
+            } else
             static_for<2>([&](auto i) {
                 static_for<2>([&](auto jj) {
                     static_for<4>([&](auto v4c) {
