@@ -17,7 +17,10 @@ GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves, bool k_full) 
         }
     }
     switch (tile) {
-        case kTile256x256: return trans_b ? gemm_dma_kernel<256, 256, true> : gemm_dma_kernel<256, 256, false>;
+        case kTile256x256:
+            if (k_full)
+                return trans_b ? gemm_dma_kernel<256, 256, true, 2, 2, true> : gemm_dma_kernel<256, 256, false, 2, 2, true>;
+            return trans_b ? gemm_dma_kernel<256, 256, true> : gemm_dma_kernel<256, 256, false>;
         case kTile256x128: return trans_b ? gemm_dma_kernel<256, 128, true> : gemm_dma_kernel<256, 128, false>;
         case kTile128x128:
             if (k_full)

@@ -137,13 +137,15 @@ struct DmaCopier {
     }
     // Copies of a K tile wholly inside K: offset = base + the tile's delta
     // (k0 * 2 bytes for A and K-contiguous B, k0 * ldb * 2 for N-contiguous B).
+    // live == false (a K tile past the last one): every lane reads past the
+    // buffer end, so the copy moves zeros and touches no memory.
     template <int Q>
-    __device__ __forceinline__ void a_part_full(uint32_t delta, uint32_t dst) const {
-        dma16(rsA, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * A_INSTR + Q) * 1024)), a_base[Q] + delta);
+    __device__ __forceinline__ void a_part_full(uint32_t delta, uint32_t dst, bool live = true) const {
+        dma16(rsA, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * A_INSTR + Q) * 1024)), live ? a_base[Q] + delta : kOob);
     }
     template <int Q>
-    __device__ __forceinline__ void b_part_full(uint32_t delta, uint32_t dst) const {
-        dma16(rsB, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * B_INSTR + Q) * 1024)), b_base[Q] + delta);
+    __device__ __forceinline__ void b_part_full(uint32_t delta, uint32_t dst, bool live = true) const {
+        dma16(rsB, __builtin_amdgcn_readfirstlane(dst + (uint32_t)((wid * B_INSTR + Q) * 1024)), live ? b_base[Q] + delta : kOob);
     }
     // A copy instruction Q of the K tile starting at k0 into the A region at
     // LDS address `dst` (a wave-uniform 32-bit LDS address, so no generic-
@@ -204,84 +206,6 @@ __device__ __forceinline__ void read_frag_part(Frag<MI, NI>& f, const char* sa, 
     }
 }
 
-// Accumulators of the wave's WTM x WTN tile -> C (or the split-K partial
-// sums), staged through LDS so every store is a 16-byte (fp32) or 8-byte
-// (bf16) vector store.  `smem` must hold NW * 32 * (WTN*4 + 16) bytes and be
-// idle (no copies in flight).
-template <int MI, int NI, int WTM, int WTN, int NW>
-__device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc)[MI][NI], char* smem, int64_t m0,
-                                               int64_t n0, int wm, int wn, int wid, int lane) {
-    const bool split_out = gridDim.y > 1;
-    const int split = blockIdx.y;
-    constexpr int EPI_LD = WTN * 4 + 16;
-    char* epi = smem + wid * 32 * EPI_LD;
-    float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
-    const int64_t ldo = split_out ? a.N : a.ldc;
-    const int osz = split_out ? 4 : (a.c_type == kF32 ? 4 : 2);
-    char* obase = split_out ? reinterpret_cast<char*>(P) : static_cast<char*>(a.C);
-    const bool vec_out = ((reinterpret_cast<uintptr_t>(obase) & 15) == 0) && ((ldo * osz) % 16 == 0);
-    constexpr int Q = WTN / 4;
-    static_for<MI>([&](auto i) {
-        static_for<NI>([&](auto j) {
-            static_for<16>([&](auto v) {
-                constexpr int vv = decltype(v)::value;
-                const int r = 8 * (vv >> 2) + 4 * (lane >> 5) + (vv & 3);
-                *reinterpret_cast<float*>(epi + r * EPI_LD + (j * 32 + (lane & 31)) * 4) = acc[i][j][vv];
-            });
-        });
-        __syncthreads();
-        const int64_t row0 = m0 + wm * WTM + i * 32;
-        const int64_t col0 = n0 + wn * WTN;
-        for (int q = lane; q < 32 * Q; q += 64) {
-            const int r = q / Q, c4 = q - r * Q;
-            const int64_t row = row0 + r, col = col0 + c4 * 4;
-            if (row >= a.M || col >= a.N) continue;
-            float4 v4 = *reinterpret_cast<const float4*>(epi + r * EPI_LD + c4 * 16);
-            float vals[4] = {v4.x, v4.y, v4.z, v4.w};
-            const int nv = (int)((a.N - col) < 4 ? (a.N - col) : 4);
-            if (!split_out && a.bias) {
-                for (int e = 0; e < nv; ++e) vals[e] += a.bias[col + e];
-            }
-            const int64_t idx = row * ldo + col;
-            if (split_out || a.c_type == kF32) {
-                float* C = reinterpret_cast<float*>(obase);
-                if (nv == 4 && vec_out) {
-                    if (!split_out && a.accumulate) {
-                        float4 c = *reinterpret_cast<const float4*>(C + idx);
-                        vals[0] += c.x; vals[1] += c.y; vals[2] += c.z; vals[3] += c.w;
-                    }
-                    *reinterpret_cast<float4*>(C + idx) = make_float4(vals[0], vals[1], vals[2], vals[3]);
-                } else {
-                    for (int e = 0; e < nv; ++e) {
-                        float val = vals[e];
-                        if (!split_out && a.accumulate) val += C[idx + e];
-                        C[idx + e] = val;
-                    }
-                }
-            } else {
-                uint16_t* C = reinterpret_cast<uint16_t*>(obase);
-                if (nv == 4 && ((reinterpret_cast<uintptr_t>(C + idx) & 7) == 0)) {
-                    if (a.accumulate) {
-                        uint2 c = *reinterpret_cast<const uint2*>(C + idx);
-                        vals[0] += bf16lo(c.x); vals[1] += bf16hi(c.x);
-                        vals[2] += bf16lo(c.y); vals[3] += bf16hi(c.y);
-                    }
-                    *reinterpret_cast<uint2*>(C + idx) =
-                        make_uint2(pack_bf16x2(vals[0], vals[1]), pack_bf16x2(vals[2], vals[3]));
-                } else {
-                    for (int e = 0; e < nv; ++e) {
-                        float val = vals[e];
-                        if (a.accumulate) val += bf16_to_f32(C[idx + e]);
-                        C[idx + e] = (uint16_t)f32_to_bf16(val);
-                    }
-                }
-            }
-        }
-        __syncthreads();
-    });
-}
-
-
 // Two-stage kernel, any tile shape of the table.  Per K tile t (stage t & 1),
 // four 16-deep K steps:
 //   ks 0..2: MFMAs of step ks, reads of step ks+1 (alternating fragment sets)
@@ -318,8 +242,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
 
     // Copy instruction Q of K tile `tile` (A first, then B) into its stage.
     // Copies are issued without a branch: those of a K tile past the last one
-    // read nothing (every offset is out of range) and land in the idle sink
-    // block -- in the last iteration their stage may still be being read.
+    // read nothing (every offset is out of range, so no memory is touched) and
+    // land in the idle sink block -- in the last iteration their stage may
+    // still be being read.
     const uint32_t smem_base = lds_addr_of(smem);
     auto issue_part = [&](int tile, auto q_c) {
         constexpr int q = decltype(q_c)::value;
@@ -327,10 +252,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
         const int64_t k0 = kbeg + (int64_t)tile * BK;
         const uint32_t sb = tile < nk ? sa + (uint32_t)A_BYTES : sa;
         if constexpr (KFULL) {
-            // past the last tile the offsets may land anywhere inside the
-            // buffers or past them: the bytes go to the sink
-            if constexpr (q < A_INSTR) cp.template a_part_full<q>((uint32_t)(k0 * 2), sa);
-            else cp.template b_part_full<q - A_INSTR>((uint32_t)(TB ? k0 * 2 : k0 * a.ldb * 2), sb);
+            const bool live = tile < nk;
+            if constexpr (q < A_INSTR) cp.template a_part_full<q>((uint32_t)(k0 * 2), sa, live);
+            else cp.template b_part_full<q - A_INSTR>((uint32_t)(TB ? k0 * 2 : k0 * a.ldb * 2), sb, live);
         } else {
             if constexpr (q < A_INSTR) cp.template a_part<q>(k0, sa);
             else cp.template b_part<q - A_INSTR>(k0, sb);
@@ -417,5 +341,6 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     __syncthreads();
     store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, lane);
 }
+
 
 }  // namespace isam

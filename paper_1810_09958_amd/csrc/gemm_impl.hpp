@@ -165,6 +165,143 @@ __device__ __forceinline__ void gemm_batch_offset(GemmArgs& a) {
     }
 }
 
+// Accumulators of the wave's WTM x WTN tile -> C (or the split-K partial
+// sums), staged through LDS so every store is a 16-byte (fp32) or 8-byte
+// (bf16) vector store.  `smem` must hold NW * 32 * (WTN*4 + 16) bytes and be
+// idle (no copies in flight).
+template <int MI, int NI, int WTM, int WTN, int NW>
+__device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc)[MI][NI], char* smem, int64_t m0,
+                                               int64_t n0, int wm, int wn, int wid, int lane) {
+    const bool split_out = gridDim.y > 1;
+    const int split = blockIdx.y;
+    constexpr int EPI_LD = WTN * 4 + 16;
+    char* epi = smem + wid * 32 * EPI_LD;
+    float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
+    const int64_t ldo = split_out ? a.N : a.ldc;
+    const int osz = split_out ? 4 : (a.c_type == kF32 ? 4 : 2);
+    char* obase = split_out ? reinterpret_cast<char*>(P) : static_cast<char*>(a.C);
+    const bool vec_out = ((reinterpret_cast<uintptr_t>(obase) & 15) == 0) && ((ldo * osz) % 16 == 0);
+    constexpr int Q = WTN / 4;
+    // Fast path for slabs wholly inside C: lane l owns the 4-column group l % Q
+    // and rows l / Q + RPI * it, so every address is a fixed per-lane base
+    // plus a constant step and no element is range-checked.
+    constexpr int RPI = 64 / Q, IT = 32 / RPI;
+    static_assert(64 % Q == 0 && 32 % RPI == 0, "wave tile width must divide into 4-column groups per lane");
+    const bool out_f32 = split_out || a.c_type == kF32;
+    const bool add_c = !split_out && a.accumulate;
+    const int64_t col0 = n0 + wn * WTN;
+    const bool cols_ok = col0 + WTN <= a.N &&
+                         (out_f32 ? vec_out
+                                  : ((reinterpret_cast<uintptr_t>(obase) & 7) == 0 && (ldo * 2) % 8 == 0));
+    const int rl = lane / Q, c4l = lane % Q;
+    float4 bias4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (cols_ok && !split_out && a.bias) {
+        const float* bp = a.bias + col0 + 4 * c4l;
+        bias4 = make_float4(bp[0], bp[1], bp[2], bp[3]);
+    }
+    auto slab_fast = [&](int64_t row0, auto f32_c, auto addc_c) {
+        constexpr bool F32 = decltype(f32_c)::value, ADDC = decltype(addc_c)::value;
+        const char* src = epi + rl * EPI_LD + c4l * 16;
+        char* dst = obase + ((row0 + rl) * ldo + col0 + 4 * c4l) * (F32 ? 4 : 2);
+        const int64_t step = (int64_t)RPI * ldo * (F32 ? 4 : 2);
+        static_for<IT>([&](auto it_c) {
+            constexpr int it = decltype(it_c)::value;
+            float4 v = *reinterpret_cast<const float4*>(src + it * RPI * EPI_LD);
+            v.x += bias4.x; v.y += bias4.y; v.z += bias4.z; v.w += bias4.w;
+            char* d = dst + it * step;
+            if constexpr (F32) {
+                if constexpr (ADDC) {
+                    const float4 c = *reinterpret_cast<const float4*>(d);
+                    v.x = c.x + v.x; v.y = c.y + v.y; v.z = c.z + v.z; v.w = c.w + v.w;
+                }
+                *reinterpret_cast<float4*>(d) = v;
+            } else {
+                if constexpr (ADDC) {
+                    const uint2 c = *reinterpret_cast<const uint2*>(d);
+                    v.x = bf16lo(c.x) + v.x; v.y = bf16hi(c.x) + v.y;
+                    v.z = bf16lo(c.y) + v.z; v.w = bf16hi(c.y) + v.w;
+                }
+                *reinterpret_cast<uint2*>(d) = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+            }
+        });
+    };
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) {
+                constexpr int vv = decltype(v)::value;
+                const int r = 8 * (vv >> 2) + 4 * (lane >> 5) + (vv & 3);
+                *reinterpret_cast<float*>(epi + r * EPI_LD + (j * 32 + (lane & 31)) * 4) = acc[i][j][vv];
+            });
+        });
+        // The staging rows belong to this wave alone and one wave's LDS
+        // accesses are performed in order, so no workgroup barrier is needed
+        // here or after the stores below (a barrier's fence would also make
+        // the wave wait for its global stores to reach memory, slab by slab).
+        asm volatile("" : : : "memory");
+        const int64_t row0 = m0 + wm * WTM + i * 32;
+        if (cols_ok && row0 + 32 <= a.M) {
+            using T_ = std::true_type;
+            using F_ = std::false_type;
+            if (out_f32) {
+                if (add_c) slab_fast(row0, T_{}, T_{});
+                else slab_fast(row0, T_{}, F_{});
+            } else {
+                if (add_c) slab_fast(row0, F_{}, T_{});
+                else slab_fast(row0, F_{}, F_{});
+            }
+            asm volatile("" : : : "memory");
+            return;
+        }
+        for (int q = lane; q < 32 * Q; q += 64) {
+            const int r = q / Q, c4 = q - r * Q;
+            const int64_t row = row0 + r, col = col0 + c4 * 4;
+            if (row >= a.M || col >= a.N) continue;
+            float4 v4 = *reinterpret_cast<const float4*>(epi + r * EPI_LD + c4 * 16);
+            float vals[4] = {v4.x, v4.y, v4.z, v4.w};
+            const int nv = (int)((a.N - col) < 4 ? (a.N - col) : 4);
+            if (!split_out && a.bias) {
+                for (int e = 0; e < nv; ++e) vals[e] += a.bias[col + e];
+            }
+            const int64_t idx = row * ldo + col;
+            if (split_out || a.c_type == kF32) {
+                float* C = reinterpret_cast<float*>(obase);
+                if (nv == 4 && vec_out) {
+                    if (!split_out && a.accumulate) {
+                        float4 c = *reinterpret_cast<const float4*>(C + idx);
+                        vals[0] += c.x; vals[1] += c.y; vals[2] += c.z; vals[3] += c.w;
+                    }
+                    *reinterpret_cast<float4*>(C + idx) = make_float4(vals[0], vals[1], vals[2], vals[3]);
+                } else {
+                    for (int e = 0; e < nv; ++e) {
+                        float val = vals[e];
+                        if (!split_out && a.accumulate) val += C[idx + e];
+                        C[idx + e] = val;
+                    }
+                }
+            } else {
+                uint16_t* C = reinterpret_cast<uint16_t*>(obase);
+                if (nv == 4 && ((reinterpret_cast<uintptr_t>(C + idx) & 7) == 0)) {
+                    if (a.accumulate) {
+                        uint2 c = *reinterpret_cast<const uint2*>(C + idx);
+                        vals[0] += bf16lo(c.x); vals[1] += bf16hi(c.x);
+                        vals[2] += bf16lo(c.y); vals[3] += bf16hi(c.y);
+                    }
+                    *reinterpret_cast<uint2*>(C + idx) =
+                        make_uint2(pack_bf16x2(vals[0], vals[1]), pack_bf16x2(vals[2], vals[3]));
+                } else {
+                    for (int e = 0; e < nv; ++e) {
+                        float val = vals[e];
+                        if (a.accumulate) val += bf16_to_f32(C[idx + e]);
+                        C[idx + e] = (uint16_t)f32_to_bf16(val);
+                    }
+                }
+            }
+        }
+        asm volatile("" : : : "memory");
+    });
+}
+
+
 template <typename T, int BM, int BN, int WM, int WN, bool TA, bool TB, bool VEC>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, TileMapArgs tmap) {
     gemm_batch_offset(a);
@@ -244,78 +381,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_tile_kernel(GemmArgs a, Til
         }
     }
 
-    // Epilogue, one 32-row slab of the wave tile at a time: the accumulators
-    // (element v of lane l is row 8*(v/4) + 4*(l/32) + v%4, column l%32 of a
-    // 32x32 block) go to a per-wave LDS buffer, then each lane reads 4
-    // consecutive columns back and writes them with one vector store.
-    const bool split_out = gridDim.y > 1;
-    constexpr int EPI_LD = WTN * 4 + 16;  // bytes per staged row (padding spreads banks)
-    static_assert(4 * 32 * EPI_LD <= 2 * STAGE, "epilogue staging must fit in LDS");
-    char* epi = smem + wid * 32 * EPI_LD;
-    float* P = split_out ? a.partial + (int64_t)split * a.M * a.N : nullptr;
-    const int64_t ldo = split_out ? a.N : a.ldc;
-    const int osz = split_out ? 4 : (a.c_type == kF32 ? 4 : 2);
-    char* obase = split_out ? reinterpret_cast<char*>(P) : static_cast<char*>(a.C);
-    const bool vec_out = ((reinterpret_cast<uintptr_t>(obase) & 15) == 0) && ((ldo * osz) % 16 == 0);
-    constexpr int Q = WTN / 4;  // float4 groups per staged row
-    static_for<MI>([&](auto i) {
-        static_for<NI>([&](auto j) {
-            static_for<16>([&](auto v) {
-                constexpr int vv = decltype(v)::value;
-                const int r = 8 * (vv >> 2) + 4 * (lane >> 5) + (vv & 3);
-                *reinterpret_cast<float*>(epi + r * EPI_LD + (j * 32 + (lane & 31)) * 4) = acc[i][j][vv];
-            });
-        });
-        __syncthreads();
-        const int64_t row0 = m0 + wm * WTM + i * 32;
-        const int64_t col0 = n0 + wn * WTN;
-        for (int q = lane; q < 32 * Q; q += 64) {
-            const int r = q / Q, c4 = q - r * Q;
-            const int64_t row = row0 + r, col = col0 + c4 * 4;
-            if (row >= a.M || col >= a.N) continue;
-            float4 v4 = *reinterpret_cast<const float4*>(epi + r * EPI_LD + c4 * 16);
-            float vals[4] = {v4.x, v4.y, v4.z, v4.w};
-            const int nv = (int)((a.N - col) < 4 ? (a.N - col) : 4);
-            if (!split_out && a.bias) {
-                for (int e = 0; e < nv; ++e) vals[e] += a.bias[col + e];
-            }
-            const int64_t idx = row * ldo + col;
-            if (split_out || a.c_type == kF32) {
-                float* C = reinterpret_cast<float*>(obase);
-                if (nv == 4 && vec_out) {
-                    if (!split_out && a.accumulate) {
-                        float4 c = *reinterpret_cast<const float4*>(C + idx);
-                        vals[0] += c.x; vals[1] += c.y; vals[2] += c.z; vals[3] += c.w;
-                    }
-                    *reinterpret_cast<float4*>(C + idx) = make_float4(vals[0], vals[1], vals[2], vals[3]);
-                } else {
-                    for (int e = 0; e < nv; ++e) {
-                        float val = vals[e];
-                        if (!split_out && a.accumulate) val += C[idx + e];
-                        C[idx + e] = val;
-                    }
-                }
-            } else {
-                uint16_t* C = reinterpret_cast<uint16_t*>(obase);
-                if (nv == 4 && ((reinterpret_cast<uintptr_t>(C + idx) & 7) == 0)) {
-                    if (a.accumulate) {
-                        uint2 c = *reinterpret_cast<const uint2*>(C + idx);
-                        vals[0] += bf16lo(c.x); vals[1] += bf16hi(c.x);
-                        vals[2] += bf16lo(c.y); vals[3] += bf16hi(c.y);
-                    }
-                    *reinterpret_cast<uint2*>(C + idx) =
-                        make_uint2(pack_bf16x2(vals[0], vals[1]), pack_bf16x2(vals[2], vals[3]));
-                } else {
-                    for (int e = 0; e < nv; ++e) {
-                        float val = vals[e];
-                        if (a.accumulate) val += bf16_to_f32(C[idx + e]);
-                        C[idx + e] = (uint16_t)f32_to_bf16(val);
-                    }
-                }
-            }
-        }
-        __syncthreads();
-    });
+    // Epilogue: the accumulators go to C (or the split-K partial sums)
+    // through a per-wave LDS buffer, one 32-row slab at a time.
+    static_assert(WM * WN * 32 * (WTN * 4 + 16) <= 2 * STAGE, "epilogue staging must fit in LDS");
+    store_acc_tile<MI, NI, WTM, WTN, WM * WN>(a, acc, smem, m0, n0, wm, wn, wid, lane);
 }
 
 // Function table for one element type: [tile][trans_a][trans_b][vec].
