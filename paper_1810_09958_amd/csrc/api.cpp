@@ -200,6 +200,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
             p.k_per_split = cdiv(cdiv(K, sp), bk) * bk;
             p.k_splits = (int)cdiv(K, p.k_per_split);
         }
+
     } else if (K <= 2048 && tiles(kTile128x128) >= cus) {
         // Shallow K: the 128x128 grid (measured, bf16 NT, K = 1024: 2048x3072
         // 24 us against 27 for 128x64; 4096x3072 39 us against 55 for 256x128,
@@ -247,11 +248,23 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
             if (p.k_splits == 1) p.k_per_split = K;
         }
     }
+    // Two K slices of 256x256 tiles whose workgroups t and t + tiles land on
+    // one XCD (workgroups are dealt to the XCDs in turn, 32 CUs each): the
+    // second slice sums the pair through that XCD's L2, with no reduction
+    // pass.  ISAM_GEMM_CONFIG fixup=0 keeps the pass.
+    const int xcds = cus % 32 == 0 ? cus / 32 : 1;
+    if (p.k_splits == 2 && p.tile == kTile256x256 && tiles(kTile256x256) % xcds == 0) p.fixup = 1;
+    if (const char* env = getenv("ISAM_GEMM_CONFIG"))
+        if (strstr(env, "fixup=0")) p.fixup = 0;
     return p;
 }
 
 size_t gemm_ws_bytes(const GemmPlan& p, int64_t M, int64_t N) {
-    return p.k_splits > 1 ? (size_t)p.k_splits * (size_t)M * (size_t)N * sizeof(float) : 0;
+    if (p.k_splits <= 1) return 0;
+    // room for the reduction pass's partials, and (two-slice plans that may
+    // sum inside the kernel) for the per-tile partials and flags
+    const size_t red = (size_t)p.k_splits * (size_t)M * (size_t)N * sizeof(float);
+    return p.fixup ? std::max(red, gemm_fixup_ws_bytes(M, N)) : red;
 }
 
 bool vec_ok(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type, const void* A,

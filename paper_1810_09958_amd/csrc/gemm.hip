@@ -2,11 +2,18 @@
 // partials in a fixed order.
 #include "gemm_impl.hpp"
 
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <atomic>
+#include <random>
+
 namespace isam {
 
 GemmKernelFn gemm_kernel_bf16(int tile, int ta, int tb, int vec);
 GemmKernelFn gemm_kernel_f32(int tile, int ta, int tb, int vec);
 GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves, bool k_full);
+GemmKernelFn gemm_dma_fixup_kernel_for(int trans_b);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk) {
     static const int dims[kTileCount][2] = {{256, 256}, {256, 128}, {128, 128},
@@ -16,7 +23,22 @@ void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk) {
     *bk = ab_type == kBF16 ? 64 : 32;
 }
 
+size_t gemm_fixup_ws_bytes(int64_t M, int64_t N) {
+    const size_t tiles = (size_t)((M + 255) / 256) * (size_t)((N + 255) / 256);
+    return tiles * (256 * 256 * 4) + tiles * 128;
+}
+
 namespace {
+// Epochs of in-kernel split sums: a random 64-bit start (so a workspace's
+// stale flags cannot match by accident) and then one value per launch.
+uint64_t next_fixup_epoch() {
+    static std::atomic<uint64_t> next{[] {
+        std::random_device rd;
+        return ((uint64_t)rd() << 32) ^ (uint64_t)rd();
+    }()};
+    return next.fetch_add(1, std::memory_order_relaxed);
+}
+
 // C = (accumulate ? C : 0) + bias + sum over splits s = 0, 1, ... of P[s].
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a, int splits) {
     const int64_t total = a.M * a.N;
@@ -109,12 +131,18 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     tile_dims(p.tile, a.ab_type, &bm, &bn, &bk);
     GemmKernelFn fn = nullptr;
     int threads = 256;
+    bool fixup = false;
     if (p.dma && a.ab_type == kBF16 && !a.trans_a && p.vec) {
         // every K slice a whole number of 64-deep tiles: copies with base + delta offsets
         const bool k_full = a.K % 64 == 0 && (p.k_splits <= 1 || p.k_per_split % 64 == 0);
         fn = gemm_dma_kernel_for(p.tile, a.trans_b, p.dma_waves, k_full);
         if (fn && p.dma_waves == 8 && (p.tile == kTile256x256 || p.tile == kTile256x128)) threads = 512;
         else fn = gemm_dma_kernel_for(p.tile, a.trans_b, 4, k_full);
+        // Two K slices of 256x256 tiles: slice 1 adds slice 0's partial sums
+        // itself (the plan has checked that both slices of a tile share an XCD).
+        fixup = p.fixup && p.k_splits == 2 && k_full && threads == 512 && p.tile == kTile256x256 &&
+                ((uintptr_t)a.partial & 255) == 0;
+        if (fixup) fn = gemm_dma_fixup_kernel_for(a.trans_b);
     }
     if (!fn)
         fn = a.ab_type == kBF16 ? gemm_kernel_bf16(p.tile, a.trans_a, a.trans_b, p.vec)
@@ -127,12 +155,21 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     t.xcd_remap = p.xcd_remap;
     t.k_per_split = p.k_splits > 1 ? p.k_per_split : a.K;
     if (t.k_per_split <= 0) t.k_per_split = 1;
+    t.fixup = fixup ? 1 : 0;
+    t.epoch = fixup ? next_fixup_epoch() : 0;
+    t.flags = fixup ? reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.partial) +
+                                                   (size_t)t.tiles_m * t.tiles_n * (256 * 256 * 4))
+                    : nullptr;
     dim3 grid((unsigned)(t.tiles_m * t.tiles_n), (unsigned)(p.k_splits > 1 ? p.k_splits : 1),
               (unsigned)(a.batch > 1 ? a.batch : 1));
     dim3 block(threads);
+    if (fixup) {
+        const char* v = getenv("ISAM_LOG");
+        if (v && *v && *v != '0') fprintf(stderr, "[isam] two K slices summed in the kernel\n");
+    }
     hipLaunchKernelGGL(fn, grid, block, 0, s, a, t);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.k_splits <= 1) return e;
+    if (e != hipSuccess || p.k_splits <= 1 || fixup) return e;
     return launch_splitk_reduce(a, p.k_splits, s);
 }
 

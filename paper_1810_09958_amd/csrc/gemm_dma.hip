@@ -4,6 +4,12 @@
 
 namespace isam {
 
+// 256x256 tiles, 8 waves, K slices of whole 64-deep tiles, two slices summed
+// inside the kernel.
+GemmKernelFn gemm_dma_fixup_kernel_for(int trans_b) {
+    return trans_b ? gemm_dma_kernel<256, 256, true, 2, 4, true, true> : gemm_dma_kernel<256, 256, false, 2, 4, true, true>;
+}
+
 GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves, bool k_full) {
     if (waves == 8) {
         switch (tile) {

@@ -215,7 +215,7 @@ __device__ __forceinline__ void read_frag_part(Frag<MI, NI>& f, const char* sa, 
 //            t+2 into stage t & 1
 // KFULL: every K slice is a whole number of 64-deep tiles, so the copies take
 // their offsets as base + delta (one add per copy instead of the range checks).
-template <int BM, int BN, bool TB, int WM = 2, int WN = 2, bool KFULL = false>
+template <int BM, int BN, bool TB, int WM = 2, int WN = 2, bool KFULL = false, bool FIX = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
     gemm_batch_offset(a);
     constexpr int NW = WM * WN, STAGES = 2, BK = 64;
@@ -338,8 +338,79 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
         }
     }
+    if constexpr (FIX) {
+        // In-kernel sum of two K slices (tmap.fixup is set for this instance).  Both slices of a tile run on one XCD
+        // (the host enables this only when they do), so the exchange goes
+        // through that XCD's L2: stores and flag with workgroup-scope
+        // write-through of L1, loads that bypass L1.  Each wave's accumulators
+        // travel in register order (16-byte pieces, lane-contiguous).
+        constexpr uint32_t TILE_BYTES = (uint32_t)BM * BN * 4;
+        const __amdgpu_buffer_rsrc_t rp =
+            make_rsrc(reinterpret_cast<char*>(a.partial) + (size_t)blockIdx.x * TILE_BYTES, TILE_BYTES);
+        const __amdgpu_buffer_rsrc_t rf = make_rsrc(tmap.flags + (size_t)blockIdx.x * 16, 128);
+        auto piece_off = [&](int i, int j, int c) {
+            return (uint32_t)((((wid * MI + i) * NI + j) * 4 + c) * 1024 + lane * 16);
+        };
+        if (blockIdx.y == 0) {
+            static_for<MI>([&](auto i) {
+                static_for<NI>([&](auto j) {
+                    static_for<4>([&](auto c) {
+                        constexpr int cc = decltype(c)::value;
+                        const f32x16_t& v = acc[decltype(i)::value][decltype(j)::value];
+                        const i32x4_t w = __builtin_bit_cast(i32x4_t, f32x4_t{v[4 * cc], v[4 * cc + 1], v[4 * cc + 2], v[4 * cc + 3]});
+                        __builtin_amdgcn_raw_buffer_store_b128(w, rp, (int)piece_off(i, j, cc), 0, 1);
+                    });
+                });
+            });
+            vm_wait<0>();  // this wave's pieces are in L2
+            __syncthreads();
+            if (tid == 0) {
+                const uint2 e = make_uint2((uint32_t)tmap.epoch, (uint32_t)(tmap.epoch >> 32));
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) int, e), rf, 0, 0, 1);
+            }
+            return;
+        }
+        // slice 1: wait for slice 0's flag (bounded; on timeout the tile becomes NaN)
+        int* ok = reinterpret_cast<int*>(smem);
+        __syncthreads();  // every wave is done with the stages
+        if (tid == 0) {
+            const uint64_t t0 = wall_clock64();
+            int good = 0;
+            for (;;) {
+                const auto v = __builtin_amdgcn_raw_buffer_load_b64(rf, 0, 0, 17);
+                const uint64_t got = (uint64_t)(uint32_t)v[0] | ((uint64_t)(uint32_t)v[1] << 32);
+                if (got == tmap.epoch) { good = 1; break; }
+                if (wall_clock64() - t0 > kFixupTimeoutTicks) break;
+                __builtin_amdgcn_s_sleep(2);
+            }
+            *ok = good;
+        }
+        __syncthreads();
+        if (__builtin_amdgcn_readfirstlane(*ok) != 0) {
+            static_for<MI>([&](auto i) {
+                static_for<NI>([&](auto j) {
+                    f32x16_t& v = acc[decltype(i)::value][decltype(j)::value];
+                    static_for<4>([&](auto c) {
+                        constexpr int cc = decltype(c)::value;
+                        const f32x4_t p = __builtin_bit_cast(
+                            f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, (int)piece_off(i, j, cc), 0, 17));
+                        v[4 * cc] = p[0] + v[4 * cc];
+                        v[4 * cc + 1] = p[1] + v[4 * cc + 1];
+                        v[4 * cc + 2] = p[2] + v[4 * cc + 2];
+                        v[4 * cc + 3] = p[3] + v[4 * cc + 3];
+                    });
+                });
+            });
+        } else {
+            static_for<MI>([&](auto i) {
+                static_for<NI>([&](auto j) {
+                    static_for<16>([&](auto v) { acc[decltype(i)::value][decltype(j)::value][decltype(v)::value] = __builtin_nanf(""); });
+                });
+            });
+        }
+    }
     __syncthreads();
-    store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, lane);
+    store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, lane, FIX);
 }
 
 

@@ -140,6 +140,13 @@ struct TileLoader {
 struct TileMapArgs {
     int tiles_m, tiles_n, group_m, xcd_remap;
     int64_t k_per_split;
+    // Two K slices summed inside the kernel (256x256 direct-to-LDS kernel
+    // only): slice 0 leaves its accumulators in `partial` and raises
+    // flags[tile] (one 128-byte line per tile) to `epoch`; slice 1 adds them
+    // and writes C.
+    int fixup;
+    uint64_t epoch;
+    uint64_t* flags;
 };
 
 __device__ __forceinline__ void map_tile(const TileMapArgs& t, int& tm, int& tn) {
@@ -171,8 +178,8 @@ __device__ __forceinline__ void gemm_batch_offset(GemmArgs& a) {
 // idle (no copies in flight).
 template <int MI, int NI, int WTM, int WTN, int NW>
 __device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc)[MI][NI], char* smem, int64_t m0,
-                                               int64_t n0, int wm, int wn, int wid, int lane) {
-    const bool split_out = gridDim.y > 1;
+                                               int64_t n0, int wm, int wn, int wid, int lane, bool fixup = false) {
+    const bool split_out = gridDim.y > 1 && !fixup;
     const int split = blockIdx.y;
     constexpr int EPI_LD = WTN * 4 + 16;
     char* epi = smem + wid * 32 * EPI_LD;

@@ -50,6 +50,7 @@ struct GemmPlan {
     int xcd_remap;   // spread consecutive tiles of one group over one XCD
     int dma;         // 1: direct-to-LDS kernel where it applies (bf16, A K-contiguous, vec)
     int dma_waves;   // 4 or 8 waves per workgroup for the direct-to-LDS kernel
+    int fixup;       // 1: a two-slice split on 256x256 tiles may sum its slices inside the kernel
     int skinny;      // 1: streaming kernel for N <= 32 (k_splits = K slices of skinny_k_slice);
                      // 2: bf16 row-streaming kernel (16 rows per workgroup, whole K, no split);
                      // 4: narrow dot-product kernel (N < 8, not a multiple of the vector width)
@@ -155,6 +156,11 @@ int gru_group_blocks_per_cu(int64_t H);
 hipError_t launch_gru_error_fill(const GruArgs& a, hipStream_t s);
 // Bound on one barrier wait of the persistent recurrence (2 s at 100 MHz).
 constexpr uint64_t kGruTimeoutTicks = 200000000ull;
+// Bounded wait of a GEMM tile's second K slice for the first (100 MHz ticks).
+constexpr uint64_t kFixupTimeoutTicks = 200000000ull;
+// Workspace of a two-slice split summed inside the kernel: one 256x256 fp32
+// tile of partial sums per output tile, then one 128-byte flag line per tile.
+size_t gemm_fixup_ws_bytes(int64_t M, int64_t N);
 // Stepwise recurrence (state init + one kernel per step, launched in order);
 // hstate is a [2][batch][H] fp32 workspace.
 hipError_t launch_gru_steps(const GruArgs& a, float* hstate, hipStream_t s);

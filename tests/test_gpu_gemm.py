@@ -177,6 +177,26 @@ def test_config_large_bf16_every_element(which):
 # 128x128; B K-contiguous (NT) and N-contiguous (NN); K a multiple of the 64-deep tile (copy
 # offsets as base + per-tile delta) and with a ragged last tile; fp32 and bf16 output;
 # unsplit and split into two K slices (partial sums + fixed-order reduction).
+# Two K slices of 256x256 tiles summed inside the kernel (slice 1 adds slice 0's partial
+# sums, exchanged through the L2 of the XCD both share): tile counts that are multiples of
+# 8 (the condition for the in-kernel sum), ragged M and N, both B layouts, both output
+# types, accumulate, repeated calls on one workspace; K with a ragged last tile takes the
+# reduction pass instead.  Every element against the oracle.
+@pytest.mark.parametrize("shape,in_kernel", [((512, 1024, 1280), True), ((500, 1000, 1280), True),
+                                             ((512, 1024, 1200), False)])
+@pytest.mark.parametrize("tb", [0, 1])
+def test_split_sum_in_kernel_every_element(shape, in_kernel, tb, monkeypatch, capfd):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,dmaw=8,splits=2")
+    monkeypatch.setenv("ISAM_LOG", "1")
+    M, N, K = shape
+    for rep in range(2):
+        for ct in ("f32", "bf16"):
+            _run_case(M, N, K, "bf16", ct, tb=tb, seed=M + K + tb + rep)
+    _run_case(M, N, K, "bf16", "f32", tb=tb, accumulate=True, seed=M + K + 7)
+    log = capfd.readouterr().err
+    assert ("two K slices summed in the kernel" in log) == in_kernel
+
+
 DMA_INSTANCES = [("0", "8"), ("0", "4"), ("1", "8"), ("1", "4"), ("2", "4")]
 
 
@@ -221,8 +241,8 @@ def _guarded_gemm(M, N, K, dt, ct, pad_cols, seed, tb=0, env=None, monkeypatch=N
     assert norm_err(body[:, :N].astype(np.float64), ref, S) <= tol
 
 
-GUARD_CASES = ["dma256", "dma256_split", "dma128", "skinny_rows", "skinny_split", "narrow", "stream",
-               "tile_f32", "small"]
+GUARD_CASES = ["dma256", "dma256_split", "dma256_split_sum", "dma128", "skinny_rows", "skinny_split", "narrow",
+               "stream", "tile_f32", "small"]
 
 
 @pytest.mark.parametrize("ct", ["f32", "bf16"])
@@ -235,6 +255,7 @@ def test_guard_bands_every_kernel(ct, case, monkeypatch):
     cases = {
         "dma256": dict(M=520, N=776, K=640, dt="bf16", env="tile=0,dma=1,dmaw=8"),
         "dma256_split": dict(M=520, N=776, K=640, dt="bf16", env="tile=0,dma=1,dmaw=8,splits=2"),
+        "dma256_split_sum": dict(M=500, N=1000, K=1280, dt="bf16", env="tile=0,dma=1,dmaw=8,splits=2"),
         "dma128": dict(M=520, N=776, K=600, dt="bf16", env="tile=2,dma=1"),
         "skinny_rows": dict(M=4100, N=32, K=1000, dt="bf16", env=None),
         "skinny_split": dict(M=300, N=24, K=6000, dt="f32", env=None),
