@@ -25,7 +25,9 @@
  *   - Entry points are thread-safe.  The library keeps no state between
  *     calls other than per-device caches filled once and never changed: CU
  *     count, LDS size, and the address of the static scratch that
- *     isam_gru_forward_noalloc uses.
+ *     isam_gru_forward_noalloc uses; and one process-wide 64-bit counter
+ *     (random start) that gives each in-kernel split-K sum of isam_gemm its
+ *     own flag value.
  */
 #ifndef ISAM_H
 #define ISAM_H
@@ -64,7 +66,15 @@ typedef enum {
  * M == 0 or N == 0: no-op.  K == 0: C = 0 (accumulate = 0) or unchanged.
  * workspace: device buffer of at least isam_gemm_workspace_size(...) bytes,
  * used for split-K partial sums; with a smaller (or NULL) workspace the call
- * still succeeds on a plan without split-K.
+ * still succeeds on a plan without split-K.  Deep products split along K into
+ * two slices on 256x256 tiles sum the slices inside the kernel when both
+ * slices of every tile run on one XCD (tile count a multiple of the XCD
+ * count, K a multiple of 64, workspace 256-byte aligned): the second slice
+ * waits for the first's flag in the workspace (a bounded wait; if it ever
+ * expires the tile's outputs are NaN) and adds its partial sums in a fixed
+ * order, so results stay deterministic.  Other split plans sum the slices
+ * in a second kernel.  The workspace needs no initial contents; concurrent
+ * calls must not share one.
  */
 isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                         int ab_type, const void* A, int64_t lda, const void* B, int64_t ldb,
