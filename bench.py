@@ -10,7 +10,9 @@ HBM:
   * 1D convolution 32 sequences x 1024 positions, 512 -> 512 channels, 5 taps, bf16 (fp32 out)
   * fp32 GEMM 128^3
 Each part is bracketed by HIP events on the stream the library launches on (torch's current
-stream), so the per-part times are device times.  The HBM-bound parts (skinny GEMM, GRU,
+stream), so the per-part times are device times; after the timed steps each part also runs
+alone, calls queued back to back between two events ("us_b2b": device time per call without
+the per-call event and launch gaps, which dominate the small parts).  The HBM-bound parts (skinny GEMM, GRU,
 separable conv) rotate over enough input copies that every call reads from HBM rather than
 the 256 MB memory-side cache; the same call on one warm buffer set is reported beside it as
 "<name>_mall_warm".  `value` is the GEMM throughput of the
@@ -335,6 +337,29 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    # Back to back: each part alone, R calls queued between two events (rotated parts keep
+    # rotating), so the figure is the device time per call without the per-call event and
+    # launch gaps of the step -- the rate a stream of such calls sustains.
+    b2b = {}
+    for i, (name, fn, info) in enumerate(comps):
+        saved = {k: os.environ.get(k) for k in info.get("env", {})}
+        os.environ.update(info.get("env", {}))
+        per_call_s = max(1e-6, float(np.mean([events[k][i][0].elapsed_time(events[k][i][1]) for k in range(K)])) * 1e-3)
+        R = int(min(200, max(10, 5e-3 / per_call_s)))
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(R):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        b2b[name] = (e0.elapsed_time(e1) * 1e3 / R, R)
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
     results = {}
     for i, (name, _, info) in enumerate(comps):
         ms = [events[k][i][0].elapsed_time(events[k][i][1]) for k in range(K)]
@@ -353,6 +378,15 @@ def main():
             r["frac_f32_peak"] = round(tfl / PEAK_F32_TFLOPS, 6)
         elif info["kind"] in ("skinny", "dwsep"):
             r["frac_hbm_peak"] = round(gbs / PEAK_HBM_GBPS, 4)
+        us_b, R = b2b[name]
+        r["us_b2b"] = round(us_b, 2)
+        r["b2b_calls"] = R
+        if info["kind"] in ("gemm_bf16", "gemm_bf16_ctx"):
+            r["frac_bf16_peak_b2b"] = round(info["flop"] / (us_b * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)
+        elif info["kind"] in ("skinny", "dwsep"):
+            r["frac_hbm_peak_b2b"] = round(info["bytes"] / (us_b * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4)
+        elif info["kind"] == "gru":
+            r["timesteps_per_s_b2b"] = round(info["steps"] / (us_b * 1e-6), 1)
         if info.get("rotation_sets", 1) > 1:
             r["rotation_sets"] = info["rotation_sets"]
         if info["kind"] == "gru":
