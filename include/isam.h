@@ -145,11 +145,13 @@ size_t isam_dwsep_conv_workspace_size(int64_t batch, int64_t H, int64_t W, int64
  *   - stepwise: the priming, recursive and finish iterations as separate
  *     kernels, one per step, launched in order (no co-residency needed, so
  *     any hidden size that meets the multiple rule is supported).
- * The persistent and stepwise schedules give the same values bit for bit.  A
- * persistent barrier wait that exceeds 2 s (never, for a launch whose
- * workgroups are all resident, as cooperative launches guarantee) ends the
- * recurrence early and fills h_seq and h_T with NaN.  Calls on one workspace
- * must not overlap in time.
+ * The persistent and stepwise schedules give the same values bit for bit.
+ * The batch-group and persistent schedules launch no more workgroups than
+ * the device holds at once, as an ordinary kernel, and need all of them
+ * resident: a barrier wait that exceeds 2 s (never on a device with no other
+ * work; possible if work on other streams -- another persistent GRU call,
+ * say -- keeps CUs occupied that long) ends the recurrence early and fills
+ * h_seq and h_T with NaN.  Calls on one workspace must not overlap in time.
  */
 isam_status_t isam_gru_forward(int64_t T, int64_t batch, int64_t input_size, int64_t hidden_size,
                                int w_type, const void* x, const float* h0, const void* W,

@@ -22,8 +22,14 @@
 //   n = tanh(Gx_n + b_n + r * ((U_n h) + b_hn)),  h' = (1 - z) n + z h.
 // The U_n h product is complete before it is scaled by r.
 //
-// All workgroups must be co-resident (cooperative launch); every barrier
-// wait is bounded and raises an error flag instead of spinning forever.
+// All workgroups must be co-resident.  The host launches no more of them
+// than the device holds at once (occupancy query), as an ordinary kernel: on
+// a device with nothing else running every workgroup is then resident from
+// the start (a cooperative launch would guarantee it even beside other work,
+// but costs about 17 us of extra gaps around the kernel).  Every barrier
+// wait is bounded and raises an error flag instead of spinning forever, so a
+// launch that shares the device with work that holds CUs for longer ends
+// with NaN outputs rather than a hang.
 #include <algorithm>
 #include <cstdlib>
 #include <mutex>
@@ -715,7 +721,7 @@ hipError_t launch_gru_group(const GruArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     GruArgs args = a;
     void* params[] = {&args};
-    e = hipLaunchCooperativeKernel(fn, dim3(a.n_wg), dim3(64 * kGWaves), params, (unsigned)lds, s);
+    e = hipLaunchKernel(fn, dim3(a.n_wg), dim3(64 * kGWaves), params, (unsigned)lds, s);
     if (e != hipSuccess) return e;
     return launch_gru_error_fill(a, s);
 }
@@ -760,7 +766,7 @@ hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     GruArgs args = a;
     void* params[] = {&args};
-    e = hipLaunchCooperativeKernel(fn, dim3(a.n_wg), dim3(64 * kWaves), params, (unsigned)lds, s);
+    e = hipLaunchKernel(fn, dim3(a.n_wg), dim3(64 * kWaves), params, (unsigned)lds, s);
     if (e != hipSuccess) return e;
     return launch_gru_error_fill(a, s);
 }
