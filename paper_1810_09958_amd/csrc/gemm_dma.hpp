@@ -230,7 +230,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     constexpr int SINK = 1024 * (A_INSTR > Copier::B_INSTR ? A_INSTR : Copier::B_INSTR) * NW;
     __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE + SINK];
 
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform: the copies' LDS destinations are then scalar values
+    const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wid / WN, wn = wid % WN;
     int tm, tn;
     map_tile(tmap, tm, tn);
