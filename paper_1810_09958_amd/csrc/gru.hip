@@ -687,8 +687,10 @@ hipError_t launch_gru_copy_state(const float* h0, float* h_T, int64_t n, hipStre
 
 hipError_t launch_gru_error_fill(const GruArgs& a, hipStream_t s) {
     const int64_t n_seq = a.h_seq ? a.T * a.batch * a.H : 0, n_T = a.h_T ? a.batch * a.H : 0;
+    // A few workgroups: the common case only reads the error word (a large grid costs
+    // about 2 us more to dispatch); the fill itself is the rare path.
     int blocks = (int)((std::max(n_seq, n_T) + 255) / 256);
-    blocks = blocks > 1024 ? 1024 : (blocks < 1 ? 1 : blocks);
+    blocks = blocks > 8 ? 8 : (blocks < 1 ? 1 : blocks);
     hipLaunchKernelGGL(gru_error_fill_kernel, dim3(blocks), dim3(256), 0, s, a.sync, a.h_seq, n_seq, a.h_T, n_T);
     return hipGetLastError();
 }
