@@ -157,6 +157,14 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     if (t.k_per_split <= 0) t.k_per_split = 1;
     t.fixup = fixup ? 1 : 0;
     t.epoch = fixup ? next_fixup_epoch() : 0;
+    t.expect = t.epoch;
+    t.wait_ticks = kFixupTimeoutTicks;
+    // Test hook: the second slice waits for a value the first never writes, under a 1 ms
+    // bound, so every tile of the product comes back as NaN.
+    if (const char* v = getenv("ISAM_GEMM_TEST_FIXUP_STALL"); fixup && v && v[0] == '1') {
+        t.expect = t.epoch + 1;
+        t.wait_ticks = 100000;
+    }
     t.flags = fixup ? reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.partial) +
                                                    (size_t)t.tiles_m * t.tiles_n * (256 * 256 * 4))
                     : nullptr;

@@ -381,8 +381,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             for (;;) {
                 const auto v = __builtin_amdgcn_raw_buffer_load_b64(rf, 0, 0, 17);
                 const uint64_t got = (uint64_t)(uint32_t)v[0] | ((uint64_t)(uint32_t)v[1] << 32);
-                if (got == tmap.epoch) { good = 1; break; }
-                if (wall_clock64() - t0 > kFixupTimeoutTicks) break;
+                if (got == tmap.expect) { good = 1; break; }
+                if (wall_clock64() - t0 > tmap.wait_ticks) break;
                 __builtin_amdgcn_s_sleep(2);
             }
             *ok = good;

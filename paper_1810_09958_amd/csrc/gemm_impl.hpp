@@ -145,7 +145,9 @@ struct TileMapArgs {
     // flags[tile] (one 128-byte line per tile) to `epoch`; slice 1 adds them
     // and writes C.
     int fixup;
-    uint64_t epoch;
+    uint64_t epoch;          // value slice 0 writes
+    uint64_t expect;         // value slice 1 waits for (== epoch but in the timeout test)
+    uint64_t wait_ticks;     // bound of slice 1's wait (100 MHz ticks)
     uint64_t* flags;
 };
 

@@ -197,6 +197,27 @@ def test_split_sum_in_kernel_every_element(shape, in_kernel, tb, monkeypatch, ca
     assert ("two K slices summed in the kernel" in log) == in_kernel
 
 
+def test_split_sum_in_kernel_timeout_gives_nan(monkeypatch):
+    # The second slice's wait for the first is bounded; the host forces it to expire (the
+    # slice waits for a flag value that is never written, under a 1 ms bound): every output is
+    # NaN, and the next call on the same workspace is correct again.
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,dmaw=8,splits=2")
+    M, N, K = 512, 1024, 1280
+    A_h = bits(synth.uniform(3, 10, (M, K), -1, 1))
+    B_h = bits(synth.uniform(3, 11, (K, N), -1, 1))
+    A, B = to_gpu(A_h), to_gpu(B_h)
+    ws = torch.empty(isam.gemm_workspace_size(M, N, K, 1, 0), device="cuda", dtype=torch.uint8)
+    monkeypatch.setenv("ISAM_GEMM_TEST_FIXUP_STALL", "1")
+    C = isam.gemm(A, B, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.all(torch.isnan(C)).item()
+    monkeypatch.delenv("ISAM_GEMM_TEST_FIXUP_STALL")
+    C = isam.gemm(A, B, workspace=ws)
+    torch.cuda.synchronize()
+    ref, S = oracle.gemm(A_h, B_h, M, N, K)
+    assert norm_err(to_host_f64(C), ref, S) <= TOL_BF16
+
+
 DMA_INSTANCES = [("0", "8"), ("0", "4"), ("1", "8"), ("1", "4"), ("2", "4")]
 
 
