@@ -146,7 +146,7 @@ _LARGE_REF = {}
 
 def _large_ref(which):
     """Oracle result and normaliser of a whole large bf16 product, computed once per module
-    (about 20 s for 8192^3 on the GPU machine's host cores)."""
+    (about 20 s for 8192^3 on 16 host cores)."""
     if which not in _LARGE_REF:
         _LARGE_REF.clear()   # hold one (2 x 512 MiB for 8192^2) at a time
         d = workloads.gemm_square_bf16() if which == "square" else workloads.gemm_rect_bf16()
