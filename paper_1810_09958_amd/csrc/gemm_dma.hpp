@@ -206,6 +206,104 @@ __device__ __forceinline__ void read_frag_part(Frag<MI, NI>& f, const char* sa, 
     }
 }
 
+// Main loop of the three-stage-B ring (see the kernel's comment): A stages at
+// LDS offsets 0 and A_BYTES, B stages at 2*A_BYTES + s*B_BYTES, s = 0..2.
+template <int BM, int BN, bool TB, int WM, int WN, int MI, int NI, typename Copier>
+__device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* smem, uint32_t smem_base, const Copier& cp,
+                                                const GemmArgs& a, int64_t kbeg, int nk, int wm, int wn, int lane) {
+    constexpr int BK = 64, A_BYTES = BM * 128, B_BYTES = BN * 128;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    const uint32_t bbase = smem_base + (uint32_t)(2 * A_BYTES);
+    auto copy_a = [&](int tt, auto q_c) {
+        const int64_t k0 = kbeg + (int64_t)tt * BK;
+        cp.template a_part_full<decltype(q_c)::value>((uint32_t)(k0 * 2), smem_base + (uint32_t)((tt & 1) * A_BYTES), tt < nk);
+    };
+    auto copy_b = [&](int tt, int bst, auto q_c) {
+        const int64_t k0 = kbeg + (int64_t)tt * BK;
+        cp.template b_part_full<decltype(q_c)::value>((uint32_t)(TB ? k0 * 2 : k0 * a.ldb * 2),
+                                                      bbase + (uint32_t)(bst * B_BYTES), tt < nk);
+    };
+    using F = Frag<MI, NI>;
+    constexpr int N_READS = MI + NI * (TB ? 1 : 2);
+    auto read_part = [&](F& f, int ast, int bst, int ks, auto idx_c) {
+        read_frag_part<decltype(idx_c)::value, MI, NI, TB, BN>(f, smem + ast * A_BYTES, smem + 2 * A_BYTES + bst * B_BYTES,
+                                                               ks, wm * WTM, wn * WTN, lane);
+    };
+    // MFMAs of f, with the reads of step ks (stages ast / bst) into g and then
+    // the copies CK (0: none; 1: B q 0-1, 2: B q 2, 3: B q 3 of tile t+2 into
+    // B stage b2; 4: A q 0-3 of tile t+2) spread over the MFMA slots.
+    auto step = [&](const F& f, F& g, int ast, int bst, int ks, auto ck_c, int t, int b2) {
+        constexpr int CK = decltype(ck_c)::value;
+        constexpr int NC = CK == 0 ? 0 : CK == 1 ? 2 : CK == 4 ? 4 : 1;
+        static_for<MI * NI>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            mfma32_bf16(acc[k / NI][k % NI], f.a[k / NI], f.b[k % NI]);
+            constexpr int SL = MI * NI, NOPS = N_READS + NC;
+            constexpr int lo = (k * NOPS + SL - 1) / SL, hi = ((k + 1) * NOPS + SL - 1) / SL;
+            static_for<hi - lo>([&](auto d) {
+                constexpr int o = lo + decltype(d)::value;
+                if constexpr (o < N_READS) {
+                    read_part(g, ast, bst, ks, std::integral_constant<int, o>{});
+                } else {
+                    constexpr int c = o - N_READS;
+                    if constexpr (CK == 1) copy_b(t + 2, b2, std::integral_constant<int, c>{});
+                    if constexpr (CK == 2) copy_b(t + 2, b2, std::integral_constant<int, 2>{});
+                    if constexpr (CK == 3) copy_b(t + 2, b2, std::integral_constant<int, 3>{});
+                    if constexpr (CK == 4) copy_a(t + 2, std::integral_constant<int, c>{});
+                }
+            });
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+    using C0 = std::integral_constant<int, 0>;
+    using C1 = std::integral_constant<int, 1>;
+    using C2 = std::integral_constant<int, 2>;
+    using C3 = std::integral_constant<int, 3>;
+    using C4 = std::integral_constant<int, 4>;
+
+    // tiles 0 and 1 whole (tile 1 reads nothing when nk == 1), then wait for tile 0
+    static_for<4>([&](auto q) { copy_a(0, q); });
+    static_for<4>([&](auto q) { copy_b(0, 0, q); });
+    static_for<4>([&](auto q) { copy_a(1, q); });
+    static_for<4>([&](auto q) { copy_b(1, 1, q); });
+    vm_wait<8>();
+    block_sync();
+    F f0, f1;
+    static_for<N_READS>([&](auto idx) { read_part(f0, 0, 0, 0, idx); });
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    int b0 = 0, b1 = 1, b2 = 2;          // B stages of tiles t, t+1, t+2
+    for (int t = 0; t < nk - 1; ++t) {
+        const int st = t & 1;
+        __builtin_amdgcn_sched_barrier(0);
+        step(f0, f1, st, b0, 1, C1{}, t, b2);
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        step(f1, f0, st, b0, 2, C2{}, t, b2);
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        step(f0, f1, st, b0, 3, C3{}, t, b2);
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        vm_wait<4>();  // only the B copies of tile t+2 may still be in flight
+        block_sync();  // every wave's share of tile t+1 landed; A stage st is free
+        step(f1, f0, st ^ 1, b1, 0, C4{}, t, b2);
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        const int bt = b0;
+        b0 = b1;
+        b1 = b2;
+        b2 = bt;
+    }
+    // last K tile: no copies, no barrier
+    const int st = (nk - 1) & 1;
+    __builtin_amdgcn_sched_barrier(0);
+    step(f0, f1, st, b0, 1, C0{}, 0, 0);
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    step(f1, f0, st, b0, 2, C0{}, 0, 0);
+    __builtin_amdgcn_s_waitcnt(0xc07f);
+    step(f0, f1, st, b0, 3, C0{}, 0, 0);
+    static_for<MI * NI>([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        mfma32_bf16(acc[k / NI][k % NI], f1.a[k / NI], f1.b[k % NI]);
+    });
+}
+
 // Two-stage kernel, any tile shape of the table.  Per K tile t (stage t & 1),
 // four 16-deep K steps:
 //   ks 0..2: MFMAs of step ks, reads of step ks+1 (alternating fragment sets)
@@ -215,6 +313,20 @@ __device__ __forceinline__ void read_frag_part(Frag<MI, NI>& f, const char* sa, 
 //            t+2 into stage t & 1
 // KFULL: every K slice is a whole number of 64-deep tiles, so the copies take
 // their offsets as base + delta (one add per copy instead of the range checks).
+//
+// 256x256 tiles with 8 waves and KFULL use a different ring (RING3): two A
+// stages and three B stages (2 x 32 + 3 x 32 KB, the whole LDS).  The copies
+// of tile t+2 into a two-stage ring can only start once every wave is done
+// with stage t, i.e. in step 3, so all 64 copies of the workgroup arrived as
+// one burst: the CU accepts about 16-20 copies and then stalls further issue
+// while it drains them at about 24 cycles per 1 KB, and a wave stalled on a
+// copy issues no MFMAs.  With a third B stage the B copies of tile t+2 go to
+// the stage of tile t-1 (free since the last barrier) and are issued in
+// steps 0-2; only the A copies remain in step 3:
+//   ks 0: B copies q 0, 1   ks 1: B copy q 2   ks 2: B copy q 3
+//   wait until at most those 4 are in flight (tile t+1 has landed), barrier
+//   ks 3: A copies q 0-3 into A stage t & 1
+// The last K tile runs without copies and without a barrier.
 template <int BM, int BN, bool TB, int WM = 2, int WN = 2, bool KFULL = false, bool FIX = false>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, TileMapArgs tmap) {
     gemm_batch_offset(a);
@@ -305,7 +417,12 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     };
     using None = std::integral_constant<int, 0>;
 
-    if (nk > 0) {
+    constexpr bool RING3 = KFULL && BM == 256 && BN == 256 && NW == 8;
+    if constexpr (RING3) {
+        static_assert(A_INSTR == 4 && Copier::B_INSTR == 4 && 2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
+                      "three-stage B ring layout");
+        if (nk > 0) ring3_main_loop<BM, BN, TB, WM, WN>(acc, smem, smem_base, cp, a, kbeg, nk, wm, wn, lane);
+    } else if (nk > 0) {
         static_for<PER_TILE>([&](auto q) { issue_part(0, q); });
         if (nk > 1) {
             static_for<PER_TILE>([&](auto q) { issue_part(1, q); });
@@ -340,6 +457,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
             __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
         }
     }
+    if constexpr (RING3) vm_wait<0>();  // copies of tiles past the end still write (zeros) into LDS
     if constexpr (FIX) {
         // In-kernel sum of two K slices (tmap.fixup is set for this instance).  Both slices of a tile run on one XCD
         // (the host enables this only when they do), so the exchange goes
