@@ -230,11 +230,15 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
                                                                ks, wm * WTM, wn * WTN, lane);
     };
     // MFMAs of f, with the reads of step ks (stages ast / bst) into g and then
-    // the copies CK (0: none; 1: B q 0-1, 2: B q 2, 3: B q 3 of tile t+2 into
-    // B stage b2; 4: A q 0-3 of tile t+2) spread over the MFMA slots.
+    // the copies CK spread over the MFMA slots (0: none; 1, 2, 3: the first
+    // half, third quarter and last quarter of the B copies of tile t+2, into
+    // B stage b2; 4: every A copy of tile t+2).
     auto step = [&](const F& f, F& g, int ast, int bst, int ks, auto ck_c, int t, int b2) {
         constexpr int CK = decltype(ck_c)::value;
-        constexpr int NC = CK == 0 ? 0 : CK == 1 ? 2 : CK == 4 ? 4 : 1;
+        constexpr int AQ = Copier::A_INSTR, BQ = Copier::B_INSTR;
+        // copies of this step: B q [0, BQ/2), [BQ/2, 3BQ/4), [3BQ/4, BQ), A q [0, AQ)
+        constexpr int QLO = CK == 1 ? 0 : CK == 2 ? BQ / 2 : CK == 3 ? 3 * BQ / 4 : 0;
+        constexpr int NC = CK == 0 ? 0 : CK == 1 ? BQ / 2 : CK == 4 ? AQ : BQ / 4;
         static_for<MI * NI>([&](auto kc) {
             constexpr int k = decltype(kc)::value;
             mfma32_bf16(acc[k / NI][k % NI], f.a[k / NI], f.b[k % NI]);
@@ -246,9 +250,7 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
                     read_part(g, ast, bst, ks, std::integral_constant<int, o>{});
                 } else {
                     constexpr int c = o - N_READS;
-                    if constexpr (CK == 1) copy_b(t + 2, b2, std::integral_constant<int, c>{});
-                    if constexpr (CK == 2) copy_b(t + 2, b2, std::integral_constant<int, 2>{});
-                    if constexpr (CK == 3) copy_b(t + 2, b2, std::integral_constant<int, 3>{});
+                    if constexpr (CK >= 1 && CK <= 3) copy_b(t + 2, b2, std::integral_constant<int, QLO + c>{});
                     if constexpr (CK == 4) copy_a(t + 2, std::integral_constant<int, c>{});
                 }
             });
@@ -262,11 +264,12 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
     using C4 = std::integral_constant<int, 4>;
 
     // tiles 0 and 1 whole (tile 1 reads nothing when nk == 1), then wait for tile 0
-    static_for<4>([&](auto q) { copy_a(0, q); });
-    static_for<4>([&](auto q) { copy_b(0, 0, q); });
-    static_for<4>([&](auto q) { copy_a(1, q); });
-    static_for<4>([&](auto q) { copy_b(1, 1, q); });
-    vm_wait<8>();
+    constexpr int AQ = Copier::A_INSTR, BQ = Copier::B_INSTR;
+    static_for<AQ>([&](auto q) { copy_a(0, q); });
+    static_for<BQ>([&](auto q) { copy_b(0, 0, q); });
+    static_for<AQ>([&](auto q) { copy_a(1, q); });
+    static_for<BQ>([&](auto q) { copy_b(1, 1, q); });
+    vm_wait<AQ + BQ>();
     block_sync();
     F f0, f1;
     static_for<N_READS>([&](auto idx) { read_part(f0, 0, 0, 0, idx); });
@@ -281,7 +284,7 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
         __builtin_amdgcn_s_waitcnt(0xc07f);
         step(f0, f1, st, b0, 3, C3{}, t, b2);
         __builtin_amdgcn_s_waitcnt(0xc07f);
-        vm_wait<4>();  // only the B copies of tile t+2 may still be in flight
+        vm_wait<BQ>();  // only the B copies of tile t+2 may still be in flight
         block_sync();  // every wave's share of tile t+1 landed; A stage st is free
         step(f1, f0, st ^ 1, b1, 0, C4{}, t, b2);
         __builtin_amdgcn_s_waitcnt(0xc07f);
@@ -314,15 +317,16 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
 // KFULL: every K slice is a whole number of 64-deep tiles, so the copies take
 // their offsets as base + delta (one add per copy instead of the range checks).
 //
-// 256x256 tiles with 8 waves and KFULL use a different ring (RING3): two A
-// stages and three B stages (2 x 32 + 3 x 32 KB, the whole LDS).  The copies
-// of tile t+2 into a two-stage ring can only start once every wave is done
-// with stage t, i.e. in step 3, so all 64 copies of the workgroup arrived as
-// one burst: the CU accepts about 16-20 copies and then stalls further issue
-// while it drains them at about 24 cycles per 1 KB, and a wave stalled on a
-// copy issues no MFMAs.  With a third B stage the B copies of tile t+2 go to
-// the stage of tile t-1 (free since the last barrier) and are issued in
-// steps 0-2; only the A copies remain in step 3:
+// 256x256 tiles with KFULL (8 or 4 waves) use a different ring (RING3): two
+// A stages and three B stages (2 x 32 + 3 x 32 KB, the whole LDS).  The
+// copies of tile t+2 into a two-stage ring can only start once every wave is
+// done with stage t, i.e. in step 3, so all 64 copies of the workgroup
+// arrived as one burst: the CU accepts about 16-20 copies and then stalls
+// further issue while it drains them at about 24 cycles per 1 KB, and a wave
+// stalled on a copy issues no MFMAs.  With a third B stage the B copies of
+// tile t+2 go to the stage of tile t-1 (free since the last barrier) and are
+// issued in steps 0-2; only the A copies remain in step 3 (8 waves, 4 + 4
+// copies per wave; 4 waves issue twice as many):
 //   ks 0: B copies q 0, 1   ks 1: B copy q 2   ks 2: B copy q 3
 //   wait until at most those 4 are in flight (tile t+1 has landed), barrier
 //   ks 3: A copies q 0-3 into A stage t & 1
@@ -417,9 +421,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     };
     using None = std::integral_constant<int, 0>;
 
-    constexpr bool RING3 = KFULL && BM == 256 && BN == 256 && NW == 8;
+    constexpr bool RING3 = KFULL && BM == 256 && BN == 256 && (NW == 8 || NW == 4);
     if constexpr (RING3) {
-        static_assert(A_INSTR == 4 && Copier::B_INSTR == 4 && 2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
+        static_assert(Copier::B_INSTR % 4 == 0 && 2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
                       "three-stage B ring layout");
         if (nk > 0) ring3_main_loop<BM, BN, TB, WM, WN>(acc, smem, smem_base, cp, a, kbeg, nk, wm, wn, lane);
     } else if (nk > 0) {

@@ -232,14 +232,16 @@ def test_dma_instances_every_element(tile, waves, tb, K, splits, monkeypatch):
     _run_case(512, 768, K, "bf16", "f32", tb=tb, accumulate=True, seed=K + 7)
 
 
-# The 256x256 8-wave kernel when every K slice is whole 64-deep tiles (two A stages, three B
-# stages, the last tile without copies): slices of one, two and three K tiles, unsplit, split with
-# a reduction pass (6 tiles) and split with the in-kernel sum (8 tiles), every element.
+# The 256x256 kernel (8 and 4 waves) when every K slice is whole 64-deep tiles (two A stages,
+# three B stages, the last tile without copies): slices of one, two and three K tiles, unsplit,
+# split with a reduction pass (6 tiles) and split with the in-kernel sum (8 tiles, 8 waves),
+# every element.
 @pytest.mark.parametrize("K,splits,N", [(64, 1, 768), (128, 1, 768), (192, 1, 768), (128, 2, 768), (640, 3, 768),
                                         (128, 2, 1024), (256, 2, 1024), (384, 2, 1024)])
 @pytest.mark.parametrize("tb", [0, 1])
-def test_dma256_whole_tile_slices(K, splits, N, tb, monkeypatch):
-    monkeypatch.setenv("ISAM_GEMM_CONFIG", f"tile=0,dma=1,dmaw=8,splits={splits}")
+@pytest.mark.parametrize("waves", [8, 4])
+def test_dma256_whole_tile_slices(K, splits, N, tb, waves, monkeypatch):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", f"tile=0,dma=1,dmaw={waves},splits={splits}")
     for ct in ("f32", "bf16"):
         _run_case(512, N, K, "bf16", ct, tb=tb, seed=K + splits + N)
     _run_case(512, N, K, "bf16", "f32", tb=tb, accumulate=True, seed=K + 3)
