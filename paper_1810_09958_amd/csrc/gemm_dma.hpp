@@ -317,16 +317,18 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
 // KFULL: every K slice is a whole number of 64-deep tiles, so the copies take
 // their offsets as base + delta (one add per copy instead of the range checks).
 //
-// 256x256 tiles with KFULL (8 or 4 waves) use a different ring (RING3): two
-// A stages and three B stages (2 x 32 + 3 x 32 KB, the whole LDS).  The
+// 256x256 tiles with KFULL (8 or 4 waves), and 128x128 tiles with KFULL, use
+// a different ring (RING3): two A stages and three B stages (2 x 32 + 3 x 32
+// KB, the whole LDS, for 256x256; 80 KB, as before, for 128x128).  The
 // copies of tile t+2 into a two-stage ring can only start once every wave is
 // done with stage t, i.e. in step 3, so all 64 copies of the workgroup
 // arrived as one burst: the CU accepts about 16-20 copies and then stalls
 // further issue while it drains them at about 24 cycles per 1 KB, and a wave
 // stalled on a copy issues no MFMAs.  With a third B stage the B copies of
 // tile t+2 go to the stage of tile t-1 (free since the last barrier) and are
-// issued in steps 0-2; only the A copies remain in step 3 (8 waves, 4 + 4
-// copies per wave; 4 waves issue twice as many):
+// issued in steps 0-2; only the A copies remain in step 3 (256x256 with 8
+// waves and 128x128 with 4: 4 + 4 copies per wave; 256x256 with 4 waves
+// issues twice as many):
 //   ks 0: B copies q 0, 1   ks 1: B copy q 2   ks 2: B copy q 3
 //   wait until at most those 4 are in flight (tile t+1 has landed), barrier
 //   ks 3: A copies q 0-3 into A stage t & 1
@@ -421,7 +423,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     };
     using None = std::integral_constant<int, 0>;
 
-    constexpr bool RING3 = KFULL && BM == 256 && BN == 256 && (NW == 8 || NW == 4);
+    constexpr bool RING3 = KFULL && ((BM == 256 && BN == 256 && (NW == 8 || NW == 4)) || (BM == 128 && BN == 128 && NW == 4));
     if constexpr (RING3) {
         static_assert(Copier::B_INSTR % 4 == 0 && 2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
                       "three-stage B ring layout");
