@@ -208,20 +208,25 @@ __device__ __forceinline__ void read_frag_part(Frag<MI, NI>& f, const char* sa, 
 
 // Main loop of the three-stage-B ring (see the kernel's comment): A stages at
 // LDS offsets 0 and A_BYTES, B stages at 2*A_BYTES + s*B_BYTES, s = 0..2.
-template <int BM, int BN, bool TB, int WM, int WN, int MI, int NI, typename Copier>
+template <int BM, int BN, bool TB, int WM, int WN, bool KFULL, int MI, int NI, typename Copier>
 __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* smem, uint32_t smem_base, const Copier& cp,
                                                 const GemmArgs& a, int64_t kbeg, int nk, int wm, int wn, int lane) {
     constexpr int BK = 64, A_BYTES = BM * 128, B_BYTES = BN * 128;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     const uint32_t bbase = smem_base + (uint32_t)(2 * A_BYTES);
+    // KFULL: offsets as base + per-tile delta; otherwise range-checked (a K
+    // tile past the end is wholly out of range and reads nothing either way)
     auto copy_a = [&](int tt, auto q_c) {
         const int64_t k0 = kbeg + (int64_t)tt * BK;
-        cp.template a_part_full<decltype(q_c)::value>((uint32_t)(k0 * 2), smem_base + (uint32_t)((tt & 1) * A_BYTES), tt < nk);
+        const uint32_t dst = smem_base + (uint32_t)((tt & 1) * A_BYTES);
+        if constexpr (KFULL) cp.template a_part_full<decltype(q_c)::value>((uint32_t)(k0 * 2), dst, tt < nk);
+        else cp.template a_part<decltype(q_c)::value>(k0, dst);
     };
     auto copy_b = [&](int tt, int bst, auto q_c) {
         const int64_t k0 = kbeg + (int64_t)tt * BK;
-        cp.template b_part_full<decltype(q_c)::value>((uint32_t)(TB ? k0 * 2 : k0 * a.ldb * 2),
-                                                      bbase + (uint32_t)(bst * B_BYTES), tt < nk);
+        const uint32_t dst = bbase + (uint32_t)(bst * B_BYTES);
+        if constexpr (KFULL) cp.template b_part_full<decltype(q_c)::value>((uint32_t)(TB ? k0 * 2 : k0 * a.ldb * 2), dst, tt < nk);
+        else cp.template b_part<decltype(q_c)::value>(k0, dst);
     };
     using F = Frag<MI, NI>;
     constexpr int N_READS = MI + NI * (TB ? 1 : 2);
@@ -317,9 +322,9 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
 // KFULL: every K slice is a whole number of 64-deep tiles, so the copies take
 // their offsets as base + delta (one add per copy instead of the range checks).
 //
-// 256x256 tiles with KFULL (8 or 4 waves), and 128x128 tiles with KFULL, use
-// a different ring (RING3): two A stages and three B stages (2 x 32 + 3 x 32
-// KB, the whole LDS, for 256x256; 80 KB, as before, for 128x128).  The
+// 256x256 tiles (8 or 4 waves) and 128x128 tiles (4 waves) use a different
+// ring (RING3): two A stages and three B stages (2 x 32 + 3 x 32 KB, the
+// whole LDS, for 256x256; 80 KB, as before, for 128x128).  The
 // copies of tile t+2 into a two-stage ring can only start once every wave is
 // done with stage t, i.e. in step 3, so all 64 copies of the workgroup
 // arrived as one burst: the CU accepts about 16-20 copies and then stalls
@@ -423,11 +428,11 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     };
     using None = std::integral_constant<int, 0>;
 
-    constexpr bool RING3 = KFULL && ((BM == 256 && BN == 256 && (NW == 8 || NW == 4)) || (BM == 128 && BN == 128 && NW == 4));
+    constexpr bool RING3 = (BM == 256 && BN == 256 && (NW == 8 || NW == 4)) || (BM == 128 && BN == 128 && NW == 4);
     if constexpr (RING3) {
         static_assert(Copier::B_INSTR % 4 == 0 && 2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
                       "three-stage B ring layout");
-        if (nk > 0) ring3_main_loop<BM, BN, TB, WM, WN>(acc, smem, smem_base, cp, a, kbeg, nk, wm, wn, lane);
+        if (nk > 0) ring3_main_loop<BM, BN, TB, WM, WN, KFULL>(acc, smem, smem_base, cp, a, kbeg, nk, wm, wn, lane);
     } else if (nk > 0) {
         static_for<PER_TILE>([&](auto q) { issue_part(0, q); });
         if (nk > 1) {
