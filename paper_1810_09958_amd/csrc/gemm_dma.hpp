@@ -243,7 +243,7 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
         constexpr int AQ = Copier::A_INSTR, BQ = Copier::B_INSTR;
         // copies of this step: B q [0, BQ/2), [BQ/2, 3BQ/4), [3BQ/4, BQ), A q [0, AQ)
         constexpr int QLO = CK == 1 ? 0 : CK == 2 ? BQ / 2 : CK == 3 ? 3 * BQ / 4 : 0;
-        constexpr int NC = CK == 0 ? 0 : CK == 1 ? BQ / 2 : CK == 4 ? AQ : BQ / 4;
+        constexpr int NC = CK == 0 ? 0 : CK == 1 ? BQ / 2 : CK == 2 ? 3 * BQ / 4 - BQ / 2 : CK == 3 ? BQ - 3 * BQ / 4 : AQ;
         static_for<MI * NI>([&](auto kc) {
             constexpr int k = decltype(kc)::value;
             mfma32_bf16(acc[k / NI][k % NI], f.a[k / NI], f.b[k % NI]);
@@ -322,9 +322,10 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
 // KFULL: every K slice is a whole number of 64-deep tiles, so the copies take
 // their offsets as base + delta (one add per copy instead of the range checks).
 //
-// 256x256 tiles (8 or 4 waves) and 128x128 tiles (4 waves) use a different
-// ring (RING3): two A stages and three B stages (2 x 32 + 3 x 32 KB, the
-// whole LDS, for 256x256; 80 KB, as before, for 128x128).  The
+// 256x256 and 256x128 tiles (8 or 4 waves) and 128x128 tiles (4 waves) use a
+// different ring (RING3): two A stages and three B stages (2 x 32 + 3 x 32 KB,
+// the whole LDS, for 256x256; 112 KB for 256x128; 80 KB, as before, for
+// 128x128).  The
 // copies of tile t+2 into a two-stage ring can only start once every wave is
 // done with stage t, i.e. in step 3, so all 64 copies of the workgroup
 // arrived as one burst: the CU accepts about 16-20 copies and then stalls
@@ -428,9 +429,9 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     };
     using None = std::integral_constant<int, 0>;
 
-    constexpr bool RING3 = (BM == 256 && BN == 256 && (NW == 8 || NW == 4)) || (BM == 128 && BN == 128 && NW == 4);
+    constexpr bool RING3 = (BM == 256 && (BN == 256 || BN == 128) && (NW == 8 || NW == 4)) || (BM == 128 && BN == 128 && NW == 4);
     if constexpr (RING3) {
-        static_assert(Copier::B_INSTR % 4 == 0 && 2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
+        static_assert(2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
                       "three-stage B ring layout");
         if (nk > 0) ring3_main_loop<BM, BN, TB, WM, WN, KFULL>(acc, smem, smem_base, cp, a, kbeg, nk, wm, wn, lane);
     } else if (nk > 0) {

@@ -232,16 +232,15 @@ def test_dma_instances_every_element(tile, waves, tb, K, splits, monkeypatch):
     _run_case(512, 768, K, "bf16", "f32", tb=tb, accumulate=True, seed=K + 7)
 
 
-# The 256x256 kernel (8 and 4 waves) when every K slice is whole 64-deep tiles (two A stages,
-# three B stages, the last tile without copies): slices of one, two and three K tiles, unsplit,
-# split with a reduction pass (6 tiles) and split with the in-kernel sum (8 tiles, 8 waves),
-# every element.
+# The direct-to-LDS kernels' two-A / three-B-stage ring (the last K tile without copies) on K
+# slices of one, two and three tiles, and a ragged one: unsplit, split with a reduction pass and,
+# for 256x256 tiles with 8 waves over 8 tiles, split with the in-kernel sum; every element.
 @pytest.mark.parametrize("K,splits,N", [(64, 1, 768), (128, 1, 768), (192, 1, 768), (128, 2, 768), (640, 3, 768),
-                                        (128, 2, 1024), (256, 2, 1024), (384, 2, 1024)])
+                                        (100, 1, 768), (128, 2, 1024), (256, 2, 1024), (384, 2, 1024)])
 @pytest.mark.parametrize("tb", [0, 1])
-@pytest.mark.parametrize("waves", [8, 4])
-def test_dma256_whole_tile_slices(K, splits, N, tb, waves, monkeypatch):
-    monkeypatch.setenv("ISAM_GEMM_CONFIG", f"tile=0,dma=1,dmaw={waves},splits={splits}")
+@pytest.mark.parametrize("tile,waves", DMA_INSTANCES)
+def test_dma_ring_short_slices(K, splits, N, tb, tile, waves, monkeypatch):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", f"tile={tile},dma=1,dmaw={waves},splits={splits}")
     for ct in ("f32", "bf16"):
         _run_case(512, N, K, "bf16", ct, tb=tb, seed=K + splits + N)
     _run_case(512, N, K, "bf16", "f32", tb=tb, accumulate=True, seed=K + 3)
