@@ -3,15 +3,22 @@
 // matrix product), with the depthwise result kept on chip as the operand of
 // the product (the inter-operation fusion of Section 6.2.2).
 //
-// fp32 products keep full fp32 precision here (v_mfma_f32_16x16x4_f32), so
-// the pointwise product is bound by the fp32 matrix-core rate.  The product
-// is computed transposed, out^T[cout][pixel] = P^T[cout][k] . Y^T[k][pixel]:
-//   * each wave owns 32 output channels; its slice of P (32 x C) lives in
-//     registers for the whole kernel as MFMA A operands;
+// The pointwise product keeps fp32 accuracy without the fp32 matrix rate:
+// every fp32 operand x is split into three bf16 terms, x = h + m + l + e
+// (h = bf16(x), m = bf16(x - h), l = bf16(x - h - m); each difference is
+// exact in fp32 and |e| <= 2^-24 |x|), and a.b is formed as the six bf16
+// products h.h + h.m + m.h + h.l + l.h + m.m with fp32 accumulation on the
+// bf16 matrix cores (v_mfma_f32_16x16x32_bf16, 16 times the fp32 MFMA
+// rate).  The dropped terms m.l, l.m, l.l are below 2^-23 |a.b|, the same
+// order as the rounding of one fp32 product.  The product is computed
+// transposed, out^T[cout][pixel] = P^T[cout][k] . Y^T[k][pixel]:
+//   * each wave owns 32 output channels; the three bf16 terms of its slice
+//     of P (32 x C) live in registers for the whole kernel as MFMA A
+//     operands;
 //   * the depthwise result Y of a tile (R output rows x W pixels) is built
-//     in LDS one 32-channel chunk at a time and read as MFMA B operands with
-//     ds_read_b128 (4 consecutive K values per lane cover 4 MFMA steps: the
-//     K order inside each 16-deep block is permuted identically in A and B);
+//     in LDS one 32-channel chunk at a time, as three bf16 term planes, and
+//     read as MFMA B operands with ds_read_b128 (8 consecutive channels of
+//     one pixel per lane);
 //   * the accumulators hold 4 consecutive output channels of one pixel per
 //     lane, so results go straight from registers to memory as 16-byte
 //     stores.
@@ -21,9 +28,12 @@
 //   depthwise of chunk c -> Y chunk in LDS, barrier
 //   MFMAs over the chunk
 // Input chunk layout: [R+2 rows][W][32 channels] fp32 (128 bytes per pixel,
-// one whole cache line per copied segment).  Y chunk layout: pixel p row of
-// 128 bytes, 16-byte unit u at u ^ ((p >> 1) & 7) (conflict-free for the
-// 16-row, 4-unit B-operand reads).
+// one whole cache line per copied segment).  Y chunk layout: term t, channel
+// unit u (8 channels), pixel p: 16 bytes at t*kYTerm + u*kYUnit + p*16.  The
+// B-operand reads of 16 lanes take 16 consecutive pixels of one unit (256
+// contiguous bytes); the unit stride is 64 bytes past a multiple of 256 so
+// that the depthwise writes of a wave (8 pixels x 4 units x 2 halves) fall on
+// distinct banks.
 // Supported: fp32 in and out, 3x3, stride 1, pad 1, depth multiplier 1,
 // C % 32 == 0 and C <= 128, C_out % 16 == 0 and C_out <= 256, W % 8 == 0 and
 // W <= 64; everything else uses the two-kernel path.
@@ -39,7 +49,25 @@ constexpr int kKC = 32;          // channels per chunk
 constexpr int kMaxW = 64;
 constexpr int kMaxC = 128;
 constexpr int kNT = kR32 * kMaxW / 16;   // pixel tiles of 16 per workgroup tile (max)
-constexpr int kKB = kMaxC / 16;          // 16-deep K blocks (max)
+constexpr int kKB = kMaxC / kKC;         // 32-deep K blocks = chunks (max)
+constexpr int kYUnit = kR32 * kMaxW * 16 + 64;
+constexpr int kYTerm = 4 * kYUnit;
+constexpr int kYBytes = 3 * kYTerm;
+
+typedef __bf16 f32s_bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32s_f32x2_t __attribute__((ext_vector_type(2)));
+// Two fp32 values to a bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32s_f32x2_t){lo, hi}, f32s_bf16x2_t));
+}
+// The three bf16 terms of two fp32 values, as packed pairs t[0] (h), t[1] (m), t[2] (l).
+__device__ __forceinline__ void split3_pair(float x0, float x1, uint32_t t[3]) {
+    t[0] = pack_bf16_rne(x0, x1);
+    const float r0 = x0 - __uint_as_float(t[0] << 16), r1 = x1 - __uint_as_float(t[0] & 0xffff0000u);
+    t[1] = pack_bf16_rne(r0, r1);
+    const float q0 = r0 - __uint_as_float(t[1] << 16), q1 = r1 - __uint_as_float(t[1] & 0xffff0000u);
+    t[2] = pack_bf16_rne(q0, q1);
+}
 
 __device__ __forceinline__ void f32_dma16(__amdgpu_buffer_rsrc_t rs, uint32_t lds_addr, uint32_t voff) {
     asm volatile(
@@ -58,11 +86,11 @@ __device__ __forceinline__ void f32_barrier() {
     __builtin_amdgcn_s_barrier();
     asm volatile("" : : : "memory");
 }
-__device__ __forceinline__ uint32_t y_off(int p, int u) { return (uint32_t)(p * 128 + ((u ^ ((p >> 1) & 7)) << 4)); }
+__device__ __forceinline__ uint32_t y_off(int t, int u, int p) { return (uint32_t)(t * kYTerm + u * kYUnit + p * 16); }
 
 __host__ __device__ __forceinline__ int xbuf_bytes(int W) { return ((kR32 + 2) * W * kKC * 4 + 1023) / 1024 * 1024; }
 __host__ __device__ __forceinline__ size_t f32_fused_lds(int W, int C) {
-    return 2 * (size_t)xbuf_bytes(W) + (size_t)kR32 * W * 128 + (size_t)9 * C * 4;
+    return 2 * (size_t)xbuf_bytes(W) + (size_t)kYBytes + (size_t)9 * C * 4;
 }
 
 template <int NT>
@@ -73,8 +101,8 @@ __global__ __launch_bounds__(64 * kWaves32) void dwsep_fused_f32_kernel(DwArgs d
     const int NCH = C / kKC;
     const int xb = xbuf_bytes(W);
     char* sX = smem;                                   // 2 x [R+2][W][32] fp32
-    char* sY = smem + 2 * xb;                          // [R*W][32] fp32 (swizzled)
-    float* sT = reinterpret_cast<float*>(sY + kR32 * W * 128);  // taps [9][C]
+    char* sY = smem + 2 * xb;                          // 3 term planes of the Y chunk
+    float* sT = reinterpret_cast<float*>(sY + kYBytes);  // taps [9][C]
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int tiles_per_img = (H + kR32 - 1) / kR32;
     const int n_tiles = (int)d.batch * tiles_per_img;
@@ -87,21 +115,31 @@ __global__ __launch_bounds__(64 * kWaves32) void dwsep_fused_f32_kernel(DwArgs d
     const float* taps = static_cast<const float*>(d.w);
     for (int i = tid; i < 9 * C; i += 64 * kWaves32) sT[i] = taps[i];
 
-    // This wave's P slice as MFMA A operands: output channel o = co0 + mt*16
-    // + lane%16, and for K step s of 16-deep block kb the K index
-    // kb*16 + 4*(lane/16) + s.
+    // The three bf16 terms of this wave's P slice as MFMA A operands: output
+    // channel o = co0 + mt*16 + lane%16 and, in 32-deep block kb, the K
+    // indices kb*32 + 8*(lane/16) + 0..7 (the B operands use the same).
     const int co0 = wid * 32;
     const int g = lane >> 4, li = lane & 15;
-    float preg[2][kKB][4];
+    uint4 pt[2][kKB][3];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-        for (int kb = 0; kb < kKB; ++kb)
+        for (int kb = 0; kb < kKB; ++kb) {
+            uint32_t w[3][4];
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const int o = co0 + mt * 16 + li, k = kb * 16 + 4 * g + s;
-                preg[mt][kb][s] = (o < C_out && k < C) ? pw[(int64_t)k * C_out + o] : 0.0f;
+            for (int e = 0; e < 4; ++e) {
+                const int o = co0 + mt * 16 + li, k = kb * 32 + 8 * g + 2 * e;
+                const float x0 = (o < C_out && k < C) ? pw[(int64_t)k * C_out + o] : 0.0f;
+                const float x1 = (o < C_out && k + 1 < C) ? pw[(int64_t)(k + 1) * C_out + o] : 0.0f;
+                uint32_t t[3];
+                split3_pair(x0, x1, t);
+                w[0][e] = t[0];
+                w[1][e] = t[1];
+                w[2][e] = t[2];
             }
+#pragma unroll
+            for (int t = 0; t < 3; ++t) pt[mt][kb][t] = make_uint4(w[t][0], w[t][1], w[t][2], w[t][3]);
+        }
     const bool wave_active = co0 < C_out;
 
     // Copy chunk c (channels c*32 .. +32) of tile `tile`'s input rows into buffer `buf`.
@@ -160,7 +198,13 @@ __global__ __launch_bounds__(64 * kWaves32) void dwsep_fused_f32_kernel(DwArgs d
                     a.w = fmaf(v.w, w.w, a.w);
                 }
             }
-            *reinterpret_cast<float4*>(sY + y_off(rl * W + dj, du)) = a;
+            // channels du*4 .. +3 = half (du & 1) of unit du / 2
+            uint32_t t01[3], t23[3];
+            split3_pair(a.x, a.y, t01);
+            split3_pair(a.z, a.w, t23);
+#pragma unroll
+            for (int t = 0; t < 3; ++t)
+                *reinterpret_cast<uint2*>(sY + y_off(t, du >> 1, rl * W + dj) + (du & 1) * 8) = make_uint2(t01[t], t23[t]);
         }
     };
 
@@ -185,29 +229,25 @@ __global__ __launch_bounds__(64 * kWaves32) void dwsep_fused_f32_kernel(DwArgs d
             f32_barrier();
             buf ^= 1;
             if (wave_active) {
+                // pt's K block index must be a compile-time constant.
 #pragma unroll
-                for (int kbl = 0; kbl < 2; ++kbl) {  // the chunk's two 16-deep K blocks
-                    const int kb = c * 2 + kbl;
-                    float4 yf[NT];
+                for (int kk = 0; kk < kKB; ++kk) {
+                    if (kk != c) continue;
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt)
-                        yf[nt] = *reinterpret_cast<const float4*>(sY + y_off(nt * 16 + li, kbl * 4 + g));
-                    // preg's K block index must be a compile-time constant.
+                    for (int nt = 0; nt < NT; ++nt) {
+                        uint4 yb[3];
 #pragma unroll
-                    for (int kk = 0; kk < kKB; ++kk) {
-                        if (kk != kb) continue;
-                        // K step outermost: consecutive MFMAs go to 2*NT different
-                        // accumulators, so none waits for the previous result.
+                        for (int t = 0; t < 3; ++t) yb[t] = *reinterpret_cast<const uint4*>(sY + y_off(t, g, nt * 16 + li));
 #pragma unroll
-                        for (int s = 0; s < 4; ++s)
-#pragma unroll
-                            for (int nt = 0; nt < NT; ++nt) {
-                                const float bv = s == 0 ? yf[nt].x : s == 1 ? yf[nt].y : s == 2 ? yf[nt].z : yf[nt].w;
-#pragma unroll
-                                for (int mt = 0; mt < 2; ++mt)
-                                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(preg[mt][kk][s], bv, acc[mt][nt],
-                                                                                       0, 0, 0);
-                            }
+                        for (int mt = 0; mt < 2; ++mt) {
+                            // smallest terms first
+                            mfma16_bf16(acc[mt][nt], pt[mt][kk][1], yb[1]);
+                            mfma16_bf16(acc[mt][nt], pt[mt][kk][2], yb[0]);
+                            mfma16_bf16(acc[mt][nt], pt[mt][kk][0], yb[2]);
+                            mfma16_bf16(acc[mt][nt], pt[mt][kk][1], yb[0]);
+                            mfma16_bf16(acc[mt][nt], pt[mt][kk][0], yb[1]);
+                            mfma16_bf16(acc[mt][nt], pt[mt][kk][0], yb[0]);
+                        }
                     }
                 }
             }
