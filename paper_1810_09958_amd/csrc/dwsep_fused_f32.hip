@@ -233,21 +233,26 @@ __global__ __launch_bounds__(64 * kWaves32) void dwsep_fused_f32_kernel(DwArgs d
 #pragma unroll
                 for (int kk = 0; kk < kKB; ++kk) {
                     if (kk != c) continue;
+                    // Pixel tiles in pairs; term products outermost, so
+                    // consecutive MFMAs go to 4 different accumulators and
+                    // none waits for the previous result.  Smallest terms
+                    // first: (P term, Y term) = (m,m) (l,h) (h,l) (m,h) (h,m) (h,h).
+                    constexpr int TA[6] = {1, 2, 0, 1, 0, 0}, TB[6] = {1, 0, 2, 0, 1, 0};
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) {
-                        uint4 yb[3];
+                    for (int n0 = 0; n0 < NT; n0 += 2) {
+                        uint4 yb[2][3];
 #pragma unroll
-                        for (int t = 0; t < 3; ++t) yb[t] = *reinterpret_cast<const uint4*>(sY + y_off(t, g, nt * 16 + li));
+                        for (int j = 0; j < 2; ++j)
 #pragma unroll
-                        for (int mt = 0; mt < 2; ++mt) {
-                            // smallest terms first
-                            mfma16_bf16(acc[mt][nt], pt[mt][kk][1], yb[1]);
-                            mfma16_bf16(acc[mt][nt], pt[mt][kk][2], yb[0]);
-                            mfma16_bf16(acc[mt][nt], pt[mt][kk][0], yb[2]);
-                            mfma16_bf16(acc[mt][nt], pt[mt][kk][1], yb[0]);
-                            mfma16_bf16(acc[mt][nt], pt[mt][kk][0], yb[1]);
-                            mfma16_bf16(acc[mt][nt], pt[mt][kk][0], yb[0]);
-                        }
+                            for (int t = 0; t < 3; ++t)
+                                if (n0 + j < NT) yb[j][t] = *reinterpret_cast<const uint4*>(sY + y_off(t, g, (n0 + j) * 16 + li));
+#pragma unroll
+                        for (int e = 0; e < 6; ++e)
+#pragma unroll
+                            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                                for (int mt = 0; mt < 2; ++mt)
+                                    if (n0 + j < NT) mfma16_bf16(acc[mt][n0 + j], pt[mt][kk][TA[e]], yb[j][TB[e]]);
                     }
                 }
             }
