@@ -102,6 +102,11 @@ size_t isam_gemm_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N, 
  *   Ho = (H + 2*pad - kh)/stride + 1, Wo = (W + 2*pad - kw)/stride + 1 (both > 0)
  * The intermediate Y is held in the workspace in in_type (bf16 Y is rounded
  * to nearest-even).  batch == 0: no-op.
+ * Precision: fp32 inputs give fp32-level results.  Where the fused fp32
+ * kernel runs (3x3, stride 1, pad 1, multiplier 1; see the workspace query),
+ * each fp32 product of the pointwise step is formed from a three-way bf16
+ * split of both operands (six bf16 products, fp32 accumulation; the dropped
+ * terms are below 2^-23 of the product).
  */
 isam_status_t isam_dwsep_conv(int64_t batch, int64_t H, int64_t W, int64_t C_in, int64_t depth_mult,
                               int64_t kh, int64_t kw, int64_t stride, int64_t pad, int64_t C_out,
