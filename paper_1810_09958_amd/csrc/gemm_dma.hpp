@@ -206,19 +206,21 @@ __device__ __forceinline__ void read_frag_part(Frag<MI, NI>& f, const char* sa, 
     }
 }
 
-// Main loop of the three-stage-B ring (see the kernel's comment): A stages at
-// LDS offsets 0 and A_BYTES, B stages at 2*A_BYTES + s*B_BYTES, s = 0..2.
-template <int BM, int BN, bool TB, int WM, int WN, bool KFULL, int MI, int NI, typename Copier>
+// Main loop of the three-stage ring (see the kernel's comment).  One operand
+// (B, or A when A3) has three stages, the other two: layout A stages then B
+// stages, each A_BYTES / B_BYTES.
+template <int BM, int BN, bool TB, int WM, int WN, bool KFULL, bool A3, int MI, int NI, typename Copier>
 __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* smem, uint32_t smem_base, const Copier& cp,
                                                 const GemmArgs& a, int64_t kbeg, int nk, int wm, int wn, int lane) {
     constexpr int BK = 64, A_BYTES = BM * 128, B_BYTES = BN * 128;
     constexpr int WTM = BM / WM, WTN = BN / WN;
-    const uint32_t bbase = smem_base + (uint32_t)(2 * A_BYTES);
+    constexpr int A_ST = A3 ? 3 : 2;
+    const uint32_t bbase = smem_base + (uint32_t)(A_ST * A_BYTES);
     // KFULL: offsets as base + per-tile delta; otherwise range-checked (a K
     // tile past the end is wholly out of range and reads nothing either way)
-    auto copy_a = [&](int tt, auto q_c) {
+    auto copy_a = [&](int tt, int ast, auto q_c) {
         const int64_t k0 = kbeg + (int64_t)tt * BK;
-        const uint32_t dst = smem_base + (uint32_t)((tt & 1) * A_BYTES);
+        const uint32_t dst = smem_base + (uint32_t)(ast * A_BYTES);
         if constexpr (KFULL) cp.template a_part_full<decltype(q_c)::value>((uint32_t)(k0 * 2), dst, tt < nk);
         else cp.template a_part<decltype(q_c)::value>(k0, dst);
     };
@@ -228,22 +230,34 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
         if constexpr (KFULL) cp.template b_part_full<decltype(q_c)::value>((uint32_t)(TB ? k0 * 2 : k0 * a.ldb * 2), dst, tt < nk);
         else cp.template b_part<decltype(q_c)::value>(k0, dst);
     };
+    // the three-stage operand (stage s3) and the two-stage one (stage tt & 1)
+    constexpr int Q3 = A3 ? Copier::A_INSTR : Copier::B_INSTR, Q2 = A3 ? Copier::B_INSTR : Copier::A_INSTR;
+    auto copy3 = [&](int tt, int s3, auto q_c) {
+        if constexpr (A3) copy_a(tt, s3, q_c);
+        else copy_b(tt, s3, q_c);
+    };
+    auto copy2 = [&](int tt, auto q_c) {
+        if constexpr (A3) copy_b(tt, tt & 1, q_c);
+        else copy_a(tt, tt & 1, q_c);
+    };
     using F = Frag<MI, NI>;
     constexpr int N_READS = MI + NI * (TB ? 1 : 2);
-    auto read_part = [&](F& f, int ast, int bst, int ks, auto idx_c) {
-        read_frag_part<decltype(idx_c)::value, MI, NI, TB, BN>(f, smem + ast * A_BYTES, smem + 2 * A_BYTES + bst * B_BYTES,
+    // s2: stage of the two-stage operand, s3: of the three-stage one
+    auto read_part = [&](F& f, int s2, int s3, int ks, auto idx_c) {
+        const int ast = A3 ? s3 : s2, bst = A3 ? s2 : s3;
+        read_frag_part<decltype(idx_c)::value, MI, NI, TB, BN>(f, smem + ast * A_BYTES, smem + A_ST * A_BYTES + bst * B_BYTES,
                                                                ks, wm * WTM, wn * WTN, lane);
     };
-    // MFMAs of f, with the reads of step ks (stages ast / bst) into g and then
+    // MFMAs of f, with the reads of step ks (stages s2 / s3) into g and then
     // the copies CK spread over the MFMA slots (0: none; 1, 2, 3: the first
-    // half, third quarter and last quarter of the B copies of tile t+2, into
-    // B stage b2; 4: every A copy of tile t+2).
-    auto step = [&](const F& f, F& g, int ast, int bst, int ks, auto ck_c, int t, int b2) {
+    // half, third quarter and last quarter of the three-stage operand's
+    // copies of tile t+2, into its stage r2; 4: every copy of the two-stage
+    // operand for tile t+2).
+    auto step = [&](const F& f, F& g, int s2, int s3, int ks, auto ck_c, int t, int r2) {
         constexpr int CK = decltype(ck_c)::value;
-        constexpr int AQ = Copier::A_INSTR, BQ = Copier::B_INSTR;
-        // copies of this step: B q [0, BQ/2), [BQ/2, 3BQ/4), [3BQ/4, BQ), A q [0, AQ)
-        constexpr int QLO = CK == 1 ? 0 : CK == 2 ? BQ / 2 : CK == 3 ? 3 * BQ / 4 : 0;
-        constexpr int NC = CK == 0 ? 0 : CK == 1 ? BQ / 2 : CK == 2 ? 3 * BQ / 4 - BQ / 2 : CK == 3 ? BQ - 3 * BQ / 4 : AQ;
+        // copies of this step: [0, Q3/2), [Q3/2, 3Q3/4), [3Q3/4, Q3) of the three-stage operand, [0, Q2) of the other
+        constexpr int QLO = CK == 1 ? 0 : CK == 2 ? Q3 / 2 : CK == 3 ? 3 * Q3 / 4 : 0;
+        constexpr int NC = CK == 0 ? 0 : CK == 1 ? Q3 / 2 : CK == 2 ? 3 * Q3 / 4 - Q3 / 2 : CK == 3 ? Q3 - 3 * Q3 / 4 : Q2;
         static_for<MI * NI>([&](auto kc) {
             constexpr int k = decltype(kc)::value;
             mfma32_bf16(acc[k / NI][k % NI], f.a[k / NI], f.b[k % NI]);
@@ -252,11 +266,11 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
             static_for<hi - lo>([&](auto d) {
                 constexpr int o = lo + decltype(d)::value;
                 if constexpr (o < N_READS) {
-                    read_part(g, ast, bst, ks, std::integral_constant<int, o>{});
+                    read_part(g, s2, s3, ks, std::integral_constant<int, o>{});
                 } else {
                     constexpr int c = o - N_READS;
-                    if constexpr (CK >= 1 && CK <= 3) copy_b(t + 2, b2, std::integral_constant<int, QLO + c>{});
-                    if constexpr (CK == 4) copy_a(t + 2, std::integral_constant<int, c>{});
+                    if constexpr (CK >= 1 && CK <= 3) copy3(t + 2, r2, std::integral_constant<int, QLO + c>{});
+                    if constexpr (CK == 4) copy2(t + 2, std::integral_constant<int, c>{});
                 }
             });
             __builtin_amdgcn_sched_barrier(0);
@@ -269,43 +283,42 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
     using C4 = std::integral_constant<int, 4>;
 
     // tiles 0 and 1 whole (tile 1 reads nothing when nk == 1), then wait for tile 0
-    constexpr int AQ = Copier::A_INSTR, BQ = Copier::B_INSTR;
-    static_for<AQ>([&](auto q) { copy_a(0, q); });
-    static_for<BQ>([&](auto q) { copy_b(0, 0, q); });
-    static_for<AQ>([&](auto q) { copy_a(1, q); });
-    static_for<BQ>([&](auto q) { copy_b(1, 1, q); });
-    vm_wait<AQ + BQ>();
+    static_for<Q2>([&](auto q) { copy2(0, q); });
+    static_for<Q3>([&](auto q) { copy3(0, 0, q); });
+    static_for<Q2>([&](auto q) { copy2(1, q); });
+    static_for<Q3>([&](auto q) { copy3(1, 1, q); });
+    vm_wait<Q2 + Q3>();
     block_sync();
     F f0, f1;
     static_for<N_READS>([&](auto idx) { read_part(f0, 0, 0, 0, idx); });
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    int b0 = 0, b1 = 1, b2 = 2;          // B stages of tiles t, t+1, t+2
+    int r0 = 0, r1 = 1, r2 = 2;          // three-stage operand: stages of tiles t, t+1, t+2
     for (int t = 0; t < nk - 1; ++t) {
         const int st = t & 1;
         __builtin_amdgcn_sched_barrier(0);
-        step(f0, f1, st, b0, 1, C1{}, t, b2);
+        step(f0, f1, st, r0, 1, C1{}, t, r2);
         __builtin_amdgcn_s_waitcnt(0xc07f);
-        step(f1, f0, st, b0, 2, C2{}, t, b2);
+        step(f1, f0, st, r0, 2, C2{}, t, r2);
         __builtin_amdgcn_s_waitcnt(0xc07f);
-        step(f0, f1, st, b0, 3, C3{}, t, b2);
+        step(f0, f1, st, r0, 3, C3{}, t, r2);
         __builtin_amdgcn_s_waitcnt(0xc07f);
-        vm_wait<BQ>();  // only the B copies of tile t+2 may still be in flight
-        block_sync();  // every wave's share of tile t+1 landed; A stage st is free
-        step(f1, f0, st ^ 1, b1, 0, C4{}, t, b2);
+        vm_wait<Q3>();  // only the three-stage operand's copies of tile t+2 may still be in flight
+        block_sync();   // every wave's share of tile t+1 landed; two-stage stage st is free
+        step(f1, f0, st ^ 1, r1, 0, C4{}, t, r2);
         __builtin_amdgcn_s_waitcnt(0xc07f);
-        const int bt = b0;
-        b0 = b1;
-        b1 = b2;
-        b2 = bt;
+        const int rt = r0;
+        r0 = r1;
+        r1 = r2;
+        r2 = rt;
     }
     // last K tile: no copies, no barrier
     const int st = (nk - 1) & 1;
     __builtin_amdgcn_sched_barrier(0);
-    step(f0, f1, st, b0, 1, C0{}, 0, 0);
+    step(f0, f1, st, r0, 1, C0{}, 0, 0);
     __builtin_amdgcn_s_waitcnt(0xc07f);
-    step(f1, f0, st, b0, 2, C0{}, 0, 0);
+    step(f1, f0, st, r0, 2, C0{}, 0, 0);
     __builtin_amdgcn_s_waitcnt(0xc07f);
-    step(f0, f1, st, b0, 3, C0{}, 0, 0);
+    step(f0, f1, st, r0, 3, C0{}, 0, 0);
     static_for<MI * NI>([&](auto kc) {
         constexpr int k = decltype(kc)::value;
         mfma32_bf16(acc[k / NI][k % NI], f1.a[k / NI], f1.b[k % NI]);
@@ -431,9 +444,10 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
 
     constexpr bool RING3 = (BM == 256 && (BN == 256 || BN == 128) && (NW == 8 || NW == 4)) || (BM == 128 && BN == 128 && NW == 4);
     if constexpr (RING3) {
-        static_assert(2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK,
-                      "three-stage B ring layout");
-        if (nk > 0) ring3_main_loop<BM, BN, TB, WM, WN, KFULL>(acc, smem, smem_base, cp, a, kbeg, nk, wm, wn, lane);
+        static_assert(2 * A_BYTES + 3 * B_BYTES <= STAGES * STAGE + SINK, "three-stage B ring layout");
+        // three B stages (three A stages measured the same on the 8192^3, 8192x1024x16384,
+        // 2048x3072x1024 and 32768x512x2560 products)
+        if (nk > 0) ring3_main_loop<BM, BN, TB, WM, WN, KFULL, false>(acc, smem, smem_base, cp, a, kbeg, nk, wm, wn, lane);
     } else if (nk > 0) {
         static_for<PER_TILE>([&](auto q) { issue_part(0, q); });
         if (nk > 1) {
