@@ -24,10 +24,11 @@
  *     (ISAM_ERR_UNSUPPORTED otherwise).
  *   - Entry points are thread-safe.  The library keeps no state between
  *     calls other than per-device caches filled once and never changed: CU
- *     count, LDS size, and the address of the static scratch that
+ *     count, LDS size, resident workgroups per CU of the stream-K GEMM
+ *     kernels, and the address of the static scratch that
  *     isam_gru_forward_noalloc uses; and one process-wide 64-bit counter
- *     (random start) that gives each in-kernel split-K sum of isam_gemm its
- *     own flag value.
+ *     (random start) that gives each in-kernel split-K or stream-K sum of
+ *     isam_gemm its own flag value.
  */
 #ifndef ISAM_H
 #define ISAM_H
@@ -73,8 +74,17 @@ typedef enum {
  * waits for the first's flag in the workspace (a bounded wait; if it ever
  * expires the tile's outputs are NaN) and adds its partial sums in a fixed
  * order, so results stay deterministic.  Other split plans sum the slices
- * in a second kernel.  The workspace needs no initial contents; concurrent
- * calls must not share one.
+ * in a second kernel.  bf16 products whose tile count leaves most compute
+ * units idle in a last partial round (A not transposed, 16-byte aligned
+ * rows, workspace 256-byte aligned) run a stream-K schedule instead
+ * (Section 3.4's allocation of work to processing units): a persistent grid
+ * sized to what the device holds at once, each workgroup an equal share of
+ * the (output tile, 64-deep K tile) units, the workgroups of one XCD
+ * splitting that XCD's range of tiles; a tile's owner starts from the
+ * partial sums the later shares of its K range left in the workspace (one
+ * fp32 tile and one flag line per workgroup), added in a fixed order, with
+ * the same bounded wait and NaN on expiry.  The workspace needs no initial
+ * contents; concurrent calls must not share one.
  */
 isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                         int ab_type, const void* A, int64_t lda, const void* B, int64_t ldb,

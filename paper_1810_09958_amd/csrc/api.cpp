@@ -6,7 +6,8 @@
 // in one place (the plan_* functions below) from the problem shape and the
 // device's compute-unit count, and can be overridden for tuning with the
 // environment variable ISAM_GEMM_CONFIG="tile=<0-5>,splits=<n>,group=<n>,xcd=<0|1>,dma=<0|1>"
-// (and small=0, rows=0, skinny=0, stream=0|1 for the special-shape kernels).
+// (and small=0, rows=0, skinny=0, stream=0|1 for the special-shape kernels, sk=0|1 for
+// the stream-K schedule, fixup=0 for the two-slice sum).
 // ISAM_LOG=1 prints each chosen plan to stderr.
 #include <hip/hip_runtime.h>
 
@@ -201,6 +202,12 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
             p.k_splits = (int)cdiv(K, p.k_per_split);
         }
 
+    } else if (ab_type == kBF16 && K > 2048 && t256 * 2 >= cus) {
+        // Deep K with 256x256 tiles for at least half the CUs: one partial
+        // round of the large tiles beats two rounds of smaller ones
+        // (measured, bf16: 3000^3 80 us against 104 for 256x128 tiles,
+        // 3072x3072x2560 62 against 83, 3584x3584x3000 82 against 109).
+        p.tile = kTile256x256;
     } else if (K <= 2048 && tiles(kTile128x128) >= cus) {
         // Shallow K: the 128x128 grid (measured, bf16 NT, K = 1024: 2048x3072
         // 24 us against 27 for 128x64; 4096x3072 39 us against 55 for 256x128,
@@ -256,10 +263,36 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     if (p.k_splits == 2 && p.tile == kTile256x256 && tiles(kTile256x256) % xcds == 0) p.fixup = 1;
     if (const char* env = getenv("ISAM_GEMM_CONFIG"))
         if (strstr(env, "fixup=0")) p.fixup = 0;
+    // Stream-K (bf16, the three-stage-ring tiles, no K split): every
+    // workgroup of a persistent grid takes an equal share of the (tile, K
+    // tile) units.  Taken by itself for 256x256 tiles when the tiles exceed
+    // the grid by at most a tenth (a second round would keep under 10 % of the
+    // CUs busy; measured, bf16: 4352x4096x3008 113 us against 135,
+    // 4352x4096x1024 51 against 54).  Larger shares lose to the plain grid:
+    // the workgroups of an XCD then walk K at different offsets, their A and
+    // B slices no longer coincide in L2 and every unit takes longer
+    // (4608x4352x2048, 1.2 tiles per workgroup: 108 against 97 us).
+    // ISAM_GEMM_CONFIG sk=0 / sk=1 switch it off / force it for any such plan.
+    // The kernel deals each XCD's range of tiles to that XCD's workgroups:
+    // every workgroup must get at least one (tile, K tile) unit, and the unit
+    // count must stay below 2^31.
+    if (ab_type == kBF16 && p.k_splits == 1 && gemm_sk_tile(p.tile) && K > 0) {
+        const int G = gemm_sk_grid(p.tile, cus);
+        const int parts = G % 8 == 0 ? 8 : 1;
+        const int64_t nt = tiles(p.tile), nkt = cdiv(K, 64);
+        const bool fits = (nt / parts) * nkt >= G / parts && nt * nkt < (int64_t(1) << 31);
+        const char* env = getenv("ISAM_GEMM_CONFIG");
+        const bool off = env && strstr(env, "sk=0"), force = env && strstr(env, "sk=1");
+        if (fits && !off && (force || (p.tile == kTile256x256 && nt > G && nt * 10 <= (int64_t)G * 11))) {
+            p.sk = 1;
+            p.sk_grid = G;
+        }
+    }
     return p;
 }
 
 size_t gemm_ws_bytes(const GemmPlan& p, int64_t M, int64_t N) {
+    if (p.sk) return gemm_sk_ws_bytes(p.tile, p.sk_grid);
     if (p.k_splits <= 1) return 0;
     // room for the reduction pass's partials, and (two-slice plans that may
     // sum inside the kernel) for the per-tile partials and flags
@@ -326,6 +359,7 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
     if (batch > 1) {
         p.k_splits = 1;
         p.k_per_split = K;
+        p.sk = 0;
     }
     p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     if (p.skinny == 4) {
@@ -342,13 +376,16 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
         p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     }
+    // Stream-K needs the direct-to-LDS kernel (bf16, A K-contiguous, aligned rows) and its
+    // workspace; otherwise the same tiles run one per workgroup.
+    if (p.sk && (trans_a || !p.vec || !workspace || workspace_bytes < gemm_ws_bytes(p, M, N))) p.sk = 0;
     if (p.k_splits > 1 && (!workspace || workspace_bytes < gemm_ws_bytes(p, M, N))) {
         if (p.skinny) p = plan_gemm(M, N, K, ab_type, device_cus(), /*allow_skinny=*/false);
         p.k_splits = 1;
         p.k_per_split = K;
         p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
     }
-    if (p.k_splits > 1) {
+    if (p.k_splits > 1 || p.sk) {
         // The split-K partial sums must not land on an operand.
         const int64_t es = (int64_t)dsize(ab_type);
         const size_t a_b = (size_t)((trans_a ? (K - 1) * lda + M : (M - 1) * lda + K) * es);
@@ -363,9 +400,9 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         if (p.tile != kTile64x64 && p.tile != kTile128x32) p.tile = kTile64x64;
     }
     if (log_enabled())
-        fprintf(stderr, "[isam] %s M=%lld N=%lld K=%lld ta=%d tb=%d ab=%d c=%d tile=%d vec=%d splits=%d kps=%lld group=%d xcd=%d dma=%d skinny=%d small=%d\n",
+        fprintf(stderr, "[isam] %s M=%lld N=%lld K=%lld ta=%d tb=%d ab=%d c=%d tile=%d vec=%d splits=%d kps=%lld group=%d xcd=%d dma=%d skinny=%d small=%d sk=%d\n",
                 who, (long long)M, (long long)N, (long long)K, trans_a, trans_b, ab_type, c_type, p.tile, p.vec,
-                p.k_splits, (long long)p.k_per_split, p.group_m, p.xcd_remap, p.dma, p.skinny, p.small);
+                p.k_splits, (long long)p.k_per_split, p.group_m, p.xcd_remap, p.dma, p.skinny, p.small, p.sk);
     GemmArgs a{};
     a.A = A;
     a.B = B;

@@ -6,6 +6,7 @@
 #include <stdlib.h>
 
 #include <atomic>
+#include <mutex>
 #include <random>
 
 namespace isam {
@@ -14,6 +15,7 @@ GemmKernelFn gemm_kernel_bf16(int tile, int ta, int tb, int vec);
 GemmKernelFn gemm_kernel_f32(int tile, int ta, int tb, int vec);
 GemmKernelFn gemm_dma_kernel_for(int tile, int trans_b, int waves, bool k_full);
 GemmKernelFn gemm_dma_fixup_kernel_for(int trans_b);
+GemmKernelFn gemm_dma_sk_kernel_for(int tile, int trans_b, bool k_full, int* threads);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk) {
     static const int dims[kTileCount][2] = {{256, 256}, {256, 128}, {128, 128},
@@ -21,6 +23,16 @@ void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk) {
     *bm = dims[tile][0];
     *bn = dims[tile][1];
     *bk = ab_type == kBF16 ? 64 : 32;
+}
+
+bool gemm_sk_tile(int tile) { return tile == kTile256x256 || tile == kTile256x128 || tile == kTile128x128; }
+
+int gemm_sk_grid(int tile, int cus) { return tile == kTile128x128 ? 2 * cus : cus; }
+
+size_t gemm_sk_ws_bytes(int tile, int grid) {
+    int bm, bn, bk;
+    tile_dims(tile, kBF16, &bm, &bn, &bk);
+    return (size_t)grid * ((size_t)bm * bn * 4 + 128);
 }
 
 size_t gemm_fixup_ws_bytes(int64_t M, int64_t N) {
@@ -117,6 +129,82 @@ hipError_t launch_splitk_reduce(const GemmArgs& a, int splits, hipStream_t s) {
 }
 }  // namespace
 
+// Workgroups of a stream-K kernel the current device holds per CU, queried
+// once per device and kernel (the query costs far more host time than a
+// launch) and never changed afterwards.
+static int sk_resident_per_cu(GemmKernelFn fn, int threads) {
+    constexpr int kDevs = 64, kFns = 32;
+    static std::mutex mu;
+    static GemmKernelFn keys[kDevs][kFns];
+    static int vals[kDevs][kFns];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevs) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    std::unique_lock<std::mutex> lk(mu, std::defer_lock);
+    try {
+        lk.lock();
+    } catch (...) {
+        return 0;
+    }
+    int i = 0;
+    for (; i < kFns && keys[dev][i]; ++i)
+        if (keys[dev][i] == fn) return vals[dev][i];
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(fn), threads, 0) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    if (i < kFns) {
+        keys[dev][i] = fn;
+        vals[dev][i] = n;
+    }
+    return n;
+}
+
+// Stream-K launch: a persistent grid of p.sk_grid workgroups; the tiles are
+// split into one contiguous range per XCD (workgroups are dealt to the 8 XCDs
+// in turn, so workgroup b runs on XCD b % 8 and the exchanges of a range stay
+// in one L2).
+// Returns false, launching nothing, when the device cannot hold the whole grid
+// at once (the waits need every workgroup resident); the caller then runs the
+// tiles one per workgroup.
+static bool launch_gemm_sk(const GemmArgs& a, const GemmPlan& p, hipStream_t s, hipError_t* err) {
+    int bm, bn, bk;
+    tile_dims(p.tile, a.ab_type, &bm, &bn, &bk);
+    int threads = 0;
+    GemmKernelFn fn = gemm_dma_sk_kernel_for(p.tile, a.trans_b, a.K % 64 == 0, &threads);
+    if (!fn) return false;
+    const int per_cu = p.tile == kTile128x128 ? 2 : 1;
+    if (sk_resident_per_cu(fn, threads) * (p.sk_grid / per_cu) < p.sk_grid) return false;
+    TileMapArgs t{};
+    t.tiles_m = (int)((a.M + bm - 1) / bm);
+    t.tiles_n = (int)((a.N + bn - 1) / bn);
+    t.group_m = p.group_m > 0 ? p.group_m : 1;
+    t.xcd_remap = 0;
+    t.k_per_split = a.K;
+    t.sk_parts = p.sk_grid % 8 == 0 ? 8 : 1;
+    t.sk_nkt = (int)((a.K + 63) / 64);
+    t.epoch = next_fixup_epoch();
+    t.expect = t.epoch;
+    t.wait_ticks = kFixupTimeoutTicks;
+    // Test hook (as for the two-slice sum): owners wait for a value no
+    // workgroup writes, under a 1 ms bound, so every tile that has partial
+    // sums from other workgroups comes back as NaN.
+    if (const char* v = getenv("ISAM_GEMM_TEST_FIXUP_STALL"); v && v[0] == '1') {
+        t.expect = t.epoch + 1;
+        t.wait_ticks = 100000;
+    }
+    t.flags = reinterpret_cast<uint64_t*>(reinterpret_cast<char*>(a.partial) + (size_t)p.sk_grid * bm * bn * 4);
+    if (const char* v = getenv("ISAM_LOG"); v && *v && *v != '0')
+        fprintf(stderr, "[isam] stream-K: %d workgroups, %d tiles x %d K tiles in %d ranges\n", p.sk_grid,
+                t.tiles_m * t.tiles_n, t.sk_nkt, t.sk_parts);
+    hipLaunchKernelGGL(fn, dim3((unsigned)p.sk_grid), dim3(threads), 0, s, a, t);
+    *err = hipGetLastError();
+    return true;
+}
+
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     if (a.batch > 1 && (p.k_splits > 1 || p.skinny || p.small)) return hipErrorInvalidValue;
     if (p.skinny == 2) return launch_skinny_rows(a, s);
@@ -132,7 +220,13 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     GemmKernelFn fn = nullptr;
     int threads = 256;
     bool fixup = false;
-    if (p.dma && a.ab_type == kBF16 && !a.trans_a && p.vec) {
+    const bool dma_ok = p.dma && a.ab_type == kBF16 && !a.trans_a && p.vec;
+    if (dma_ok && p.sk && p.k_splits <= 1 && a.batch <= 1 && gemm_sk_tile(p.tile) && a.K > 0 &&
+        ((uintptr_t)a.partial & 255) == 0) {
+        hipError_t e = hipSuccess;
+        if (launch_gemm_sk(a, p, s, &e)) return e;
+    }
+    if (dma_ok) {
         // every K slice a whole number of 64-deep tiles: copies with base + delta offsets
         const bool k_full = a.K % 64 == 0 && (p.k_splits <= 1 || p.k_per_split % 64 == 0);
         fn = gemm_dma_kernel_for(p.tile, a.trans_b, p.dma_waves, k_full);

@@ -325,6 +325,182 @@ __device__ __forceinline__ void ring3_main_loop(f32x16_t (&acc)[MI][NI], char* s
     });
 }
 
+// Exchange of one workgroup tile's fp32 accumulators between workgroups of
+// one XCD (the in-kernel split sums): a partial-sum tile of BM x BN floats,
+// each wave's accumulators in register order (16-byte pieces, lane-
+// contiguous: piece p of wave w at byte ((w * pieces + p) * 1024 + lane * 16)),
+// and a 128-byte flag line holding a 64-bit epoch.  Stores use workgroup-
+// scope write-through of L1, so they sit in the XCD's L2; loads bypass L1 and
+// read the L2's copy.  The per-lane part of every address is lane * 16 and the
+// rest is wave-uniform (a scalar offset), so no per-piece address registers
+// are needed and all of a block's loads can be in flight at once.
+template <int BM, int BN>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t partial_rsrc(float* base, int slot) {
+    constexpr uint32_t TILE_BYTES = (uint32_t)BM * BN * 4;
+    return make_rsrc(reinterpret_cast<char*>(base) + (size_t)slot * TILE_BYTES, TILE_BYTES);
+}
+// Stores the accumulators, waits until every wave's stores are in L2, then
+// raises the flag to `epoch`.
+template <int MI, int NI>
+__device__ __forceinline__ void partial_publish(const f32x16_t (&acc)[MI][NI], __amdgpu_buffer_rsrc_t rp,
+                                                __amdgpu_buffer_rsrc_t rf, uint64_t epoch, int wid, int lane) {
+    const int vo = lane * 16, wbase = wid * MI * NI * 4 * 1024;
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<4>([&](auto c) {
+                constexpr int cc = decltype(c)::value;
+                constexpr int piece = (decltype(i)::value * NI + decltype(j)::value) * 4 + cc;
+                const f32x16_t& v = acc[decltype(i)::value][decltype(j)::value];
+                const i32x4_t w = __builtin_bit_cast(i32x4_t, f32x4_t{v[4 * cc], v[4 * cc + 1], v[4 * cc + 2], v[4 * cc + 3]});
+                __builtin_amdgcn_raw_buffer_store_b128(w, rp, vo, wbase + piece * 1024, 1);
+            });
+        });
+    });
+    vm_wait<0>();  // this wave's pieces are in L2
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint2 e = make_uint2((uint32_t)epoch, (uint32_t)(epoch >> 32));
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) int, e), rf, 0, 0, 1);
+    }
+}
+// Thread 0 polls the flag until it holds `expect` or `ticks` of the 100 MHz
+// clock have passed; every thread gets the outcome (through `*okword`, one LDS
+// word no wave is using).
+__device__ __forceinline__ bool partial_wait(__amdgpu_buffer_rsrc_t rf, uint64_t expect, uint64_t ticks, int* okword) {
+    if (threadIdx.x == 0) {
+        const uint64_t t0 = wall_clock64();
+        int good = 0;
+        for (;;) {
+            const auto v = __builtin_amdgcn_raw_buffer_load_b64(rf, 0, 0, 17);
+            const uint64_t got = (uint64_t)(uint32_t)v[0] | ((uint64_t)(uint32_t)v[1] << 32);
+            if (got == expect) { good = 1; break; }
+            if (wall_clock64() - t0 > ticks) break;
+            __builtin_amdgcn_s_sleep(2);
+        }
+        *okword = good;
+    }
+    __syncthreads();
+    const bool ok = __builtin_amdgcn_readfirstlane(*okword) != 0;
+    __syncthreads();  // the word may be overwritten after this
+    return ok;
+}
+// acc += the partial-sum tile, element by element in register order: the 4 * NI
+// pieces of one row of accumulator blocks are loaded together, then added.
+template <int MI, int NI>
+__device__ __forceinline__ void partial_add(f32x16_t (&acc)[MI][NI], __amdgpu_buffer_rsrc_t rp, int wid, int lane) {
+    const int vo = lane * 16, wbase = wid * MI * NI * 4 * 1024;
+    static_for<MI>([&](auto i) {
+        constexpr int ii = decltype(i)::value;
+        f32x4_t p[NI][4];
+        static_for<NI>([&](auto j) {
+            static_for<4>([&](auto c) {
+                constexpr int piece = (ii * NI + decltype(j)::value) * 4 + decltype(c)::value;
+                p[decltype(j)::value][decltype(c)::value] =
+                    __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, vo, wbase + piece * 1024, 17));
+            });
+        });
+        __builtin_amdgcn_sched_barrier(0);  // every load of the row issued before the first add
+        static_for<NI>([&](auto j) {
+            f32x16_t& v = acc[ii][decltype(j)::value];
+            static_for<4>([&](auto c) {
+                constexpr int cc = decltype(c)::value;
+                const f32x4_t& q = p[decltype(j)::value][cc];
+                v[4 * cc] = q[0] + v[4 * cc];
+                v[4 * cc + 1] = q[1] + v[4 * cc + 1];
+                v[4 * cc + 2] = q[2] + v[4 * cc + 2];
+                v[4 * cc + 3] = q[3] + v[4 * cc + 3];
+            });
+        });
+    });
+}
+// Stream-K partial sums in tile layout: slot s holds a BM x BN fp32 tile,
+// row-major (tile-local row r, column c at byte (r * BN + c) * 4).  A
+// workgroup writes its accumulators there through each wave's LDS staging
+// rows (16-byte stores, workgroup-scope write-through of L1, so they sit in
+// the XCD's L2), waits until every wave's stores are in L2 and raises its
+// flag to `epoch`.
+template <int BN, int MI, int NI, int WTM, int WTN, int NW>
+__device__ __forceinline__ void sk_publish(f32x16_t (&acc)[MI][NI], char* smem, __amdgpu_buffer_rsrc_t rp,
+                                           __amdgpu_buffer_rsrc_t rf, uint64_t epoch, int wm, int wn, int wid,
+                                           int lane) {
+    constexpr int EPI_LD = WTN * 4 + 16, Q = WTN / 4, RPI = 64 / Q, IT = 32 / RPI;
+    char* epi = smem + wid * 32 * EPI_LD;
+    const int rl = lane / Q, c4l = lane % Q;
+    const int vo = (rl * BN + wn * WTN + 4 * c4l) * 4;
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) {
+                constexpr int vv = decltype(v)::value;
+                const int r = 8 * (vv >> 2) + 4 * (lane >> 5) + (vv & 3);
+                *reinterpret_cast<float*>(epi + r * EPI_LD + (decltype(j)::value * 32 + (lane & 31)) * 4) =
+                    acc[decltype(i)::value][decltype(j)::value][vv];
+            });
+        });
+        // the staging rows belong to this wave; its LDS accesses are performed in order
+        asm volatile("" : : : "memory");
+        static_for<IT>([&](auto it_c) {
+            constexpr int it = decltype(it_c)::value;
+            const float4 v = *reinterpret_cast<const float4*>(epi + (rl + it * RPI) * EPI_LD + c4l * 16);
+            const int so = (wm * WTM + decltype(i)::value * 32 + it * RPI) * BN * 4;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, v), rp, vo, so, 1);
+        });
+        asm volatile("" : : : "memory");
+    });
+    vm_wait<0>();  // this wave's stores are in L2
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint2 e = make_uint2((uint32_t)epoch, (uint32_t)(epoch >> 32));
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) int, e), rf, 0, 0, 1);
+    }
+}
+
+// Epilogue term of a stream-K owner: the partial sums of its contributors'
+// slots (first_slot, first_slot + stride, ...; n of them), added in that order
+// to every group of 4 accumulators, or NaN when a wait expired (ok == false).
+template <int BN, int BM>
+struct SkPartials {
+    static constexpr bool kActive = true;
+    float* partial;
+    int first_slot, stride, n;
+    bool ok;
+    template <int IT>
+    __device__ __forceinline__ void slab(float4 (&v)[IT], int r, int c, int step) const {
+        for (int k = 0; k < n; ++k) {
+            const __amdgpu_buffer_rsrc_t rp = partial_rsrc<BM, BN>(partial, first_slot + k * stride);
+            f32x4_t p[IT];
+            static_for<IT>([&](auto it_c) {
+                constexpr int it = decltype(it_c)::value;
+                p[it] = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, ((r + it * step) * BN + c) * 4, 0, 17));
+            });
+            __builtin_amdgcn_sched_barrier(0);  // every load of the slab issued before the first add
+            static_for<IT>([&](auto it_c) {
+                constexpr int it = decltype(it_c)::value;
+                v[it].x += p[it][0]; v[it].y += p[it][1]; v[it].z += p[it][2]; v[it].w += p[it][3];
+            });
+        }
+        if (!ok) static_for<IT>([&](auto it_c) { v[decltype(it_c)::value] = make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""), __builtin_nanf("")); });
+    }
+    __device__ __forceinline__ void one(float4& v, int r, int c) const {
+        float4 w[1] = {v};
+        for (int k = 0; k < n; ++k) {
+            const f32x4_t p = __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                partial_rsrc<BM, BN>(partial, first_slot + k * stride), (r * BN + c) * 4, 0, 17));
+            w[0].x += p[0]; w[0].y += p[1]; w[0].z += p[2]; w[0].w += p[3];
+        }
+        if (!ok) w[0] = make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""));
+        v = w[0];
+    }
+};
+
+template <int MI, int NI>
+__device__ __forceinline__ void acc_fill_nan(f32x16_t (&acc)[MI][NI]) {
+    static_for<MI>([&](auto i) {
+        static_for<NI>([&](auto j) {
+            static_for<16>([&](auto v) { acc[decltype(i)::value][decltype(j)::value][decltype(v)::value] = __builtin_nanf(""); });
+        });
+    });
+}
+
 // Two-stage kernel, any tile shape of the table.  Per K tile t (stage t & 1),
 // four 16-deep K steps:
 //   ks 0..2: MFMAs of step ks, reads of step ks+1 (alternating fragment sets)
@@ -485,79 +661,117 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
     }
     if constexpr (RING3) vm_wait<0>();  // copies of tiles past the end still write (zeros) into LDS
     if constexpr (FIX) {
-        // In-kernel sum of two K slices (tmap.fixup is set for this instance).  Both slices of a tile run on one XCD
-        // (the host enables this only when they do), so the exchange goes
-        // through that XCD's L2: stores and flag with workgroup-scope
-        // write-through of L1, loads that bypass L1.  Each wave's accumulators
-        // travel in register order (16-byte pieces, lane-contiguous).
-        constexpr uint32_t TILE_BYTES = (uint32_t)BM * BN * 4;
-        const __amdgpu_buffer_rsrc_t rp =
-            make_rsrc(reinterpret_cast<char*>(a.partial) + (size_t)blockIdx.x * TILE_BYTES, TILE_BYTES);
+        // In-kernel sum of two K slices (tmap.fixup is set for this instance).
+        // Both slices of a tile run on one XCD (the host enables this only
+        // when they do), so the exchange goes through that XCD's L2.
+        const __amdgpu_buffer_rsrc_t rp = partial_rsrc<BM, BN>(a.partial, blockIdx.x);
         const __amdgpu_buffer_rsrc_t rf = make_rsrc(tmap.flags + (size_t)blockIdx.x * 16, 128);
-        auto piece_off = [&](int i, int j, int c) {
-            return (uint32_t)((((wid * MI + i) * NI + j) * 4 + c) * 1024 + lane * 16);
-        };
         if (blockIdx.y == 0) {
-            static_for<MI>([&](auto i) {
-                static_for<NI>([&](auto j) {
-                    static_for<4>([&](auto c) {
-                        constexpr int cc = decltype(c)::value;
-                        const f32x16_t& v = acc[decltype(i)::value][decltype(j)::value];
-                        const i32x4_t w = __builtin_bit_cast(i32x4_t, f32x4_t{v[4 * cc], v[4 * cc + 1], v[4 * cc + 2], v[4 * cc + 3]});
-                        __builtin_amdgcn_raw_buffer_store_b128(w, rp, (int)piece_off(i, j, cc), 0, 1);
-                    });
-                });
-            });
-            vm_wait<0>();  // this wave's pieces are in L2
-            __syncthreads();
-            if (tid == 0) {
-                const uint2 e = make_uint2((uint32_t)tmap.epoch, (uint32_t)(tmap.epoch >> 32));
-                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) int, e), rf, 0, 0, 1);
-            }
+            partial_publish<MI, NI>(acc, rp, rf, tmap.epoch, wid, lane);
             return;
         }
         // slice 1: wait for slice 0's flag (bounded; on timeout the tile becomes NaN)
-        int* ok = reinterpret_cast<int*>(smem);
         __syncthreads();  // every wave is done with the stages
-        if (tid == 0) {
-            const uint64_t t0 = wall_clock64();
-            int good = 0;
-            for (;;) {
-                const auto v = __builtin_amdgcn_raw_buffer_load_b64(rf, 0, 0, 17);
-                const uint64_t got = (uint64_t)(uint32_t)v[0] | ((uint64_t)(uint32_t)v[1] << 32);
-                if (got == tmap.expect) { good = 1; break; }
-                if (wall_clock64() - t0 > tmap.wait_ticks) break;
-                __builtin_amdgcn_s_sleep(2);
-            }
-            *ok = good;
-        }
-        __syncthreads();
-        if (__builtin_amdgcn_readfirstlane(*ok) != 0) {
-            static_for<MI>([&](auto i) {
-                static_for<NI>([&](auto j) {
-                    f32x16_t& v = acc[decltype(i)::value][decltype(j)::value];
-                    static_for<4>([&](auto c) {
-                        constexpr int cc = decltype(c)::value;
-                        const f32x4_t p = __builtin_bit_cast(
-                            f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, (int)piece_off(i, j, cc), 0, 17));
-                        v[4 * cc] = p[0] + v[4 * cc];
-                        v[4 * cc + 1] = p[1] + v[4 * cc + 1];
-                        v[4 * cc + 2] = p[2] + v[4 * cc + 2];
-                        v[4 * cc + 3] = p[3] + v[4 * cc + 3];
-                    });
-                });
-            });
-        } else {
-            static_for<MI>([&](auto i) {
-                static_for<NI>([&](auto j) {
-                    static_for<16>([&](auto v) { acc[decltype(i)::value][decltype(j)::value][decltype(v)::value] = __builtin_nanf(""); });
-                });
-            });
-        }
+        if (partial_wait(rf, tmap.expect, tmap.wait_ticks, reinterpret_cast<int*>(smem))) partial_add<MI, NI>(acc, rp, wid, lane);
+        else acc_fill_nan<MI, NI>(acc);
     }
     __syncthreads();
     store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, lane, FIX);
 }
 
+
+// Stream-K schedule of the three-stage-ring kernel, for products whose tile
+// count leaves most compute units idle in a last partial round (the paper's
+// allocation of work to processing units, Section 3.4, with the partial
+// products of one output tile summed as in its Fig. 2).  One workgroup per
+// CU (two for 128x128 tiles, whose ring takes half the LDS), persistent.
+// The tiles are cut into sk_parts contiguous ranges, one per XCD (workgroup b
+// runs on XCD b % sk_parts under the round-robin dispatch), and the (tile,
+// 64-deep K tile) units of a range are dealt to that XCD's workgroups in
+// equal contiguous runs, so each workgroup computes about the same number of
+// MFMAs.  A run is a sequence of segments, each one tile's K range [kt0, kt1):
+//   * kt0 > 0 (only a run's first segment can start inside a tile): the
+//     workgroup leaves its sums in its partial-sum slot (tile layout) and
+//     raises its flag;
+//   * kt0 == 0: the workgroup owns the tile.  If the tile continues past its
+//     run, the continuation belongs to the next workgroups of the XCD, which
+//     compute it first thing; the owner computes its own K range, waits for
+//     their flags, and its epilogue adds their partial sums in workgroup
+//     order (a fixed order, so the result does not depend on timing) before
+//     writing C.
+// A workgroup's first segment never waits, so every wait ends; each is
+// bounded all the same (on timeout the tile becomes NaN).  Exchanges stay
+// inside one XCD's L2.
+template <int BM, int BN, bool TB, int WM, int WN, bool KFULL>
+__global__ __launch_bounds__(64 * WM * WN, BM == 128 ? 2 : 1) void gemm_dma_sk_kernel(GemmArgs a, TileMapArgs tmap) {
+    constexpr int NW = WM * WN, BK = 64;
+    constexpr int WTM = BM / WM, WTN = BN / WN, MI = WTM / 32, NI = WTN / 32;
+    constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
+    using Copier = DmaCopier<BM, BN, TB, NW>;
+    static_assert(Copier::A_INSTR + Copier::B_INSTR < 64, "vmcnt range");
+    constexpr int LDS = 2 * A_BYTES + 3 * B_BYTES;
+    static_assert(NW * 32 * (WTN * 4 + 16) <= LDS, "epilogue staging must fit in LDS");
+    __shared__ __attribute__((aligned(1024))) char smem[LDS];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wid / WN, wn = wid % WN;
+    const uint32_t smem_base = lds_addr_of(smem);
+
+    const int parts = tmap.sk_parts, nkt = tmap.sk_nkt;
+    const int x = (int)blockIdx.x % parts, li = (int)blockIdx.x / parts, gx = (int)gridDim.x / parts;
+    // (the host keeps tiles * K tiles below 2^31 and gives every workgroup at
+    // least one unit, so runs are never empty)
+    const int tiles = tmap.tiles_m * tmap.tiles_n;
+    const int t_lo = x * tiles / parts, t_hi = (x + 1) * tiles / parts;
+    const int units = (t_hi - t_lo) * nkt, base = units / gx, rem = units - base * gx;
+    auto run_begin = [&](int i) { return i * base + min(i, rem); };
+
+    f32x16_t acc[MI][NI];
+    int u = run_begin(li);
+    const int u_end = run_begin(li + 1);
+    while (u < u_end) {
+        const int tl = u / nkt;
+        const int kt0 = u - tl * nkt;
+        const int kt1 = min(nkt, kt0 + (u_end - u));
+        int tm, tn;
+        tile_coords(tmap, t_lo + tl, tm, tn);
+        const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+        const int64_t kbeg = (int64_t)kt0 * BK, kend = min(a.K, (int64_t)kt1 * BK);
+        // The lane index goes through an empty asm each segment, so the
+        // compiler recomputes the per-lane LDS, copy and store offsets in
+        // each segment instead of hoisting them out of the segment loop and
+        // holding them in registers across the main loop.
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        static_for<MI>([&](auto i) {
+            static_for<NI>([&](auto j) {
+                static_for<16>([&](auto v) { acc[i][j][decltype(v)::value] = 0.0f; });
+            });
+        });
+        const Copier cp(a, m0, n0, kend, wid, ln);
+        ring3_main_loop<BM, BN, TB, WM, WN, KFULL, false>(acc, smem, smem_base, cp, a, kbeg, kt1 - kt0, wm, wn, ln);
+        vm_wait<0>();     // copies of K tiles past the segment still write (zeros) into LDS
+        __syncthreads();  // every wave is done with the stages the staging rows overlap
+        if (kt0 > 0) {
+            sk_publish<BN, MI, NI, WTM, WTN, NW>(acc, smem, partial_rsrc<BM, BN>(a.partial, blockIdx.x),
+                                                 make_rsrc(tmap.flags + (size_t)blockIdx.x * 16, 128), tmap.epoch, wm,
+                                                 wn, wid, ln);
+        } else {
+            // the tile's later K tiles: runs of workgroups li+1, li+2, ... of this XCD
+            SkPartials<BN, BM> ex{a.partial, (li + 1) * parts + x, parts, 0, true};
+            const int tile_end = (tl + 1) * nkt;
+            for (int j = li + 1; kt1 < nkt && j < gx && run_begin(j) < tile_end; ++j) {
+                const int slot = j * parts + x;
+                ex.ok = partial_wait(make_rsrc(tmap.flags + (size_t)slot * 16, 128), tmap.expect, tmap.wait_ticks,
+                                     reinterpret_cast<int*>(smem)) && ex.ok;
+                ++ex.n;
+            }
+            store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, ln, true, ex);
+        }
+        __syncthreads();  // the next segment's copies overwrite the stages / staging rows
+        u += kt1 - kt0;
+    }
+}
 
 }  // namespace isam

@@ -149,19 +149,32 @@ struct TileMapArgs {
     uint64_t expect;         // value slice 1 waits for (== epoch but in the timeout test)
     uint64_t wait_ticks;     // bound of slice 1's wait (100 MHz ticks)
     uint64_t* flags;
+    // Stream-K schedule (persistent direct-to-LDS kernel only): the tiles are
+    // cut into sk_parts contiguous ranges, one per XCD, and the (tile, K tile)
+    // units of a range are dealt evenly to that XCD's workgroups; sk_nkt is
+    // the number of 64-deep K tiles per output tile.  The same epoch / expect /
+    // wait_ticks / flags protocol as the two-slice sum, one flag line and one
+    // partial-sum tile per workgroup.
+    int sk_parts, sk_nkt;
 };
+
+// Output tile number `tile` in the grouped rasterisation: groups of group_m
+// tile rows, column by column inside a group.
+__device__ __forceinline__ void tile_coords(const TileMapArgs& t, int tile, int& tm, int& tn) {
+    const int width = t.group_m * t.tiles_n;
+    const int group = tile / width;
+    const int first_m = group * t.group_m;
+    const int gm = min(t.tiles_m - first_m, t.group_m);
+    const int inner = tile - group * width;
+    tm = first_m + inner % gm;
+    tn = inner / gm;
+}
 
 __device__ __forceinline__ void map_tile(const TileMapArgs& t, int& tm, int& tn) {
     int bid = blockIdx.x;
     const int G = gridDim.x;
     if (t.xcd_remap && (G & 7) == 0) bid = (bid & 7) * (G >> 3) + (bid >> 3);
-    const int width = t.group_m * t.tiles_n;
-    const int group = bid / width;
-    const int first_m = group * t.group_m;
-    const int gm = min(t.tiles_m - first_m, t.group_m);
-    const int inner = bid - group * width;
-    tm = first_m + inner % gm;
-    tn = inner / gm;
+    tile_coords(t, bid, tm, tn);
 }
 
 // Problem blockIdx.z of a strided batch: offset the operand pointers.
@@ -174,13 +187,25 @@ __device__ __forceinline__ void gemm_batch_offset(GemmArgs& a) {
     }
 }
 
+// No extra terms in the epilogue (see store_acc_tile).
+struct NoExtra {
+    static constexpr bool kActive = false;
+    template <int IT>
+    __device__ __forceinline__ void slab(float4 (&)[IT], int, int, int) const {}
+    __device__ __forceinline__ void one(float4&, int, int) const {}
+};
+
 // Accumulators of the wave's WTM x WTN tile -> C (or the split-K partial
 // sums), staged through LDS so every store is a 16-byte (fp32) or 8-byte
 // (bf16) vector store.  `smem` must hold NW * 32 * (WTN*4 + 16) bytes and be
-// idle (no copies in flight).
-template <int MI, int NI, int WTM, int WTN, int NW>
+// idle (no copies in flight).  An active `extra` adds terms to each group of
+// 4 accumulators before the bias: extra.slab(v, r, c, step) to the groups of
+// tile rows r, r + step, ... at tile columns c..c+3, extra.one(v, r, c) to one
+// group (tile-local coordinates).
+template <int MI, int NI, int WTM, int WTN, int NW, typename Extra = NoExtra>
 __device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc)[MI][NI], char* smem, int64_t m0,
-                                               int64_t n0, int wm, int wn, int wid, int lane, bool fixup = false) {
+                                               int64_t n0, int wm, int wn, int wid, int lane, bool fixup = false,
+                                               const Extra& extra = Extra{}) {
     const bool split_out = gridDim.y > 1 && !fixup;
     const int split = blockIdx.y;
     constexpr int EPI_LD = WTN * 4 + 16;
@@ -213,9 +238,7 @@ __device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc
         const char* src = epi + rl * EPI_LD + c4l * 16;
         char* dst = obase + ((row0 + rl) * ldo + col0 + 4 * c4l) * (F32 ? 4 : 2);
         const int64_t step = (int64_t)RPI * ldo * (F32 ? 4 : 2);
-        static_for<IT>([&](auto it_c) {
-            constexpr int it = decltype(it_c)::value;
-            float4 v = *reinterpret_cast<const float4*>(src + it * RPI * EPI_LD);
+        auto finish = [&](float4 v, int it) {
             v.x += bias4.x; v.y += bias4.y; v.z += bias4.z; v.w += bias4.w;
             char* d = dst + it * step;
             if constexpr (F32) {
@@ -232,7 +255,26 @@ __device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc
                 }
                 *reinterpret_cast<uint2*>(d) = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
             }
-        });
+        };
+        if constexpr (Extra::kActive) {
+            // groups of CH rows: staged values, extra terms, then bias and stores
+            constexpr int CH = IT < 4 ? IT : 4;
+            static_for<IT / CH>([&](auto g_c) {
+                constexpr int g = decltype(g_c)::value;
+                float4 ex[CH];
+                static_for<CH>([&](auto k_c) {
+                    ex[decltype(k_c)::value] =
+                        *reinterpret_cast<const float4*>(src + (g * CH + decltype(k_c)::value) * RPI * EPI_LD);
+                });
+                extra.template slab<CH>(ex, (int)(row0 - m0) + rl + g * CH * RPI, (int)(col0 - n0) + 4 * c4l, RPI);
+                static_for<CH>([&](auto k_c) { finish(ex[decltype(k_c)::value], g * CH + decltype(k_c)::value); });
+            });
+        } else {
+            static_for<IT>([&](auto it_c) {
+                constexpr int it = decltype(it_c)::value;
+                finish(*reinterpret_cast<const float4*>(src + it * RPI * EPI_LD), it);
+            });
+        }
     };
     static_for<MI>([&](auto i) {
         static_for<NI>([&](auto j) {
@@ -266,6 +308,7 @@ __device__ __forceinline__ void store_acc_tile(const GemmArgs& a, f32x16_t (&acc
             const int64_t row = row0 + r, col = col0 + c4 * 4;
             if (row >= a.M || col >= a.N) continue;
             float4 v4 = *reinterpret_cast<const float4*>(epi + r * EPI_LD + c4 * 16);
+            if constexpr (Extra::kActive) extra.one(v4, (int)(row0 - m0) + r, (int)(col0 - n0) + c4 * 4);
             float vals[4] = {v4.x, v4.y, v4.z, v4.w};
             const int nv = (int)((a.N - col) < 4 ? (a.N - col) : 4);
             if (!split_out && a.bias) {

@@ -55,7 +55,16 @@ struct GemmPlan {
                      // 2: bf16 row-streaming kernel (16 rows per workgroup, whole K, no split);
                      // 4: narrow dot-product kernel (N < 8, not a multiple of the vector width)
     int small;       // 1: small-product kernel (one 32x32 tile per workgroup, waves split K)
+    int sk;          // 1: stream-K schedule of the direct-to-LDS kernel (persistent grid of
+                     //    sk_grid workgroups sharing the (tile, K tile) units evenly)
+    int sk_grid;
 };
+// Stream-K schedule: persistent grid size for a tile shape (one workgroup per
+// CU; two for 128x128 tiles, whose ring takes half the LDS) and its workspace
+// (one fp32 partial-sum tile and one 128-byte flag line per workgroup).
+int gemm_sk_grid(int tile, int cus);
+size_t gemm_sk_ws_bytes(int tile, int grid);
+bool gemm_sk_tile(int tile);
 // Small products: at most kSmallMaxTiles output tiles of 32x32 and K <= kSmallMaxK
 // (A K-contiguous, 16-byte aligned operands, batch 1: checked by the caller).
 constexpr int64_t kSmallMaxTiles = 64;

@@ -218,6 +218,75 @@ def test_split_sum_in_kernel_timeout_gives_nan(monkeypatch):
     assert norm_err(to_host_f64(C), ref, S) <= TOL_BF16
 
 
+# Stream-K schedule: a persistent grid in which every workgroup takes an equal share of the
+# (output tile, 64-deep K tile) units of its XCD's range of tiles, and a tile's owner starts
+# from the partial sums of the later shares of its K range (fixed order).  Forced on each tile
+# shape it covers, with a few more tiles than workgroups (shares of 1 to 1.1 tiles, so most
+# tiles are split between two workgroups): both B layouts, K a multiple of 64 and ragged,
+# ragged M and N with a tile count that is not a multiple of the XCD count, both output
+# types, accumulate.  Every element.
+SK_CASES = [("0", 4352, 4096), ("1", 4352, 2048), ("1", 4400, 1904), ("2", 2900, 2944)]
+
+
+@pytest.mark.parametrize("tile,M,N", SK_CASES)
+@pytest.mark.parametrize("tb", [0, 1])
+@pytest.mark.parametrize("K", [640, 600])
+def test_stream_k_every_element(tile, M, N, tb, K, monkeypatch, capfd):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", f"tile={tile},dma=1,sk=1")
+    monkeypatch.setenv("ISAM_LOG", "1")
+    for ct in ("f32", "bf16"):
+        _run_case(M, N, K, "bf16", ct, tb=tb, seed=M + N + K + tb)
+    _run_case(M, N, K, "bf16", "f32", tb=tb, accumulate=True, seed=M + K + 5)
+    assert "stream-K" in capfd.readouterr().err
+
+
+# The planner takes stream-K by itself where 256x256 tiles exceed the grid by at most a tenth
+# (272 tiles on 256 workgroups), K a multiple of 64 and ragged.  Every element, and
+# bit-identical on a second call.
+@pytest.mark.parametrize("shape", [(4352, 4096, 1024), (4352, 4096, 1000)])
+def test_stream_k_planned_every_element(shape, monkeypatch, capfd):
+    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    monkeypatch.setenv("ISAM_LOG", "1")
+    M, N, K = shape
+    A_h = bits(synth.normal(M, 40, (M, K)) / np.sqrt(K))
+    B_h = bits(synth.normal(M, 41, (K, N)) / np.sqrt(K))
+    A, B = to_gpu(A_h), to_gpu(B_h)
+    C1 = isam.gemm(A, B)
+    C2 = isam.gemm(A, B)
+    torch.cuda.synchronize()
+    assert "stream-K" in capfd.readouterr().err
+    assert torch.equal(C1, C2)
+    ref, S = oracle.gemm(A_h, B_h, M, N, K)
+    assert norm_err(to_host_f64(C1), ref, S) <= TOL_BF16
+
+
+def test_stream_k_timeout_gives_nan(monkeypatch):
+    # An owner's wait for the partial sums of its tile is bounded; the host forces it to expire
+    # (the flag value waited for is never written, 1 ms bound): the tiles shared between
+    # workgroups come back NaN, the others are still right, and the next call on the same
+    # workspace is correct everywhere.
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,sk=1")
+    M, N, K = 4352, 4096, 640
+    A_h = bits(synth.uniform(5, 10, (M, K), -1, 1))
+    B_h = bits(synth.uniform(5, 11, (K, N), -1, 1))
+    A, B = to_gpu(A_h), to_gpu(B_h)
+    ws = torch.empty(isam.gemm_workspace_size(M, N, K, 1, 0), device="cuda", dtype=torch.uint8)
+    monkeypatch.setenv("ISAM_GEMM_TEST_FIXUP_STALL", "1")
+    C = isam.gemm(A, B, workspace=ws)
+    torch.cuda.synchronize()
+    ref, S = oracle.gemm(A_h, B_h, M, N, K)
+    tiles = to_host_f64(C).reshape(M // 256, 256, N // 256, 256).transpose(0, 2, 1, 3)
+    nan_tile = np.isnan(tiles).any(axis=(2, 3))
+    assert nan_tile.any() and not nan_tile.all()
+    assert np.isnan(tiles[nan_tile]).all(), "a tile is partly NaN"
+    good = ~np.repeat(np.repeat(nan_tile, 256, axis=0), 256, axis=1)
+    assert norm_err(np.where(good, to_host_f64(C), ref), ref, S) <= TOL_BF16
+    monkeypatch.delenv("ISAM_GEMM_TEST_FIXUP_STALL")
+    C = isam.gemm(A, B, workspace=ws)
+    torch.cuda.synchronize()
+    assert norm_err(to_host_f64(C), ref, S) <= TOL_BF16
+
+
 DMA_INSTANCES = [("0", "8"), ("0", "4"), ("1", "8"), ("1", "4"), ("2", "4")]
 
 
@@ -276,15 +345,15 @@ def _guarded_gemm(M, N, K, dt, ct, pad_cols, seed, tb=0, env=None, monkeypatch=N
     assert norm_err(body[:, :N].astype(np.float64), ref, S) <= tol
 
 
-GUARD_CASES = ["dma256", "dma256_split", "dma256_split_sum", "dma128", "skinny_rows", "skinny_split", "narrow",
-               "stream", "tile_f32", "small"]
+GUARD_CASES = ["dma256", "dma256_split", "dma256_split_sum", "dma128", "dma_sk", "skinny_rows", "skinny_split",
+               "narrow", "stream", "tile_f32", "small"]
 
 
 @pytest.mark.parametrize("ct", ["f32", "bf16"])
 @pytest.mark.parametrize("case", GUARD_CASES)
 def test_guard_bands_every_kernel(ct, case, monkeypatch):
     # Each GEMM kernel writes exactly its M x N block: the direct-to-LDS kernels (256x256
-    # whole and split along K, 128x128), the skinny kernels (one pass and split-K), the
+    # whole and split along K, 128x128, the stream-K schedule), the skinny kernels (one pass and split-K), the
     # narrow dot-product kernel, the streaming kernel, the fp32 tile kernel and the small-
     # product kernel, with C rows padded (ldc > N).
     cases = {
@@ -292,6 +361,7 @@ def test_guard_bands_every_kernel(ct, case, monkeypatch):
         "dma256_split": dict(M=520, N=776, K=640, dt="bf16", env="tile=0,dma=1,dmaw=8,splits=2"),
         "dma256_split_sum": dict(M=500, N=1000, K=1280, dt="bf16", env="tile=0,dma=1,dmaw=8,splits=2"),
         "dma128": dict(M=520, N=776, K=600, dt="bf16", env="tile=2,dma=1"),
+        "dma_sk": dict(M=4400, N=1904, K=600, dt="bf16", env="tile=1,dma=1,sk=1"),
         "skinny_rows": dict(M=4100, N=32, K=1000, dt="bf16", env=None),
         "skinny_split": dict(M=300, N=24, K=6000, dt="f32", env=None),
         "narrow": dict(M=1000, N=3, K=2000, dt="bf16", env=None),
