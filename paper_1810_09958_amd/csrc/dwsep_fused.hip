@@ -107,6 +107,31 @@ __device__ __forceinline__ void f_barrier() {
 template <int C>
 constexpr int a_tile_bytes() { return kFPix * C * 2; }
 
+// Producer ring rows: logical 16-byte unit (unit column x, channel unit u) of
+// a row.  With 4 channel units per column (C = 128) each block of 4 columns
+// (16 units, 256 bytes) is rotated by 4 units per block: unit (x, u) sits at
+// 16 (x/4) + (4 (x%4) + u + 4 ((x/4)%4)) % 16.  A stencil read has lane
+// (jl, ul) = (lane / 4, lane % 4) at column 4 jl + dj, and the four jl of
+// every 16-lane ds_read_b128 phase ({0-3, 12-15, 20-27}, {4-11, 16-19, 28-31},
+// and + 32) differ mod 4, so the 16 lanes of a phase hit 16 different groups
+// of 4 banks (unrotated, all four jl share one group: 4-way conflicts).
+// Other channel counts keep the plain layout.
+template <int UPW>
+__device__ __forceinline__ int ring_pos(int x, int u) {
+    if constexpr (UPW == 4) return 16 * (x >> 2) + ((4 * (x & 3) + u + 4 * ((x >> 2) & 3)) & 15);
+    else return x * UPW + u;
+}
+// Inverse of ring_pos: the logical unit x * UPW + u held at physical unit p.
+template <int UPW>
+__device__ __forceinline__ int ring_unit(int p) {
+    if constexpr (UPW == 4) {
+        const int b = p >> 4, lo = ((p & 15) - 4 * (b & 3)) & 15;
+        return 16 * b + lo;
+    } else {
+        return p;
+    }
+}
+
 template <int R, int C, typename TO, int NP = kProducers>
 __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwArgs d, const void* pw, void* out,
                                                                    int64_t C_out, int n_slots, int row_instr) {
@@ -162,7 +187,9 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
         char* dst = ring + nx_slot * slot_bytes;
         const bool row_ok = ir >= 0 && ir < H;
         for (int q = 0; q < row_instr; ++q) {
-            const int v = q * 64 + lane;  // unit v holds column v / UPW - 1: zero halo at -1 and W
+            // physical unit q * 64 + lane holds logical unit v: column v / UPW - 1 (zero halo at -1
+            // and W), channel unit v % UPW
+            const int v = ring_unit<UPW>(q * 64 + lane);
             const int x = v / UPW - 1, u = v % UPW;
             const bool ok = row_ok && x >= 0 && x < W;
             const uint32_t off =
@@ -260,18 +287,22 @@ __global__ __launch_bounds__(64 * (NP + kConsumers)) void dwsep_fused_kernel(DwA
             }
             // One pass: the lane reads columns j0-1 .. j0+CPL of each of the
             // R+2 rows (the halo columns make every read unconditional; a run
-            // past the image reads column W-1 and is not stored), all reads
+            // past the image is not stored), all reads
             // in flight at once, then computes its CPL x R outputs: each
             // loaded column serves up to three outputs instead of being read
             // once per output.
-            const int j0 = jl * CPL;
+            // Unit columns past W+1 feed only outputs past the image (not
+            // stored); they are clamped to the row's last unit column, which
+            // keeps every read inside the row and (unlike a clamp at W+1)
+            // adds no bank conflicts.
+            const int j0 = jl * CPL, xcap = row_instr * 64 / UPW - 1;
             uint4 v[R + 2][CPL + 2];
 #pragma unroll
             for (int k = 0; k < R + 2; ++k)
 #pragma unroll
                 for (int dj = 0; dj < CPL + 2; ++dj) {
-                    const int x = min(j0 + dj, W + 1);  // unit column x holds image column x-1
-                    v[k][dj] = *reinterpret_cast<const uint4*>(rowp[k] + (x * UPW + ul) * 16);
+                    const int x = min(j0 + dj, xcap);  // unit column x holds image column x-1
+                    v[k][dj] = *reinterpret_cast<const uint4*>(rowp[k] + ring_pos<UPW>(x, ul) * 16);
                 }
 #pragma unroll
             for (int cl = 0; cl < CPL; ++cl) {
