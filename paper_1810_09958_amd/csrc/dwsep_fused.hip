@@ -108,28 +108,28 @@ template <int C>
 constexpr int a_tile_bytes() { return kFPix * C * 2; }
 
 // Producer ring rows: logical 16-byte unit (unit column x, channel unit u) of
-// a row.  With 4 channel units per column (C = 128) each block of 4 columns
-// (16 units, 256 bytes) is rotated by 4 units per block: unit (x, u) sits at
-// 16 (x/4) + (4 (x%4) + u + 4 ((x/4)%4)) % 16.  A stencil read has lane
-// (jl, ul) = (lane / 4, lane % 4) at column 4 jl + dj, and the four jl of
-// every 16-lane ds_read_b128 phase ({0-3, 12-15, 20-27}, {4-11, 16-19, 28-31},
-// and + 32) differ mod 4, so the 16 lanes of a phase hit 16 different groups
-// of 4 banks (unrotated, all four jl share one group: 4-way conflicts).
-// Other channel counts keep the plain layout.
+// a row, at a physical unit rotated within blocks of 16 units (256 bytes):
+//   4 channel units per column (C = 128): unit (x, u) at
+//     16 (x/4) + (4 (x%4) + u + 4 ((x/4)%4)) % 16;
+//   2 channel units per column (C = 64): unit (x, u) at
+//     16 (x/8) + (2 (x%8) + u + 2 ((x/8)%2)) % 16.
+// A stencil read has lane (jl, ul) = (lane / UPW, lane % UPW) at column
+// CPL jl + dj.  The jl of every 16-lane ds_read_b128 phase ({0-3, 12-15,
+// 20-27}, {4-11, 16-19, 28-31}, and + 32) differ mod 4 (C = 128) or mod 8
+// (C = 64), so the 16 lanes of a phase hit 16 different groups of 4 banks;
+// unrotated, 4 (C = 128) or 2 (C = 64) lanes shared each group.
 template <int UPW>
 __device__ __forceinline__ int ring_pos(int x, int u) {
+    static_assert(UPW == 4 || UPW == 2, "ring layout defined for 2 or 4 channel units per column");
     if constexpr (UPW == 4) return 16 * (x >> 2) + ((4 * (x & 3) + u + 4 * ((x >> 2) & 3)) & 15);
-    else return x * UPW + u;
+    else return 16 * (x >> 3) + ((2 * (x & 7) + u + 2 * ((x >> 3) & 1)) & 15);
 }
 // Inverse of ring_pos: the logical unit x * UPW + u held at physical unit p.
 template <int UPW>
 __device__ __forceinline__ int ring_unit(int p) {
-    if constexpr (UPW == 4) {
-        const int b = p >> 4, lo = ((p & 15) - 4 * (b & 3)) & 15;
-        return 16 * b + lo;
-    } else {
-        return p;
-    }
+    const int b = p >> 4;
+    if constexpr (UPW == 4) return 16 * b + (((p & 15) - 4 * (b & 3)) & 15);
+    else return 16 * b + (((p & 15) - 2 * (b & 1)) & 15);
 }
 
 template <int R, int C, typename TO, int NP = kProducers>
