@@ -24,9 +24,9 @@
  *     (ISAM_ERR_UNSUPPORTED otherwise).
  *   - Entry points are thread-safe.  The library keeps no state between
  *     calls other than per-device caches filled once and never changed: CU
- *     count, LDS size, resident workgroups per CU of the stream-K GEMM
- *     kernels, and the address of the static scratch that
- *     isam_gru_forward_noalloc uses; and one process-wide 64-bit counter
+ *     count, LDS size, the dynamic-LDS limit set on each kernel that needs
+ *     one, resident workgroups per CU of the persistent kernels, and the
+ *     address of the static scratch that isam_gru_forward_noalloc uses; and one process-wide 64-bit counter
  *     (random start) that gives each in-kernel split-K or stream-K sum of
  *     isam_gemm its own flag value.
  */

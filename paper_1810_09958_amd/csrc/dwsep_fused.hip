@@ -491,7 +491,7 @@ hipError_t launch_dwsep_fused(const DwArgs& d, const void* pw, void* out, int64_
     const int grid = (int)std::min<int64_t>(tiles, cus);
     void* fn = p.R == 2 ? (d.C == 128 ? fused_fn<2, 128>(out_type) : fused_fn<2, 64>(out_type))
                         : (d.C == 128 ? fused_fn<1, 128>(out_type) : fused_fn<1, 64>(out_type));
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds);
+    hipError_t e = ensure_dynamic_lds(fn, p.lds);
     if (e != hipSuccess) return e;
     DwArgs dd = d;
     int n_slots = p.n_slots, row_instr = p.row_instr;

@@ -311,7 +311,7 @@ hipError_t launch_dwsep_fused_f32(const DwArgs& d, const void* pw, void* out, in
         case 8: fn = reinterpret_cast<void*>(dwsep_fused_f32_kernel<8>); break;
         default: return hipErrorInvalidValue;
     }
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = ensure_dynamic_lds(fn, lds);
     if (e != hipSuccess) return e;
     DwArgs dd = d;
     const float* p = static_cast<const float*>(pw);

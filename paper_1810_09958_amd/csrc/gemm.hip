@@ -6,7 +6,6 @@
 #include <stdlib.h>
 
 #include <atomic>
-#include <mutex>
 #include <random>
 
 namespace isam {
@@ -129,40 +128,6 @@ hipError_t launch_splitk_reduce(const GemmArgs& a, int splits, hipStream_t s) {
 }
 }  // namespace
 
-// Workgroups of a stream-K kernel the current device holds per CU, queried
-// once per device and kernel (the query costs far more host time than a
-// launch) and never changed afterwards.
-static int sk_resident_per_cu(GemmKernelFn fn, int threads) {
-    constexpr int kDevs = 64, kFns = 32;
-    static std::mutex mu;
-    static GemmKernelFn keys[kDevs][kFns];
-    static int vals[kDevs][kFns];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevs) {
-        (void)hipGetLastError();
-        return 0;
-    }
-    std::unique_lock<std::mutex> lk(mu, std::defer_lock);
-    try {
-        lk.lock();
-    } catch (...) {
-        return 0;
-    }
-    int i = 0;
-    for (; i < kFns && keys[dev][i]; ++i)
-        if (keys[dev][i] == fn) return vals[dev][i];
-    int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(fn), threads, 0) != hipSuccess) {
-        (void)hipGetLastError();
-        return 0;
-    }
-    if (i < kFns) {
-        keys[dev][i] = fn;
-        vals[dev][i] = n;
-    }
-    return n;
-}
-
 // Stream-K launch: a persistent grid of p.sk_grid workgroups; the tiles are
 // split into one contiguous range per XCD (workgroups are dealt to the 8 XCDs
 // in turn, so workgroup b runs on XCD b % 8 and the exchanges of a range stay
@@ -177,7 +142,7 @@ static bool launch_gemm_sk(const GemmArgs& a, const GemmPlan& p, hipStream_t s, 
     GemmKernelFn fn = gemm_dma_sk_kernel_for(p.tile, a.trans_b, a.K % 64 == 0, &threads);
     if (!fn) return false;
     const int per_cu = p.tile == kTile128x128 ? 2 : 1;
-    if (sk_resident_per_cu(fn, threads) * (p.sk_grid / per_cu) < p.sk_grid) return false;
+    if (resident_per_cu(reinterpret_cast<const void*>(fn), threads, 0) * (p.sk_grid / per_cu) < p.sk_grid) return false;
     TileMapArgs t{};
     t.tiles_m = (int)((a.M + bm - 1) / bm);
     t.tiles_n = (int)((a.N + bn - 1) / bn);

@@ -666,14 +666,9 @@ __global__ void copy_state_kernel(const float* h0, float* hT, int64_t n) {
 }  // namespace
 
 int gru_blocks_per_cu(int w_type, size_t lds) {
-    int n = 0;
     const void* fn = w_type == kBF16 ? reinterpret_cast<const void*>(gru_recurrent_kernel<bf16_t>)
                                      : reinterpret_cast<const void*>(gru_recurrent_kernel<float>);
-    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, 64 * kWaves, lds) != hipSuccess) {
-        (void)hipGetLastError();
-        return 1;
-    }
+    const int n = resident_per_cu(fn, 64 * kWaves, lds);
     return n > 0 ? n : 1;
 }
 
@@ -713,7 +708,7 @@ hipError_t launch_gru_group(const GruArgs& a, hipStream_t s) {
         a.n_wg != a.xcds * P * ((a.groups + a.xcds - 1) / a.xcds) || a.n_wg > kGruMaxWgs)
         return hipErrorInvalidValue;
     const size_t lds = gru_group_lds_bytes();
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = ensure_dynamic_lds(fn, lds);
     if (e != hipSuccess) return e;
     int64_t n = a.batch * a.H;
     int blocks = (int)((n + 255) / 256);
@@ -737,14 +732,7 @@ int gru_group_blocks_per_cu(int64_t H) {
         case 4: fn = reinterpret_cast<void*>(gru_group_kernel<4>); break;
         default: return 0;
     }
-    int n = 0;
-    const size_t lds = gru_group_lds_bytes();
-    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, 64 * kGWaves, lds) != hipSuccess) {
-        (void)hipGetLastError();
-        return 0;
-    }
-    return n;
+    return resident_per_cu(fn, 64 * kGWaves, gru_group_lds_bytes());
 }
 
 size_t gru_lds_bytes(int w_type, int64_t H, int J) {
@@ -757,7 +745,7 @@ hipError_t launch_gru_recurrent(const GruArgs& a, hipStream_t s) {
     const size_t lds = gru_lds_bytes(a.w_type, a.H, a.units_per_wg);
     void* fn = a.w_type == kBF16 ? reinterpret_cast<void*>(gru_recurrent_kernel<bf16_t>)
                                  : reinterpret_cast<void*>(gru_recurrent_kernel<float>);
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = ensure_dynamic_lds(fn, lds);
     if (e != hipSuccess) return e;
     int64_t n = a.batch * a.H;
     int blocks = (int)((n + 255) / 256);

@@ -85,6 +85,13 @@ hipError_t launch_skinny_rows(const GemmArgs& a, hipStream_t s);
 hipError_t launch_narrow(const GemmArgs& a, hipStream_t s);
 
 void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk);
+
+// Launch facts cached per device and kernel (launch_cache.cpp): raise a
+// kernel's dynamic-LDS limit to at least `lds` bytes, and its resident
+// workgroups per CU at `threads` threads and `lds` dynamic LDS bytes (0 when
+// the runtime cannot say).
+hipError_t ensure_dynamic_lds(const void* fn, size_t lds);
+int resident_per_cu(const void* fn, int threads, size_t lds);
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
 
 // Depthwise kh x kw convolution, NHWC.  Y is [batch][Ho][Wo][C*cm] in y_type.

@@ -647,7 +647,7 @@ hipError_t launch_narrow(const GemmArgs& a, hipStream_t s) {
     const size_t lds = std::max<size_t>((size_t)ks * a.N * es, kNarrowWaves * kNarrowRows * 7 * sizeof(float));
     const void* fn = a.ab_type == kBF16 ? reinterpret_cast<const void*>(narrow_kernel<uint16_t>)
                                         : reinterpret_cast<const void*>(narrow_kernel<float>);
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = ensure_dynamic_lds(fn, lds);
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)((a.M + kNarrowRows - 1) / kNarrowRows)), block(64 * kNarrowWaves);
     if (a.ab_type == kBF16) hipLaunchKernelGGL(narrow_kernel<uint16_t>, grid, block, lds, s, a, (int)ks);
