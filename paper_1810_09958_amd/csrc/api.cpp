@@ -263,29 +263,40 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     if (p.k_splits == 2 && p.tile == kTile256x256 && tiles(kTile256x256) % xcds == 0) p.fixup = 1;
     if (const char* env = getenv("ISAM_GEMM_CONFIG"))
         if (strstr(env, "fixup=0")) p.fixup = 0;
-    // Stream-K (bf16, the three-stage-ring tiles, no K split): every
-    // workgroup of a persistent grid takes an equal share of the (tile, K
-    // tile) units.  Taken by itself for 256x256 tiles when the tiles exceed
-    // the grid by at most a tenth (a second round would keep under 10 % of the
-    // CUs busy; measured, bf16: 4352x4096x3008 113 us against 135,
-    // 4352x4096x1024 51 against 54).  Larger shares lose to the plain grid:
-    // the workgroups of an XCD then walk K at different offsets, their A and
-    // B slices no longer coincide in L2 and every unit takes longer
-    // (4608x4352x2048, 1.2 tiles per workgroup: 108 against 97 us).
-    // ISAM_GEMM_CONFIG sk=0 / sk=1 switch it off / force it for any such plan.
-    // The kernel deals each XCD's range of tiles to that XCD's workgroups:
-    // every workgroup must get at least one (tile, K tile) unit, and the unit
-    // count must stay below 2^31.
+    // Stream-K (bf16, the three-stage-ring tiles, no K split): a persistent
+    // grid; each XCD's range of tiles runs its whole rounds one tile per
+    // workgroup, then deals the remaining tiles' (tile, K tile) units to its
+    // workgroups in equal shares.  Taken by itself for 256x256 tiles when at
+    // least one whole round exists and the last, partial round would keep at
+    // most a quarter of the CUs busy, in one of two forms (measured, bf16,
+    // plain grid / stream-K / hipBLASLt, µs):
+    //   * shares of at least 8 K tiles: the whole rounds run first
+    //     (4352x4352x4096 178 / 161 / 163, 6144x6144x4096 290 / 261 / 265,
+    //     8192x4608x2048 154-176 / 153-161 / 151);
+    //   * a remainder of at most an eighth of a round: it joins the last whole
+    //     round (sk_keep = 1), every share 1-1.125 tiles (4352x4096x3008 133 /
+    //     111 / 122, 4352x4096x1024 55 / 51 / 55; cut into one-unit shares
+    //     instead, 4352x4096x1024 took 95 µs exchanging partial sums).
+    // Otherwise the plain grid: with shares of a fraction of a tile, or of
+    // 1.2 tiles, the workgroups of an XCD walk K at different offsets and lose
+    // L2 reuse (4608x4352x2048: 97-104 against 103-108; 5000^3, half a round
+    // left: 247-272 against 265-278).  ISAM_GEMM_CONFIG sk=0 / sk=1 switch it
+    // off / force it (forced, the form follows the same rule; with fewer tiles
+    // than workgroups every tile is shared).
     if (ab_type == kBF16 && p.k_splits == 1 && gemm_sk_tile(p.tile) && K > 0) {
         const int G = gemm_sk_grid(p.tile, cus);
-        const int parts = G % 8 == 0 ? 8 : 1;
+        const int parts = G % 8 == 0 ? 8 : 1, gx = G / parts;
         const int64_t nt = tiles(p.tile), nkt = cdiv(K, 64);
-        const bool fits = (nt / parts) * nkt >= G / parts && nt * nkt < (int64_t(1) << 31);
+        const int64_t tx = nt / parts, full = tx / gx, rem = tx - full * gx;
+        const bool fits = nt * nkt < (int64_t(1) << 31);
+        const bool long_shares = rem * nkt >= 8 * (int64_t)gx, small_rem = rem * 8 <= gx;
         const char* env = getenv("ISAM_GEMM_CONFIG");
         const bool off = env && strstr(env, "sk=0"), force = env && strstr(env, "sk=1");
-        if (fits && !off && (force || (p.tile == kTile256x256 && nt > G && nt * 10 <= (int64_t)G * 11))) {
+        const bool pays = p.tile == kTile256x256 && full >= 1 && rem > 0 && rem * 4 <= gx && (long_shares || small_rem);
+        if (fits && !off && (force || pays)) {
             p.sk = 1;
             p.sk_grid = G;
+            p.sk_keep = (full >= 1 && !long_shares) ? 1 : 0;
         }
     }
     return p;

@@ -151,6 +151,7 @@ static bool launch_gemm_sk(const GemmArgs& a, const GemmPlan& p, hipStream_t s, 
     t.k_per_split = a.K;
     t.sk_parts = p.sk_grid % 8 == 0 ? 8 : 1;
     t.sk_nkt = (int)((a.K + 63) / 64);
+    t.sk_keep = p.sk_keep;
     t.epoch = next_fixup_epoch();
     t.expect = t.epoch;
     t.wait_ticks = kFixupTimeoutTicks;

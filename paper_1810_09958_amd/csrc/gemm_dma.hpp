@@ -686,10 +686,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
 // products of one output tile summed as in its Fig. 2).  One workgroup per
 // CU (two for 128x128 tiles, whose ring takes half the LDS), persistent.
 // The tiles are cut into sk_parts contiguous ranges, one per XCD (workgroup b
-// runs on XCD b % sk_parts under the round-robin dispatch), and the (tile,
-// 64-deep K tile) units of a range are dealt to that XCD's workgroups in
-// equal contiguous runs, so each workgroup computes about the same number of
-// MFMAs.  A run is a sequence of segments, each one tile's K range [kt0, kt1):
+// runs on XCD b % sk_parts under the round-robin dispatch).  The whole rounds
+// the range fills go first (all but the last when sk_keep = 1), one whole
+// tile per workgroup and round (so the workgroups of an XCD walk K together
+// and share their A and B slices in L2); the (tile, 64-deep K tile) units of
+// the remaining tiles are then dealt to the XCD's workgroups in equal
+// contiguous runs, so each workgroup computes about the same number of MFMAs.  A run is a sequence of
+// segments, each one tile's K range [kt0, kt1):
 //   * kt0 > 0 (only a run's first segment can start inside a tile): the
 //     workgroup leaves its sums in its partial-sum slot (tile layout) and
 //     raises its flag;
@@ -720,22 +723,36 @@ __global__ __launch_bounds__(64 * WM * WN, BM == 128 ? 2 : 1) void gemm_dma_sk_k
 
     const int parts = tmap.sk_parts, nkt = tmap.sk_nkt;
     const int x = (int)blockIdx.x % parts, li = (int)blockIdx.x / parts, gx = (int)gridDim.x / parts;
-    // (the host keeps tiles * K tiles below 2^31 and gives every workgroup at
-    // least one unit, so runs are never empty)
     const int tiles = tmap.tiles_m * tmap.tiles_n;
     const int t_lo = x * tiles / parts, t_hi = (x + 1) * tiles / parts;
-    const int units = (t_hi - t_lo) * nkt, base = units / gx, rem = units - base * gx;
+    // Whole rounds first (every workgroup one whole tile per round, all of
+    // them walking K together), then the remaining tiles' units in runs; with
+    // sk_keep = 1 the last whole round joins the runs, so a small remainder is
+    // not cut into many short shares.  (The host keeps tiles * K tiles below
+    // 2^31.  With fewer remaining units than workgroups the last workgroups'
+    // runs are empty and start at the end of the last tile, so no owner counts
+    // them as contributors.)
+    const int full = max(0, (t_hi - t_lo) / gx - tmap.sk_keep), s_lo = t_lo + full * gx;
+    const int units = (t_hi - s_lo) * nkt, base = units / gx, rem = units - base * gx;
     auto run_begin = [&](int i) { return i * base + min(i, rem); };
 
     f32x16_t acc[MI][NI];
     int u = run_begin(li);
     const int u_end = run_begin(li + 1);
-    while (u < u_end) {
-        const int tl = u / nkt;
-        const int kt0 = u - tl * nkt;
-        const int kt1 = min(nkt, kt0 + (u_end - u));
+    for (int r = 0; r < full || u < u_end;) {
+        int tile, tl = 0, kt0 = 0, kt1 = nkt;
+        if (r < full) {
+            tile = t_lo + r * gx + li;
+            ++r;
+        } else {
+            tl = u / nkt;
+            kt0 = u - tl * nkt;
+            kt1 = min(nkt, kt0 + (u_end - u));
+            tile = s_lo + tl;
+            u += kt1 - kt0;
+        }
         int tm, tn;
-        tile_coords(tmap, t_lo + tl, tm, tn);
+        tile_coords(tmap, tile, tm, tn);
         const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
         const int64_t kbeg = (int64_t)kt0 * BK, kend = min(a.K, (int64_t)kt1 * BK);
         // The lane index goes through an empty asm each segment, so the
@@ -770,7 +787,6 @@ __global__ __launch_bounds__(64 * WM * WN, BM == 128 ? 2 : 1) void gemm_dma_sk_k
             store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, ln, true, ex);
         }
         __syncthreads();  // the next segment's copies overwrite the stages / staging rows
-        u += kt1 - kt0;
     }
 }
 

@@ -156,6 +156,7 @@ struct TileMapArgs {
     // wait_ticks / flags protocol as the two-slice sum, one flag line and one
     // partial-sum tile per workgroup.
     int sk_parts, sk_nkt;
+    int sk_keep;  // whole rounds left to the stream-K share (0 or 1; see the kernel)
 };
 
 // Output tile number `tile` in the grouped rasterisation: groups of group_m

@@ -58,6 +58,7 @@ struct GemmPlan {
     int sk;          // 1: stream-K schedule of the direct-to-LDS kernel (persistent grid of
                      //    sk_grid workgroups sharing the (tile, K tile) units evenly)
     int sk_grid;
+    int sk_keep;     // whole rounds left to the stream-K shares (0 or 1)
 };
 // Stream-K schedule: persistent grid size for a tile shape (one workgroup per
 // CU; two for 128x128 tiles, whose ring takes half the LDS) and its workspace

@@ -240,10 +240,25 @@ def test_stream_k_every_element(tile, M, N, tb, K, monkeypatch, capfd):
     assert "stream-K" in capfd.readouterr().err
 
 
-# The planner takes stream-K by itself where 256x256 tiles exceed the grid by at most a tenth
-# (272 tiles on 256 workgroups), K a multiple of 64 and ragged.  Every element, and
-# bit-identical on a second call.
-@pytest.mark.parametrize("shape", [(4352, 4096, 1024), (4352, 4096, 1000)])
+# Whole rounds first, then the remaining tiles' units in shares: 4352 x 4352 (289 tiles of
+# 256x256, 36-37 per XCD on 32 workgroups) with K deep enough (64 K tiles) that the 4-5
+# remaining tiles are shared without the last whole round.  Forced, both output types, K a
+# multiple of 64 and ragged; every element.
+@pytest.mark.parametrize("K", [4096, 4040])
+def test_stream_k_whole_rounds_first_every_element(K, monkeypatch, capfd):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,sk=1")
+    monkeypatch.setenv("ISAM_LOG", "1")
+    for ct in ("f32", "bf16"):
+        _run_case(4352, 4352, K, "bf16", ct, seed=K + (ct == "bf16"))
+    assert "stream-K" in capfd.readouterr().err
+
+
+# The planner takes stream-K by itself for 256x256 tiles when at least one whole round exists
+# and the last round would keep at most a quarter of the CUs busy: 4352 x 4096 (272 tiles; the
+# small remainder joins the last whole round) with K a multiple of 64 and ragged, and
+# 4352 x 4352 x 4096 (289 tiles; whole round first).  Every element, and bit-identical on a
+# second call.
+@pytest.mark.parametrize("shape", [(4352, 4096, 1024), (4352, 4096, 1000), (4352, 4352, 4096)])
 def test_stream_k_planned_every_element(shape, monkeypatch, capfd):
     monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
     monkeypatch.setenv("ISAM_LOG", "1")
