@@ -78,20 +78,35 @@ typedef enum {
  * units idle in a last partial round (A not transposed, 16-byte aligned
  * rows, workspace 256-byte aligned) run a stream-K schedule instead
  * (Section 3.4's allocation of work to processing units): a persistent grid
- * sized to what the device holds at once, each workgroup an equal share of
- * the (output tile, 64-deep K tile) units, the workgroups of one XCD
- * splitting that XCD's range of tiles; a tile's owner starts from the
- * partial sums the later shares of its K range left in the workspace (one
- * fp32 tile and one flag line per workgroup), added in a fixed order, with
- * the same bounded wait and NaN on expiry.  The workspace needs no initial
- * contents; concurrent calls must not share one.
+ * sized to what the device holds at once, the workgroups of one XCD splitting
+ * that XCD's range of tiles: whole tiles round by round first, then equal
+ * shares of the remaining (output tile, 64-deep K tile) units; a tile's owner
+ * starts from the partial sums the later shares of its K range left in the
+ * workspace (one fp32 tile and one flag line per workgroup), added in a fixed
+ * order, with the same bounded wait and NaN on expiry.
+ * Operands whose rows cannot be copied 16 bytes at a time (K, or M with
+ * trans_a / N without trans_b, not a multiple of 8 bf16 / 4 fp32 values, or a
+ * base pointer or leading dimension off 16 bytes), and bf16 A with trans_a,
+ * are first copied into the start of the workspace when the product is large
+ * enough for the large tiles and the workspace (256-byte aligned) holds the
+ * copies: A as [M][Kp], B as [Kp][N] (trans_b = 0, N a multiple of the vector
+ * width) or [N][Kp], each rounded up to 256 bytes, with zeros in the padded K
+ * positions (Kp: K rounded up to the vector width, or to a multiple of 64 when
+ * both operands are copied and that adds at most K/16); the rest of the
+ * workspace serves the packed product as above.  isam_gemm_workspace_size
+ * includes these bytes when the sizes alone call for them; a caller passing
+ * misaligned pointers or leading dimensions adds them itself, or the product
+ * runs on the element-wise tile kernel.  A workspace that overlaps A, B or C
+ * is rejected.  The workspace needs no initial contents; concurrent calls
+ * must not share one.
  */
 isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                         int ab_type, const void* A, int64_t lda, const void* B, int64_t ldb,
                         int accumulate, int c_type, void* C, int64_t ldc,
                         void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace (bytes) the preferred plan of isam_gemm needs for these sizes; 0 if none. */
+/* Workspace (bytes) the preferred plan of isam_gemm needs for these sizes (split-K or
+ * stream-K partial sums, packed operand copies); 0 if none. */
 size_t isam_gemm_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                                 int ab_type, int c_type);
 

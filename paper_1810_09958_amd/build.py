@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libisam.so")
-SOURCES = ["api.cpp", "launch_cache.cpp", "gemm.hip", "gemm_bf16.hip", "gemm_f32.hip", "gemm_dma.hip", "gemm_dma_sk.hip", "gemm_small.hip", "gemm_stream.hip", "skinny.hip", "dwconv.hip", "dwsep_fused.hip", "dwsep_fused_f32.hip", "gru.hip"]
+SOURCES = ["api.cpp", "launch_cache.cpp", "gemm.hip", "gemm_bf16.hip", "gemm_f32.hip", "gemm_dma.hip", "gemm_dma_sk.hip", "gemm_small.hip", "gemm_stream.hip", "pack.hip", "skinny.hip", "dwconv.hip", "dwsep_fused.hip", "dwsep_fused_f32.hip", "gru.hip"]
 ARCH = "gfx950"
 
 

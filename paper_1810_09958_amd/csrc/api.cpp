@@ -45,12 +45,10 @@ isam_status_t hip_fail(hipError_t e, const char* what) {
     return fail(ISAM_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Read at every call (as the kernel-side log lines do), so a process can switch it.
 bool log_enabled() {
-    static const bool on = [] {
-        const char* v = getenv("ISAM_LOG");
-        return v && v[0] && v[0] != '0';
-    }();
-    return on;
+    const char* v = getenv("ISAM_LOG");
+    return v && v[0] && v[0] != '0';
 }
 
 bool valid_dtype(int t) { return t == ISAM_F32 || t == ISAM_BF16; }
@@ -322,6 +320,75 @@ bool vec_ok(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_ty
     return true;
 }
 
+// Operands whose rows cannot be fetched in 16-byte pieces are copied into the
+// workspace first (pack.hip), so that the product runs on the MFMA kernels that
+// copy 16 bytes at a time instead of the element-wise tile kernel (bf16
+// 8192x8192x8100: 13.8 ms there).  A packed A is [M][Kp] (K-contiguous, also
+// when it was given transposed); a packed B keeps its layout when its rows can
+// be padded ([N][Kp], or [Kp][N] with N a multiple of the vector width) and is
+// transposed to [N][Kp] otherwise.  Kp is K rounded up to the vector width (to
+// a multiple of 64 when both operands are copied and that adds at most 1/16);
+// the padded K positions are zero in both operands.  bf16 A given as [K][M] is
+// copied too, transposed, for the direct-to-LDS kernels.  Only products that the
+// planner would give large tiles are packed (the copies cost about as much as
+// reading and writing both operands once).
+struct PackPlan {
+    bool pays = false;
+    bool a = false, b = false;        // operand copied
+    bool a_tr = false, b_tr = false;  // copied with a transpose
+    int trans_a = 0, trans_b = 0;     // layouts of the product that follows
+    int64_t Kp = 0;
+    int64_t b_rows = 0, b_cols = 0;   // packed B
+    size_t a_bytes = 0, b_bytes = 0;  // each a multiple of 256
+};
+
+PackPlan pack_plan(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type, bool a_mis, bool b_mis) {
+    PackPlan k;
+    const int64_t E = ab_type == ISAM_BF16 ? 8 : 4, es = (int64_t)dsize(ab_type);
+    auto al = [](int64_t v) { return (size_t)((v + 255) & ~(int64_t)255); };
+    k.Kp = cdiv(K, E) * E;
+    k.a = a_mis || k.Kp != K;
+    k.b = b_mis || k.Kp != K;
+    // Both copied: pad K to whole 64-deep tiles when that adds at most 1/16
+    // (the kernels' whole-tile instance takes no per-copy range checks).
+    if (k.a && k.b && (cdiv(K, 64) * 64 - K) * 16 <= K) k.Kp = cdiv(K, 64) * 64;
+    k.trans_a = trans_a;
+    k.trans_b = trans_b;
+    if (k.a) {
+        k.a_tr = trans_a != 0;
+        k.trans_a = 0;
+        k.a_bytes = al(M * k.Kp * es);
+    }
+    if (k.b) {
+        if (trans_b || N % E == 0) {
+            k.b_rows = trans_b ? N : k.Kp;
+            k.b_cols = trans_b ? k.Kp : N;
+        } else {
+            k.b_tr = true;
+            k.trans_b = 1;
+            k.b_rows = N;
+            k.b_cols = k.Kp;
+        }
+        k.b_bytes = al(k.b_rows * k.b_cols * es);
+    }
+    const GemmPlan q = plan_gemm(M, N, k.Kp, ab_type, device_cus());
+    const bool big = !q.small && !q.skinny && q.tile != kTile64x64 && q.tile != kTile128x32;
+    const bool fits = (int64_t)k.a_bytes <= kMaxExtent && (int64_t)k.b_bytes <= kMaxExtent;
+    const char* env = getenv("ISAM_GEMM_CONFIG");
+    k.pays = (k.a || k.b) && big && fits && !(env && strstr(env, "pack=0"));
+    return k;
+}
+
+bool pack_a_needed(int trans_a, int64_t M, int64_t K, int ab_type, const void* A, int64_t lda) {
+    const int64_t E = ab_type == ISAM_BF16 ? 8 : 4, es = (int64_t)dsize(ab_type);
+    return ((uintptr_t)A & 15) || (lda * es) % 16 || (trans_a ? M : K) % E;
+}
+
+bool pack_b_needed(int trans_b, int64_t N, int64_t K, int ab_type, const void* B, int64_t ldb) {
+    const int64_t E = ab_type == ISAM_BF16 ? 8 : 4, es = (int64_t)dsize(ab_type);
+    return ((uintptr_t)B & 15) || (ldb * es) % 16 || (trans_b ? K : N) % E;
+}
+
 isam_status_t validate_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int ab_type,
                             const void* A, int64_t lda, const void* B, int64_t ldb, int accumulate,
                             int c_type, const void* C, int64_t ldc, const char* who) {
@@ -373,6 +440,47 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         p.sk = 0;
     }
     p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
+    // bf16 A given as [K][M] is also copied (transposed): the direct-to-LDS
+    // kernels need A K-contiguous (4096^3 with A transposed: 197 us on the
+    // vector tile kernel, 141 us with the copy).
+    if ((!p.vec || (trans_a && ab_type == kBF16)) && batch == 1 && K > 0) {
+        const PackPlan k = pack_plan(trans_a, trans_b, M, N, K, ab_type,
+                                     (trans_a && ab_type == kBF16) || pack_a_needed(trans_a, M, K, ab_type, A, lda),
+                                     pack_b_needed(trans_b, N, K, ab_type, B, ldb));
+        const size_t pack_bytes = k.a_bytes + k.b_bytes;
+        char* ws = static_cast<char*>(workspace);
+        if (k.pays && ws && ((uintptr_t)ws & 255) == 0 && workspace_bytes >= pack_bytes) {
+            const int64_t es = (int64_t)dsize(ab_type);
+            const void* Ap = k.a ? ws : A;
+            const void* Bp = k.b ? ws + k.a_bytes : B;
+            const int64_t ldap = k.a ? k.Kp : lda, ldbp = k.b ? k.b_cols : ldb;
+            if (vec_ok(k.trans_a, k.trans_b, M, N, k.Kp, ab_type, Ap, ldap, Bp, ldbp)) {
+                const size_t a_b = (size_t)((trans_a ? (K - 1) * lda + M : (M - 1) * lda + K) * es);
+                const size_t b_b = (size_t)((trans_b ? (N - 1) * ldb + K : (K - 1) * ldb + N) * es);
+                const size_t c_b = (size_t)((M - 1) * ldc + N) * dsize(c_type);
+                if (overlaps(ws, pack_bytes, A, a_b) || overlaps(ws, pack_bytes, B, b_b) ||
+                    overlaps(ws, pack_bytes, C, c_b))
+                    return fail(ISAM_ERR_INVALID_ARG, "%s: workspace overlaps A, B or C", who);
+                if (log_enabled())
+                    fprintf(stderr, "[isam] %s packed operands: A %d%s, B %d%s, K %lld -> %lld\n", who, (int)k.a,
+                            k.a_tr ? " (transposed)" : "", (int)k.b, k.b_tr ? " (transposed)" : "", (long long)K,
+                            (long long)k.Kp);
+                const int cus = device_cus();
+                hipError_t e = hipSuccess;
+                if (k.a)
+                    e = k.a_tr ? launch_pack(A, K, M, lda, ws, M, k.Kp, (int)es, true, cus, stream)
+                               : launch_pack(A, M, K, lda, ws, M, k.Kp, (int)es, false, cus, stream);
+                if (e == hipSuccess && k.b)
+                    e = trans_b || !k.b_tr ? launch_pack(B, trans_b ? N : K, trans_b ? K : N, ldb, ws + k.a_bytes,
+                                                         k.b_rows, k.b_cols, (int)es, false, cus, stream)
+                                           : launch_pack(B, K, N, ldb, ws + k.a_bytes, k.b_rows, k.b_cols, (int)es,
+                                                         true, cus, stream);
+                if (e != hipSuccess) return hip_fail(e, who);
+                return run_gemm(k.trans_a, k.trans_b, M, N, k.Kp, ab_type, Ap, ldap, Bp, ldbp, accumulate, c_type, C,
+                                ldc, bias, ws + pack_bytes, workspace_bytes - pack_bytes, stream, who);
+            }
+        }
+    }
     if (p.skinny == 4) {
         // the narrow kernel reads A in 16-byte pieces and B element-wise
         const int64_t es = (int64_t)dsize(ab_type);
@@ -480,11 +588,22 @@ isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t 
 
 size_t isam_gemm_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                                 int ab_type, int c_type) {
-    (void)trans_a;
-    (void)trans_b;
     (void)c_type;
     if (M <= 0 || N <= 0 || K <= 0 || !valid_dtype(ab_type)) return 0;
-    return gemm_ws_bytes(plan_gemm(M, N, K, ab_type, device_cus()), M, N);
+    if ((trans_a != 0 && trans_a != 1) || (trans_b != 0 && trans_b != 1)) return 0;
+    size_t ws = gemm_ws_bytes(plan_gemm(M, N, K, ab_type, device_cus()), M, N);
+    // Rows that the sizes alone make unfit for 16-byte copies (a contiguous
+    // dimension off the vector width), and bf16 A given as [K][M]: room to pack
+    // them, and what the packed product then uses.
+    const int64_t E = ab_type == ISAM_BF16 ? 8 : 4;
+    const bool a_mis = (trans_a ? M : K) % E != 0 || (trans_a && ab_type == ISAM_BF16),
+               b_mis = (trans_b ? K : N) % E != 0;
+    if (a_mis || b_mis) {
+        const PackPlan k = pack_plan(trans_a, trans_b, M, N, K, ab_type, a_mis, b_mis);
+        if (k.pays)
+            ws = std::max(ws, k.a_bytes + k.b_bytes + gemm_ws_bytes(plan_gemm(M, N, k.Kp, ab_type, device_cus()), M, N));
+    }
+    return ws;
 }
 
 static bool dw_out_dims(int64_t H, int64_t W, int64_t kh, int64_t kw, int64_t stride, int64_t pad,

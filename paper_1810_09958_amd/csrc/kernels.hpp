@@ -94,6 +94,12 @@ void tile_dims(int tile, int ab_type, int* bm, int* bn, int* bk);
 hipError_t ensure_dynamic_lds(const void* fn, size_t lds);
 int resident_per_cu(const void* fn, int threads, size_t lds);
 hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
+// Copies src[s_rows][s_cols] (leading dimension ld, elements of esize = 2 or 4
+// bytes) into the dense dst[d_rows][d_cols] -- transposed (dst[i][j] =
+// src[j][i]) if asked -- with zeros outside the source; d_cols * esize must
+// be a multiple of 16 and dst 16-byte aligned for the plain copy.
+hipError_t launch_pack(const void* src, int64_t s_rows, int64_t s_cols, int64_t ld, void* dst, int64_t d_rows,
+                       int64_t d_cols, int esize, bool transpose, int cus, hipStream_t s);
 
 // Depthwise kh x kw convolution, NHWC.  Y is [batch][Ho][Wo][C*cm] in y_type.
 struct DwArgs {

@@ -90,6 +90,47 @@ def test_gemm_splitk_workspace_must_not_overlap_operands(L):
         assert b"workspace overlaps" in L.isam_last_error()
 
 
+def test_gemm_workspace_query_covers_packing(L, monkeypatch):
+    # A contiguous dimension off the vector width (8 bf16 / 4 fp32 values): room for the
+    # packed operands with K rounded up (A as [M][Kp]; B as [Kp][N], or [N][Kp] when N is
+    # off the vector width), each a multiple of 256 bytes, plus what the packed product
+    # uses itself.  Kp: a multiple of 64 when both are copied and that adds at most K/16.
+    # Only B copied, K unchanged (N off the vector width), or A only (A transposed).
+    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 1001, BF16, BF16) == 2 * (2048 * 1024 * 2)
+    assert L.isam_gemm_workspace_size(1, 1, 2048, 2048, 1001, BF16, F32) == 2 * (2048 * 1024 * 2)
+    assert L.isam_gemm_workspace_size(0, 0, 8192, 8192, 8100, BF16, BF16) == 2 * (8192 * 8128 * 2)
+    assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 1001, F32, F32) == 2 * (2048 * 1024 * 4)
+    # K = 961: a multiple of 64 (1024) would add more than 1/16, so the vector width (968)
+    assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 961, BF16, BF16) == 2 * (2048 * 968 * 2)
+    assert L.isam_gemm_workspace_size(0, 0, 2048, 2044, 1024, BF16, BF16) == 2044 * 1024 * 2
+    assert L.isam_gemm_workspace_size(1, 0, 2044, 2048, 1024, BF16, BF16) == 2044 * 1024 * 2
+    # deep K: the packed product is split along K and its partial sums follow the copies
+    assert L.isam_gemm_workspace_size(0, 0, 1024, 1024, 4101, BF16, BF16) == \
+        2 * (1024 * 4160 * 2) + 8 * 1024 * 1024 * 4
+    # bf16 A given as [K][M] is copied transposed (fp32 is not)
+    assert L.isam_gemm_workspace_size(1, 0, 4096, 4096, 4096, BF16, BF16) == 4096 * 4096 * 2
+    assert L.isam_gemm_workspace_size(1, 1, 4096, 4096, 4096, BF16, F32) == 4096 * 4096 * 2
+    assert L.isam_gemm_workspace_size(1, 0, 4096, 4096, 4096, F32, F32) == 0
+    # products too small for the large tiles are not packed
+    assert L.isam_gemm_workspace_size(0, 0, 100, 100, 101, BF16, BF16) == 0
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "pack=0")
+    assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 1001, BF16, BF16) == 0
+
+
+def test_gemm_pack_workspace_must_not_overlap_operands(L, monkeypatch):
+    # The packed copies go to the start of the workspace: one that overlaps A, B or C is
+    # rejected before anything is launched.
+    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    M, N, K = 2048, 2048, 1001
+    need = L.isam_gemm_workspace_size(0, 0, M, N, K, BF16, BF16)
+    A, B, C = (ctypes.c_void_p(v) for v in (0x100000000, 0x200000000, 0x300000000))
+    for ws in (C, A, B):
+        assert gemm(L, M=M, N=N, K=K, ab=BF16, A=A, lda=K, B=B, ldb=N, ct=BF16, C=C, ldc=N,
+                    ws=ws, wsb=need) == INVALID
+        assert b"workspace overlaps" in L.isam_last_error()
+
+
 def test_gemm_empty_is_noop(L):
     assert gemm(L, M=0, A=None, B=None, C=None) == OK
     assert gemm(L, N=0, A=None, B=None, C=None) == OK

@@ -361,7 +361,7 @@ def _guarded_gemm(M, N, K, dt, ct, pad_cols, seed, tb=0, env=None, monkeypatch=N
 
 
 GUARD_CASES = ["dma256", "dma256_split", "dma256_split_sum", "dma128", "dma_sk", "skinny_rows", "skinny_split",
-               "narrow", "stream", "tile_f32", "small"]
+               "narrow", "stream", "tile_f32", "small", "packed"]
 
 
 @pytest.mark.parametrize("ct", ["f32", "bf16"])
@@ -383,6 +383,7 @@ def test_guard_bands_every_kernel(ct, case, monkeypatch):
         "stream": dict(M=300, N=72, K=96, dt="bf16", env="stream=1"),
         "tile_f32": dict(M=300, N=200, K=130, dt="f32", env=None),
         "small": dict(M=100, N=64, K=520, dt="f32", env=None),
+        "packed": dict(M=2048, N=2040, K=1001, dt="bf16", env=None),
     }
     c = cases[case]
     _guarded_gemm(c["M"], c["N"], c["K"], c["dt"], ct, pad_cols=8, seed=100 + GUARD_CASES.index(case),
@@ -469,6 +470,96 @@ def test_dma_128_tile_copy_modes(K, tb):
     ref, S = oracle.gemm(np.ascontiguousarray(A_h[rows]), Bm, len(rows), N, K)
     got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
     assert norm_err(got, ref, S) <= TOL_BF16
+
+
+# Operands whose rows cannot be copied 16 bytes at a time (K or the contiguous M / N off the
+# vector width, a leading dimension or base pointer off 16 bytes) are packed into the
+# workspace with zero-padded K and run on the MFMA kernels; every element against the oracle.
+def _packed_case(M, N, K, dt, ct, ta, tb, monkeypatch, capfd, a_shift=0, ld_pad=0, accumulate=False,
+                 expect_pack=True, workspace=None, seed=0):
+    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    monkeypatch.setenv("ISAM_LOG", "1")
+    Am = synth.uniform(seed, 50, (M, K), -1, 1)
+    Bm = synth.uniform(seed, 51, (K, N), -1, 1)
+    A_host = np.ascontiguousarray(Am.T) if ta else Am
+    B_host = np.ascontiguousarray(Bm.T) if tb else Bm
+    if ld_pad:
+        A_host = np.pad(A_host, ((0, 0), (0, ld_pad)), constant_values=5.0)
+        B_host = np.pad(B_host, ((0, 0), (0, ld_pad)), constant_values=-5.0)
+    if dt == "bf16":
+        A_host, B_host = bits(A_host), bits(B_host)
+    A_flat = to_gpu(np.concatenate([np.zeros(a_shift, A_host.dtype), A_host.ravel()]))
+    A = A_flat[a_shift:].view(A_host.shape)
+    B = to_gpu(B_host)
+    if ld_pad:
+        A = A[:, : A.shape[1] - ld_pad]
+        B = B[:, : B.shape[1] - ld_pad]
+    tdt = torch.bfloat16 if ct == "bf16" else torch.float32
+    C_in = None
+    if accumulate:
+        c0 = synth.uniform(seed, 52, (M, N), -1, 1)
+        C = to_gpu(bits(c0) if ct == "bf16" else c0)
+        C_in = to_host_f64(C)
+        isam.gemm(A, B, C, trans_a=bool(ta), trans_b=bool(tb), accumulate=True, workspace=workspace)
+    else:
+        C = isam.gemm(A, B, trans_a=bool(ta), trans_b=bool(tb), out_dtype=tdt, workspace=workspace)
+    torch.cuda.synchronize()
+    err_log = capfd.readouterr().err
+    assert ("packed operands" in err_log) == expect_pack, err_log[-2000:]
+    ref, S = oracle.gemm(A_host, B_host, M, N, K, ta, tb, lda=A_host.shape[1], ldb=B_host.shape[1], C_in=C_in)
+    tol = TOL_F32 if (dt == "f32" and ct == "f32") else TOL_BF16
+    assert norm_err(to_host_f64(C), ref, S) <= tol
+    return C
+
+
+@pytest.mark.parametrize("dt,ct", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_packed_odd_k_every_element(dt, ct, ta, tb, monkeypatch, capfd):
+    # K = 1001: both operands padded to K = 1024, A transposed into
+    # [M][K] when it is given as [K][M]; 2048^2 takes the 128x128 tiles.  With A [K][M] and
+    # B [K][N] no row runs along K: fp32 is then not packed, bf16 only for A's transpose.
+    _packed_case(2048, 2048, 1001, dt, ct, ta, tb, monkeypatch, capfd,
+                 expect_pack=not (ta and not tb and dt == "f32"))
+
+
+@pytest.mark.parametrize("case", ["n_ragged", "m_ragged_ta", "ta_aligned", "tt_aligned", "a_shift", "ld_odd",
+                                  "accumulate", "deep_k", "k_vector_pad"])
+def test_packed_layouts_every_element(case, monkeypatch, capfd):
+    c = {
+        # B [K][N] with N off the vector width: packed transposed to [N][K]
+        "n_ragged": dict(M=2048, N=2044, K=1024, ta=0, tb=0),
+        # A [K][M] with M off the vector width: packed transposed to [M][K]
+        "m_ragged_ta": dict(M=2044, N=2048, K=1024, ta=1, tb=0),
+        # bf16 A given as [K][M] with aligned rows: copied transposed for the direct-to-LDS kernel
+        "ta_aligned": dict(M=2048, N=2048, K=1024, ta=1, tb=0),
+        "tt_aligned": dict(M=2048, N=2048, K=1024, ta=1, tb=1),
+        # A's base 2 bytes past a 16-byte boundary: only A is copied
+        "a_shift": dict(M=2048, N=2048, K=1024, ta=0, tb=1, a_shift=1),
+        # leading dimensions K + 1 (rows off 16 bytes) in both operands
+        "ld_odd": dict(M=2048, N=2048, K=1024, ta=0, tb=1, ld_pad=1),
+        "accumulate": dict(M=2048, N=2048, K=1001, ta=0, tb=0, accumulate=True),
+        # deep odd K on 256x256 tiles (split along K after packing)
+        "deep_k": dict(M=1024, N=1024, K=4101, ta=0, tb=0),
+        # K padded to the vector width only (968; 1024 would add more than 1/16)
+        "k_vector_pad": dict(M=2048, N=2048, K=961, ta=0, tb=1),
+    }[case]
+    kw = {k: v for k, v in c.items() if k not in ("M", "N", "K", "ta", "tb")}
+    if case in ("a_shift", "ld_odd"):
+        # the sizes-only workspace query cannot see a pointer or leading dimension: the caller
+        # passes room for the copies (here both operands, 2 x 4 MiB)
+        kw["workspace"] = torch.empty(8 << 20, device="cuda", dtype=torch.uint8)
+    _packed_case(c["M"], c["N"], c["K"], "bf16", "bf16", c["ta"], c["tb"], monkeypatch, capfd, **kw)
+
+
+def test_packed_needs_workspace_else_tile_kernel(monkeypatch, capfd):
+    # Without room for the packed copies the element-wise tile kernel runs; same results to
+    # the tolerance, and the sizes-only workspace query covers the packed path.
+    M, N, K = 2048, 2048, 1001
+    assert isam.gemm_workspace_size(M, N, K, 1, 1) == 2 * (2048 * 1024 * 2)
+    tiny = torch.empty(16, device="cuda", dtype=torch.uint8)
+    C0 = _packed_case(M, N, K, "bf16", "bf16", 0, 0, monkeypatch, capfd, expect_pack=False, workspace=tiny)
+    C1 = _packed_case(M, N, K, "bf16", "bf16", 0, 0, monkeypatch, capfd)
+    assert torch.isfinite(C0.float()).all() and torch.isfinite(C1.float()).all()
 
 
 # Very shallow bf16 products (K <= 256, N <= 256 with N % 4 == 0, A and B not transposed): the
