@@ -97,8 +97,18 @@ typedef enum {
  * includes these bytes when the sizes alone call for them; a caller passing
  * misaligned pointers or leading dimensions adds them itself, or the product
  * runs on the element-wise tile kernel.  A workspace that overlaps A, B or C
- * is rejected.  The workspace needs no initial contents; concurrent calls
- * must not share one.
+ * is rejected.
+ * Large fp32 products (A [M][K]; B [N][K], or [K][N] with N a multiple of 8;
+ * M*N >= 512*(M+N); workspace 256-byte aligned and holding the copies) run on
+ * the bf16 matrix cores: each operand value x is split into three bf16 terms
+ * h = bf16(x), m = bf16(x - h), l = bf16(x - h - m), copied into the start of
+ * the workspace as six K blocks (12 bytes per operand value), and one bf16
+ * product over K' = 6*Kp sums hh + hm + mh + hl + lh + mm in fp32: the fp32
+ * product to within the dropped terms (below 2^-23 of |a*b|).  Inputs must be
+ * finite and below 3.39e38 in magnitude there (an infinite input gives NaN
+ * instead of +-inf).  isam_gemm_workspace_size includes these bytes when the
+ * split applies; with a smaller workspace the fp32 tile kernel runs.  The
+ * workspace needs no initial contents; concurrent calls must not share one.
  */
 isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                         int ab_type, const void* A, int64_t lda, const void* B, int64_t ldb,
@@ -106,7 +116,7 @@ isam_status_t isam_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t 
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace (bytes) the preferred plan of isam_gemm needs for these sizes (split-K or
- * stream-K partial sums, packed operand copies); 0 if none. */
+ * stream-K partial sums, packed or split operand copies); 0 if none. */
 size_t isam_gemm_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                                 int ab_type, int c_type);
 

@@ -379,6 +379,41 @@ PackPlan pack_plan(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, in
     return k;
 }
 
+// Large fp32 products run on the bf16 matrix cores: each operand value is
+// split into three bf16 terms (pack.hip) laid out as six K blocks, A as
+// (h, h, m, h, l, m) and B as (h, m, h, l, h, m), so that one bf16 product over
+// K' = 6 Kp forms hh + hm + mh + hl + lh + mm -- the fp32 product to within
+// the dropped terms' 2^-23 relative size, accumulated in fp32.  Six bf16
+// products cost less than a quarter of one fp32 product on the matrix cores
+// (fp32 8192^3: 8.47 ms on the fp32 tile kernel).  Needs A [M][K] (no
+// transpose), B [N][K] or [K][N] with N a multiple of 8, and workspace for
+// the split copies (12 bytes per operand value); only products where the
+// copies cost well under the time saved (M N >= 512 (M + N), large tiles).
+constexpr uint32_t kSplitPatA = 0u | 0u << 2 | 1u << 4 | 0u << 6 | 2u << 8 | 1u << 10;
+constexpr uint32_t kSplitPatB = 0u | 1u << 2 | 0u << 4 | 2u << 6 | 0u << 8 | 1u << 10;
+
+struct SplitPlan {
+    bool pays = false;
+    int64_t Kp = 0;                   // K of each block
+    size_t a_bytes = 0, b_bytes = 0;  // each a multiple of 256
+};
+
+SplitPlan split_plan(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K) {
+    SplitPlan k;
+    if (trans_a || (!trans_b && N % 8) || K <= 0) return k;
+    auto al = [](int64_t v) { return (size_t)((v + 255) & ~(int64_t)255); };
+    k.Kp = cdiv(K, 8) * 8;
+    if ((cdiv(K, 64) * 64 - K) * 16 <= K) k.Kp = cdiv(K, 64) * 64;
+    k.a_bytes = al(M * 6 * k.Kp * 2);
+    k.b_bytes = al(N * 6 * k.Kp * 2);
+    const GemmPlan q = plan_gemm(M, N, 6 * k.Kp, kBF16, device_cus());
+    const bool big = !q.small && !q.skinny && q.tile != kTile64x64 && q.tile != kTile128x32 && q.tile != kTile128x64;
+    const bool fits = (int64_t)k.a_bytes <= kMaxExtent && (int64_t)k.b_bytes <= kMaxExtent;
+    const char* env = getenv("ISAM_GEMM_CONFIG");
+    k.pays = big && fits && M * N >= 512 * (M + N) && !(env && strstr(env, "f32split=0"));
+    return k;
+}
+
 bool pack_a_needed(int trans_a, int64_t M, int64_t K, int ab_type, const void* A, int64_t lda) {
     const int64_t E = ab_type == ISAM_BF16 ? 8 : 4, es = (int64_t)dsize(ab_type);
     return ((uintptr_t)A & 15) || (lda * es) % 16 || (trans_a ? M : K) % E;
@@ -440,6 +475,35 @@ isam_status_t run_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K
         p.sk = 0;
     }
     p.vec = (K == 0) ? 1 : (vec_ok(trans_a, trans_b, M, N, K, ab_type, A, lda, B, ldb) ? 1 : 0);
+    if (ab_type == kF32 && batch == 1 && K > 0) {
+        const SplitPlan k = split_plan(trans_a, trans_b, M, N, K);
+        char* ws = static_cast<char*>(workspace);
+        const size_t split_bytes = k.a_bytes + k.b_bytes;
+        if (k.pays && ws && ((uintptr_t)ws & 255) == 0 && workspace_bytes >= split_bytes) {
+            const int64_t es = (int64_t)dsize(ab_type);
+            const size_t a_b = (size_t)(((M - 1) * lda + K) * es);
+            const size_t b_b = (size_t)((trans_b ? (N - 1) * ldb + K : (K - 1) * ldb + N) * es);
+            const size_t c_b = (size_t)((M - 1) * ldc + N) * dsize(c_type);
+            if (overlaps(ws, split_bytes, A, a_b) || overlaps(ws, split_bytes, B, b_b) ||
+                overlaps(ws, split_bytes, C, c_b))
+                return fail(ISAM_ERR_INVALID_ARG, "%s: workspace overlaps A, B or C", who);
+            if (log_enabled())
+                fprintf(stderr, "[isam] %s fp32 split into bf16 terms: K %lld -> 6 x %lld\n", who, (long long)K,
+                        (long long)k.Kp);
+            const int cus = device_cus();
+            uint16_t* As = reinterpret_cast<uint16_t*>(ws);
+            uint16_t* Bs = reinterpret_cast<uint16_t*>(ws + k.a_bytes);
+            const float* Af = static_cast<const float*>(A);
+            const float* Bf = static_cast<const float*>(B);
+            hipError_t e = launch_split6(Af, M, K, lda, As, M, k.Kp, k.Kp, false, kSplitPatA, cus, stream);
+            if (e == hipSuccess)
+                e = trans_b ? launch_split6(Bf, N, K, ldb, Bs, N, k.Kp, k.Kp, false, kSplitPatB, cus, stream)
+                            : launch_split6(Bf, K, N, ldb, Bs, k.Kp, N, k.Kp, true, kSplitPatB, cus, stream);
+            if (e != hipSuccess) return hip_fail(e, who);
+            return run_gemm(0, trans_b, M, N, 6 * k.Kp, kBF16, As, 6 * k.Kp, Bs, trans_b ? 6 * k.Kp : N, accumulate,
+                            c_type, C, ldc, bias, ws + split_bytes, workspace_bytes - split_bytes, stream, who);
+        }
+    }
     // bf16 A given as [K][M] is also copied (transposed): the direct-to-LDS
     // kernels need A K-contiguous (4096^3 with A transposed: 197 us on the
     // vector tile kernel, 141 us with the copy).
@@ -595,6 +659,12 @@ size_t isam_gemm_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N, 
     // Rows that the sizes alone make unfit for 16-byte copies (a contiguous
     // dimension off the vector width), and bf16 A given as [K][M]: room to pack
     // them, and what the packed product then uses.
+    if (ab_type == ISAM_F32) {
+        const SplitPlan k = split_plan(trans_a, trans_b, M, N, K);
+        if (k.pays)
+            return std::max(ws, k.a_bytes + k.b_bytes +
+                                    gemm_ws_bytes(plan_gemm(M, N, 6 * k.Kp, kBF16, device_cus()), M, N));
+    }
     const int64_t E = ab_type == ISAM_BF16 ? 8 : 4;
     const bool a_mis = (trans_a ? M : K) % E != 0 || (trans_a && ab_type == ISAM_BF16),
                b_mis = (trans_b ? K : N) % E != 0;

@@ -55,6 +55,26 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
 }
 
+// fp32 as the sum of three bf16 terms: h = bf16(x), m = bf16(x - h),
+// l = bf16(x - h - m) (each difference is exact in fp32; |x - h - m - l| is
+// at most 2^-24 |x|).  A product a.b to fp32 accuracy is then the six bf16
+// products hh + hm + mh + hl + lh + mm, every one exact in fp32 (the dropped
+// ml, lm, ll are below 2^-23 |a.b|).
+typedef __bf16 f32s_bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32s_f32x2_t __attribute__((ext_vector_type(2)));
+// Two fp32 values to a bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32s_f32x2_t){lo, hi}, f32s_bf16x2_t));
+}
+// The three bf16 terms of two fp32 values, as packed pairs t[0] (h), t[1] (m), t[2] (l).
+__device__ __forceinline__ void split3_pair(float x0, float x1, uint32_t t[3]) {
+    t[0] = pack_bf16_rne(x0, x1);
+    const float r0 = x0 - __uint_as_float(t[0] << 16), r1 = x1 - __uint_as_float(t[0] & 0xffff0000u);
+    t[1] = pack_bf16_rne(r0, r1);
+    const float q0 = r0 - __uint_as_float(t[1] << 16), q1 = r1 - __uint_as_float(t[1] & 0xffff0000u);
+    t[2] = pack_bf16_rne(q0, q1);
+}
+
 // ---------------------------------------------------------------------------
 // Buffer resources: a raw (stride 0) buffer whose loads past num_records
 // bytes return zero.  Used for ragged tile edges: an out-of-range element is

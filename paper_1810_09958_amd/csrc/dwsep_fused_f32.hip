@@ -54,21 +54,6 @@ constexpr int kYUnit = kR32 * kMaxW * 16 + 64;
 constexpr int kYTerm = 4 * kYUnit;
 constexpr int kYBytes = 3 * kYTerm;
 
-typedef __bf16 f32s_bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32s_f32x2_t __attribute__((ext_vector_type(2)));
-// Two fp32 values to a bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32s_f32x2_t){lo, hi}, f32s_bf16x2_t));
-}
-// The three bf16 terms of two fp32 values, as packed pairs t[0] (h), t[1] (m), t[2] (l).
-__device__ __forceinline__ void split3_pair(float x0, float x1, uint32_t t[3]) {
-    t[0] = pack_bf16_rne(x0, x1);
-    const float r0 = x0 - __uint_as_float(t[0] << 16), r1 = x1 - __uint_as_float(t[0] & 0xffff0000u);
-    t[1] = pack_bf16_rne(r0, r1);
-    const float q0 = r0 - __uint_as_float(t[1] << 16), q1 = r1 - __uint_as_float(t[1] & 0xffff0000u);
-    t[2] = pack_bf16_rne(q0, q1);
-}
-
 __device__ __forceinline__ void f32_dma16(__amdgpu_buffer_rsrc_t rs, uint32_t lds_addr, uint32_t voff) {
     asm volatile(
         "s_mov_b32 m0, %0\n\t"

@@ -98,6 +98,13 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s);
 // bytes) into the dense dst[d_rows][d_cols] -- transposed (dst[i][j] =
 // src[j][i]) if asked -- with zeros outside the source; d_cols * esize must
 // be a multiple of 16 and dst 16-byte aligned for the plain copy.
+// fp32 operand split into six bf16 K blocks of kp values (terms by the 2-bit
+// fields of pattern: 0 = h, 1 = m, 2 = l).  k_rows = false: src [s_rows][K],
+// dst [d_rows][6 kp] (d_cols = kp); k_rows = true: src [K][s_cols], dst
+// [6 kp][d_cols] (d_rows = kp).  d_cols a multiple of 8, dst 16-byte aligned.
+hipError_t launch_split6(const float* src, int64_t s_rows, int64_t s_cols, int64_t ld, uint16_t* dst,
+                         int64_t d_rows, int64_t d_cols, int64_t kp, bool k_rows, uint32_t pattern, int cus,
+                         hipStream_t s);
 hipError_t launch_pack(const void* src, int64_t s_rows, int64_t s_cols, int64_t ld, void* dst, int64_t d_rows,
                        int64_t d_cols, int esize, bool transpose, int cus, hipStream_t s);
 

@@ -127,6 +127,45 @@ __global__ __launch_bounds__(kPackThreads) void pack_transpose_kernel(const T* _
     }
 }
 
+// fp32 operand split for the bf16-term product (see split3_pair): a source
+// value becomes its three bf16 terms, written into six K blocks of Kp values
+// in the order the 2-bit fields of `pattern` give (0 = h, 1 = m, 2 = l), so
+// that one bf16 product over K' = 6 Kp sums the six significant term
+// products.  Zeros outside the source.  KROWS = false: K is the contiguous
+// source dimension (src [rows][K]); dst [rows][6 Kp], block b at column b Kp.
+// KROWS = true: K is the source row (src [K][cols]); dst [6 Kp][cols], block b
+// at row b Kp.  One 8-value group of a destination row per lane and step.
+template <bool KROWS>
+__global__ __launch_bounds__(kPackThreads) void split6_kernel(const float* __restrict__ src, int64_t s_rows,
+                                                               int64_t s_cols, int64_t ld, uint16_t* __restrict__ dst,
+                                                               int64_t d_rows, int64_t d_cols, int64_t kp,
+                                                               uint32_t pattern, int vec) {
+    const uint32_t upr = (uint32_t)(d_cols / 8), units = (uint32_t)d_rows * upr;
+    for (uint32_t u = blockIdx.x * kPackThreads + threadIdx.x; u < units; u += gridDim.x * kPackThreads) {
+        const uint32_t r = u / upr;
+        const int64_t c0 = (int64_t)(u - r * upr) * 8;
+        float x[8];
+        const float* q = src + (int64_t)r * ld + c0;
+        if (vec && (int64_t)r < s_rows && c0 + 8 <= s_cols) {
+            const float4 a = reinterpret_cast<const float4*>(q)[0], b = reinterpret_cast<const float4*>(q)[1];
+            x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = ((int64_t)r < s_rows && c0 + e < s_cols) ? q[e] : 0.0f;
+        }
+        uint32_t t[4][3];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) split3_pair(x[2 * p], x[2 * p + 1], t[p]);
+#pragma unroll
+        for (int b = 0; b < 6; ++b) {
+            const int term = (pattern >> (2 * b)) & 3;
+            const uint4 v = make_uint4(t[0][term], t[1][term], t[2][term], t[3][term]);
+            const int64_t off = KROWS ? ((int64_t)b * kp + r) * d_cols + c0 : (int64_t)r * 6 * kp + (int64_t)b * kp + c0;
+            *reinterpret_cast<uint4*>(dst + off) = v;
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_pack(const void* src, int64_t s_rows, int64_t s_cols, int64_t ld, void* dst, int64_t d_rows,
@@ -172,6 +211,22 @@ hipError_t launch_pack(const void* src, int64_t s_rows, int64_t s_cols, int64_t 
             else go(pack_copy_kernel<uint32_t, 4>, s32, d32);
         }
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_split6(const float* src, int64_t s_rows, int64_t s_cols, int64_t ld, uint16_t* dst,
+                         int64_t d_rows, int64_t d_cols, int64_t kp, bool k_rows, uint32_t pattern, int cus,
+                         hipStream_t s) {
+    if (d_rows <= 0 || d_cols <= 0) return hipSuccess;
+    const int vec = ((uintptr_t)src % 16 == 0 && (ld * 4) % 16 == 0) ? 1 : 0;
+    const int64_t units = d_rows * (d_cols / 8);
+    const int64_t blocks = std::min<int64_t>((units + kPackThreads - 1) / kPackThreads, (int64_t)cus * 16);
+    if (k_rows)
+        hipLaunchKernelGGL(split6_kernel<true>, dim3((unsigned)blocks), dim3(kPackThreads), 0, s, src, s_rows, s_cols,
+                           ld, dst, d_rows, d_cols, kp, pattern, vec);
+    else
+        hipLaunchKernelGGL(split6_kernel<false>, dim3((unsigned)blocks), dim3(kPackThreads), 0, s, src, s_rows,
+                           s_cols, ld, dst, d_rows, d_cols, kp, pattern, vec);
     return hipGetLastError();
 }
 

@@ -100,7 +100,9 @@ def test_gemm_workspace_query_covers_packing(L, monkeypatch):
     assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 1001, BF16, BF16) == 2 * (2048 * 1024 * 2)
     assert L.isam_gemm_workspace_size(1, 1, 2048, 2048, 1001, BF16, F32) == 2 * (2048 * 1024 * 2)
     assert L.isam_gemm_workspace_size(0, 0, 8192, 8192, 8100, BF16, BF16) == 2 * (8192 * 8128 * 2)
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "f32split=0")
     assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 1001, F32, F32) == 2 * (2048 * 1024 * 4)
+    monkeypatch.delenv("ISAM_GEMM_CONFIG")
     # K = 961: a multiple of 64 (1024) would add more than 1/16, so the vector width (968)
     assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 961, BF16, BF16) == 2 * (2048 * 968 * 2)
     assert L.isam_gemm_workspace_size(0, 0, 2048, 2044, 1024, BF16, BF16) == 2044 * 1024 * 2
@@ -116,6 +118,36 @@ def test_gemm_workspace_query_covers_packing(L, monkeypatch):
     assert L.isam_gemm_workspace_size(0, 0, 100, 100, 101, BF16, BF16) == 0
     monkeypatch.setenv("ISAM_GEMM_CONFIG", "pack=0")
     assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 1001, BF16, BF16) == 0
+
+
+def test_gemm_workspace_query_covers_fp32_split(L, monkeypatch):
+    # Large fp32 products with A [M][K] (B either layout, N a multiple of 8 when B is
+    # [K][N]) run as one bf16 product over six K blocks of each operand's bf16 terms: room
+    # for both split copies (12 bytes per operand value, K per block rounded up to 64 when
+    # that adds at most K/16) plus what that bf16 product uses (here four K slices).
+    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    assert L.isam_gemm_workspace_size(0, 0, 2048, 2048, 1001, F32, F32) == \
+        2 * (2048 * 6 * 1024 * 2) + 4 * 2048 * 2048 * 4
+    assert L.isam_gemm_workspace_size(0, 1, 4096, 4096, 4096, F32, F32) == 2 * (4096 * 6 * 4096 * 2)
+    assert L.isam_gemm_workspace_size(0, 0, 4096, 4096, 4096, F32, BF16) == 2 * (4096 * 6 * 4096 * 2)
+    # not split: A transposed, B [K][N] with N off 8, products whose copies would not pay
+    assert L.isam_gemm_workspace_size(1, 0, 4096, 4096, 4096, F32, F32) == 0
+    assert L.isam_gemm_workspace_size(0, 0, 4096, 4092, 4096, F32, F32) == 0
+    small = L.isam_gemm_workspace_size(0, 0, 512, 512, 512, F32, F32)
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "f32split=0")
+    assert L.isam_gemm_workspace_size(0, 1, 4096, 4096, 4096, F32, F32) == 0
+    assert L.isam_gemm_workspace_size(0, 0, 512, 512, 512, F32, F32) == small
+
+
+def test_gemm_split_workspace_must_not_overlap_operands(L, monkeypatch):
+    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    M, N, K = 4096, 4096, 4096
+    need = L.isam_gemm_workspace_size(0, 1, M, N, K, F32, F32)
+    A, B, C = (ctypes.c_void_p(v) for v in (0x100000000, 0x200000000, 0x300000000))
+    for ws in (C, A, B):
+        assert gemm(L, tb=1, M=M, N=N, K=K, ab=F32, A=A, lda=K, B=B, ldb=K, ct=F32, C=C, ldc=N,
+                    ws=ws, wsb=need) == INVALID
+        assert b"workspace overlaps" in L.isam_last_error()
 
 
 def test_gemm_pack_workspace_must_not_overlap_operands(L, monkeypatch):

@@ -476,8 +476,11 @@ def test_dma_128_tile_copy_modes(K, tb):
 # vector width, a leading dimension or base pointer off 16 bytes) are packed into the
 # workspace with zero-padded K and run on the MFMA kernels; every element against the oracle.
 def _packed_case(M, N, K, dt, ct, ta, tb, monkeypatch, capfd, a_shift=0, ld_pad=0, accumulate=False,
-                 expect_pack=True, workspace=None, seed=0):
-    monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+                 expect_pack=True, workspace=None, seed=0, key="packed operands", env=None):
+    if env is None:
+        monkeypatch.delenv("ISAM_GEMM_CONFIG", raising=False)
+    else:
+        monkeypatch.setenv("ISAM_GEMM_CONFIG", env)
     monkeypatch.setenv("ISAM_LOG", "1")
     Am = synth.uniform(seed, 50, (M, K), -1, 1)
     Bm = synth.uniform(seed, 51, (K, N), -1, 1)
@@ -505,10 +508,11 @@ def _packed_case(M, N, K, dt, ct, ta, tb, monkeypatch, capfd, a_shift=0, ld_pad=
         C = isam.gemm(A, B, trans_a=bool(ta), trans_b=bool(tb), out_dtype=tdt, workspace=workspace)
     torch.cuda.synchronize()
     err_log = capfd.readouterr().err
-    assert ("packed operands" in err_log) == expect_pack, err_log[-2000:]
+    assert (key in err_log) == expect_pack, err_log[-2000:]
     ref, S = oracle.gemm(A_host, B_host, M, N, K, ta, tb, lda=A_host.shape[1], ldb=B_host.shape[1], C_in=C_in)
     tol = TOL_F32 if (dt == "f32" and ct == "f32") else TOL_BF16
-    assert norm_err(to_host_f64(C), ref, S) <= tol
+    err = norm_err(to_host_f64(C), ref, S)
+    assert err <= tol, err
     return C
 
 
@@ -518,8 +522,9 @@ def test_packed_odd_k_every_element(dt, ct, ta, tb, monkeypatch, capfd):
     # K = 1001: both operands padded to K = 1024, A transposed into
     # [M][K] when it is given as [K][M]; 2048^2 takes the 128x128 tiles.  With A [K][M] and
     # B [K][N] no row runs along K: fp32 is then not packed, bf16 only for A's transpose.
+    # (fp32 with the bf16-term split switched off: that path is tested below.)
     _packed_case(2048, 2048, 1001, dt, ct, ta, tb, monkeypatch, capfd,
-                 expect_pack=not (ta and not tb and dt == "f32"))
+                 expect_pack=not (ta and not tb and dt == "f32"), env="f32split=0" if dt == "f32" else None)
 
 
 @pytest.mark.parametrize("case", ["n_ragged", "m_ragged_ta", "ta_aligned", "tt_aligned", "a_shift", "ld_odd",
@@ -560,6 +565,25 @@ def test_packed_needs_workspace_else_tile_kernel(monkeypatch, capfd):
     C0 = _packed_case(M, N, K, "bf16", "bf16", 0, 0, monkeypatch, capfd, expect_pack=False, workspace=tiny)
     C1 = _packed_case(M, N, K, "bf16", "bf16", 0, 0, monkeypatch, capfd)
     assert torch.isfinite(C0.float()).all() and torch.isfinite(C1.float()).all()
+
+
+# Large fp32 products run as one bf16 product over six K blocks of the operands' bf16 terms
+# (A (h, h, m, h, l, m), B (h, m, h, l, h, m)): every element against the oracle at the fp32
+# tolerance, with the fp32 tile kernel (f32split=0) beside it.
+@pytest.mark.parametrize("case", ["nn_ragged_k", "nt", "bf16_out", "accumulate", "a_shift", "nn_4096", "native"])
+def test_fp32_split_every_element(case, monkeypatch, capfd):
+    c = {
+        "nn_ragged_k": dict(M=2048, N=2048, K=1001, tb=0),   # K per block 1024, four K slices after
+        "nt": dict(M=2048, N=2048, K=1024, tb=1),
+        "bf16_out": dict(M=2048, N=2048, K=1024, tb=0, ct="bf16"),
+        "accumulate": dict(M=2048, N=2048, K=1000, tb=1, accumulate=True),
+        "a_shift": dict(M=2048, N=2048, K=1024, tb=0, a_shift=1),  # A 4 bytes past 16: element reads
+        "nn_4096": dict(M=4096, N=4096, K=4096, tb=0),
+        "native": dict(M=2048, N=2048, K=1024, tb=0, env="f32split=0", expect_pack=False),
+    }[case]
+    kw = {k: v for k, v in c.items() if k not in ("M", "N", "K", "tb", "ct")}
+    _packed_case(c["M"], c["N"], c["K"], "f32", c.get("ct", "f32"), 0, c["tb"], monkeypatch, capfd,
+                 key="fp32 split into bf16 terms", **kw)
 
 
 # Very shallow bf16 products (K <= 256, N <= 256 with N % 4 == 0, A and B not transposed): the
