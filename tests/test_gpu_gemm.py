@@ -361,16 +361,17 @@ def _guarded_gemm(M, N, K, dt, ct, pad_cols, seed, tb=0, env=None, monkeypatch=N
 
 
 GUARD_CASES = ["dma256", "dma256_split", "dma256_split_sum", "dma128", "dma_sk", "skinny_rows", "skinny_split",
-               "narrow", "stream", "tile_f32", "small", "packed"]
+               "narrow", "stream", "tile_f32", "small", "packed", "f32_split"]
 
 
 @pytest.mark.parametrize("ct", ["f32", "bf16"])
 @pytest.mark.parametrize("case", GUARD_CASES)
 def test_guard_bands_every_kernel(ct, case, monkeypatch):
     # Each GEMM kernel writes exactly its M x N block: the direct-to-LDS kernels (256x256
-    # whole and split along K, 128x128, the stream-K schedule), the skinny kernels (one pass and split-K), the
-    # narrow dot-product kernel, the streaming kernel, the fp32 tile kernel and the small-
-    # product kernel, with C rows padded (ldc > N).
+    # whole and split along K, 128x128, the stream-K schedule), the skinny kernels (one pass
+    # and split-K), the narrow dot-product kernel, the streaming kernel, the fp32 tile kernel,
+    # the small-product kernel, and the products on operands packed or split into bf16 terms
+    # in the workspace, with C rows padded (ldc > N).
     cases = {
         "dma256": dict(M=520, N=776, K=640, dt="bf16", env="tile=0,dma=1,dmaw=8"),
         "dma256_split": dict(M=520, N=776, K=640, dt="bf16", env="tile=0,dma=1,dmaw=8,splits=2"),
@@ -384,6 +385,7 @@ def test_guard_bands_every_kernel(ct, case, monkeypatch):
         "tile_f32": dict(M=300, N=200, K=130, dt="f32", env=None),
         "small": dict(M=100, N=64, K=520, dt="f32", env=None),
         "packed": dict(M=2048, N=2040, K=1001, dt="bf16", env=None),
+        "f32_split": dict(M=2048, N=2040, K=1000, dt="f32", env=None),
     }
     c = cases[case]
     _guarded_gemm(c["M"], c["N"], c["K"], c["dt"], ct, pad_cols=8, seed=100 + GUARD_CASES.index(case),
@@ -528,7 +530,7 @@ def test_packed_odd_k_every_element(dt, ct, ta, tb, monkeypatch, capfd):
 
 
 @pytest.mark.parametrize("case", ["n_ragged", "m_ragged_ta", "ta_aligned", "tt_aligned", "a_shift", "ld_odd",
-                                  "accumulate", "deep_k", "k_vector_pad"])
+                                  "accumulate", "deep_k", "k_vector_pad", "k3", "k13_nt"])
 def test_packed_layouts_every_element(case, monkeypatch, capfd):
     c = {
         # B [K][N] with N off the vector width: packed transposed to [N][K]
@@ -547,6 +549,9 @@ def test_packed_layouts_every_element(case, monkeypatch, capfd):
         "deep_k": dict(M=1024, N=1024, K=4101, ta=0, tb=0),
         # K padded to the vector width only (968; 1024 would add more than 1/16)
         "k_vector_pad": dict(M=2048, N=2048, K=961, ta=0, tb=1),
+        # K below one 64-deep tile: padded to 8 / 16, one ragged K tile
+        "k3": dict(M=4096, N=4096, K=3, ta=0, tb=0),
+        "k13_nt": dict(M=4096, N=4096, K=13, ta=0, tb=1),
     }[case]
     kw = {k: v for k, v in c.items() if k not in ("M", "N", "K", "ta", "tb")}
     if case in ("a_shift", "ld_odd"):
@@ -570,7 +575,8 @@ def test_packed_needs_workspace_else_tile_kernel(monkeypatch, capfd):
 # Large fp32 products run as one bf16 product over six K blocks of the operands' bf16 terms
 # (A (h, h, m, h, l, m), B (h, m, h, l, h, m)): every element against the oracle at the fp32
 # tolerance, with the fp32 tile kernel (f32split=0) beside it.
-@pytest.mark.parametrize("case", ["nn_ragged_k", "nt", "bf16_out", "accumulate", "a_shift", "nn_4096", "native"])
+@pytest.mark.parametrize("case", ["nn_ragged_k", "nt", "bf16_out", "accumulate", "a_shift", "nn_4096", "native",
+                                  "k5", "n_ragged_nt"])
 def test_fp32_split_every_element(case, monkeypatch, capfd):
     c = {
         "nn_ragged_k": dict(M=2048, N=2048, K=1001, tb=0),   # K per block 1024, four K slices after
@@ -580,6 +586,10 @@ def test_fp32_split_every_element(case, monkeypatch, capfd):
         "a_shift": dict(M=2048, N=2048, K=1024, tb=0, a_shift=1),  # A 4 bytes past 16: element reads
         "nn_4096": dict(M=4096, N=4096, K=4096, tb=0),
         "native": dict(M=2048, N=2048, K=1024, tb=0, env="f32split=0", expect_pack=False),
+        # K = 5: six blocks of 8 (bf16 K' = 48, one ragged K tile)
+        "k5": dict(M=4096, N=4096, K=5, tb=0),
+        # B as [N][K] with N off 8 (allowed: K runs along B's rows)
+        "n_ragged_nt": dict(M=2048, N=2044, K=1024, tb=1),
     }[case]
     kw = {k: v for k, v in c.items() if k not in ("M", "N", "K", "tb", "ct")}
     _packed_case(c["M"], c["N"], c["K"], "f32", c.get("ct", "f32"), 0, c["tb"], monkeypatch, capfd,
