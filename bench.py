@@ -8,7 +8,7 @@ HBM:
   * GRU forward T=64, batch 32, input = hidden = 1024, bf16 weights (also T=128 and batch 4)
   * separable depthwise conv 32 x 56 x 56 x 128 -> 256, bf16 (fp32 out) and fp32
   * 1D convolution 32 sequences x 1024 positions, 512 -> 512 channels, 5 taps, bf16 (fp32 out)
-  * fp32 GEMM 128^3
+  * fp32 GEMM 128^3; as context, fp32 GEMM 4096^3 (run as six bf16 term products)
 Each part is bracketed by HIP events on the stream the library launches on (torch's current
 stream), so the per-part times are device times; after the timed steps each part also runs
 alone, calls queued back to back between two events ("us_b2b": device time per call without
@@ -103,6 +103,7 @@ def main():
     import torch
 
     import paper_1810_09958_amd as isam
+    import synth
     from synth import workloads
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -302,6 +303,14 @@ def main():
     if want("gemm_128x128x128_f32"):
         comps.append(("gemm_128x128x128_f32", lambda: isam.gemm(A1, B1, C1, workspace=ws1),
                       {"kind": "gemm_f32", "flop": 2.0 * 128 ** 3, "bytes": 3 * 4 * 128 * 128}))
+    # -- large fp32 GEMM (context): the bf16-term split path ------------------------------
+    if want("gemm_4096x4096x4096_f32_ctx"):
+        A4 = gpu(synth.uniform(4096, 60, (4096, 4096), -1, 1))
+        B4 = gpu(synth.uniform(4096, 61, (4096, 4096), -1, 1))
+        C4 = torch.empty((4096, 4096), device=dev)
+        ws4 = torch.empty(max(1, isam.gemm_workspace_size(4096, 4096, 4096, 0, 0)), device=dev, dtype=torch.uint8)
+        comps.append(("gemm_4096x4096x4096_f32_ctx", lambda: isam.gemm(A4, B4, C4, workspace=ws4),
+                      {"kind": "gemm_f32_split", "flop": 2.0 * 4096 ** 3, "bytes": 3 * 4 * 4096 * 4096}))
     torch.cuda.synchronize()
     t_setup = time.time() - t_setup
 
@@ -376,6 +385,9 @@ def main():
             r["frac_bf16_peak"] = round(tfl / PEAK_BF16_TFLOPS, 4)
         elif info["kind"] == "gemm_f32":
             r["frac_f32_peak"] = round(tfl / PEAK_F32_TFLOPS, 6)
+        elif info["kind"] == "gemm_f32_split":
+            # six bf16 products per fp32 product on the bf16 matrix cores
+            r["frac_bf16_peak_of_term_products"] = round(6 * tfl / PEAK_BF16_TFLOPS, 4)
         elif info["kind"] in ("skinny", "dwsep"):
             r["frac_hbm_peak"] = round(gbs / PEAK_HBM_GBPS, 4)
         us_b, R = b2b[name]
