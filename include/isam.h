@@ -73,7 +73,9 @@ typedef enum {
  * count, K a multiple of 64, workspace 256-byte aligned): the second slice
  * waits for the first's flag in the workspace (a bounded wait; if it ever
  * expires the tile's outputs are NaN) and adds its partial sums in a fixed
- * order, so results stay deterministic.  Other split plans sum the slices
+ * order, so results stay deterministic; when every workgroup of the grid is
+ * resident at once, each slice instead finishes half of the tile's rows with
+ * the other slice's partial sums for that half (the same sums).  Other split plans sum the slices
  * in a second kernel.  bf16 products whose tile count leaves most compute
  * units idle in a last partial round (A not transposed, 16-byte aligned
  * rows, workspace 256-byte aligned) run a stream-K schedule instead

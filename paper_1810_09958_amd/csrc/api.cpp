@@ -7,7 +7,7 @@
 // device's compute-unit count, and can be overridden for tuning with the
 // environment variable ISAM_GEMM_CONFIG="tile=<0-5>,splits=<n>,group=<n>,xcd=<0|1>,dma=<0|1>"
 // (and small=0, rows=0, skinny=0, stream=0|1 for the special-shape kernels, sk=0|1 for
-// the stream-K schedule, fixup=0 for the two-slice sum).
+// the stream-K schedule, fixup=0 for the two-slice sum, fixup=1 for its one-way form).
 // ISAM_LOG=1 prints each chosen plan to stderr.
 #include <hip/hip_runtime.h>
 
@@ -257,10 +257,17 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int ab_type, int cus, bool a
     // one XCD (workgroups are dealt to the XCDs in turn, 32 CUs each): the
     // second slice sums the pair through that XCD's L2, with no reduction
     // pass.  ISAM_GEMM_CONFIG fixup=0 keeps the pass.
+    // When the whole grid (both slices of every tile) fits on the CUs at once,
+    // the slices split the finishing work instead: each publishes the half
+    // tile the other finishes and waits for the other's half (fixup = 2;
+    // 8192x1024x16384 bf16: 128 tiles, 256 workgroups).
     const int xcds = cus % 32 == 0 ? cus / 32 : 1;
-    if (p.k_splits == 2 && p.tile == kTile256x256 && tiles(kTile256x256) % xcds == 0) p.fixup = 1;
-    if (const char* env = getenv("ISAM_GEMM_CONFIG"))
+    if (p.k_splits == 2 && p.tile == kTile256x256 && tiles(kTile256x256) % xcds == 0)
+        p.fixup = 2 * tiles(kTile256x256) <= cus ? 2 : 1;
+    if (const char* env = getenv("ISAM_GEMM_CONFIG")) {
         if (strstr(env, "fixup=0")) p.fixup = 0;
+        if (strstr(env, "fixup=1") && p.fixup) p.fixup = 1;
+    }
     // Stream-K (bf16, the three-stage-ring tiles, no K split): a persistent
     // grid; each XCD's range of tiles runs its whole rounds one tile per
     // workgroup, then deals the remaining tiles' (tile, K tile) units to its

@@ -215,7 +215,11 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     t.xcd_remap = p.xcd_remap;
     t.k_per_split = p.k_splits > 1 ? p.k_per_split : a.K;
     if (t.k_per_split <= 0) t.k_per_split = 1;
-    t.fixup = fixup ? 1 : 0;
+    // The symmetric form waits in both slices, so it needs every workgroup
+    // resident at once (the plan has checked that the grid is within the CU
+    // count); the one-way form's first slice never waits.
+    t.fixup = fixup ? ((p.fixup == 2 && resident_per_cu(reinterpret_cast<const void*>(fn), threads, 0) >= 1) ? 2 : 1)
+                    : 0;
     t.epoch = fixup ? next_fixup_epoch() : 0;
     t.expect = t.epoch;
     t.wait_ticks = kFixupTimeoutTicks;
@@ -233,7 +237,8 @@ hipError_t launch_gemm(const GemmArgs& a, const GemmPlan& p, hipStream_t s) {
     dim3 block(threads);
     if (fixup) {
         const char* v = getenv("ISAM_LOG");
-        if (v && *v && *v != '0') fprintf(stderr, "[isam] two K slices summed in the kernel\n");
+        if (v && *v && *v != '0')
+            fprintf(stderr, "[isam] two K slices summed in the kernel%s\n", t.fixup == 2 ? " (each slice finishes half)" : "");
     }
     hipLaunchKernelGGL(fn, grid, block, 0, s, a, t);
     hipError_t e = hipGetLastError();

@@ -341,9 +341,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t partial_rsrc(float* base, int 
 }
 // Stores the accumulators, waits until every wave's stores are in L2, then
 // raises the flag to `epoch`.
+// This wave's accumulators into its part of the tile's partial-sum area
+// (workgroup-scope write-through, so they sit in the XCD's L2), then a wait
+// until they are there.
 template <int MI, int NI>
-__device__ __forceinline__ void partial_publish(const f32x16_t (&acc)[MI][NI], __amdgpu_buffer_rsrc_t rp,
-                                                __amdgpu_buffer_rsrc_t rf, uint64_t epoch, int wid, int lane) {
+__device__ __forceinline__ void partial_store(const f32x16_t (&acc)[MI][NI], __amdgpu_buffer_rsrc_t rp, int wid,
+                                              int lane) {
     const int vo = lane * 16, wbase = wid * MI * NI * 4 * 1024;
     static_for<MI>([&](auto i) {
         static_for<NI>([&](auto j) {
@@ -356,7 +359,12 @@ __device__ __forceinline__ void partial_publish(const f32x16_t (&acc)[MI][NI], _
             });
         });
     });
-    vm_wait<0>();  // this wave's pieces are in L2
+    vm_wait<0>();
+}
+template <int MI, int NI>
+__device__ __forceinline__ void partial_publish(const f32x16_t (&acc)[MI][NI], __amdgpu_buffer_rsrc_t rp,
+                                                __amdgpu_buffer_rsrc_t rf, uint64_t epoch, int wid, int lane) {
+    partial_store<MI, NI>(acc, rp, wid, lane);  // this wave's pieces are in L2
     __syncthreads();
     if (threadIdx.x == 0) {
         const uint2 e = make_uint2((uint32_t)epoch, (uint32_t)(epoch >> 32));
@@ -665,6 +673,30 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_dma_kernel(GemmArgs a, Tile
         // Both slices of a tile run on one XCD (the host enables this only
         // when they do), so the exchange goes through that XCD's L2.
         const __amdgpu_buffer_rsrc_t rp = partial_rsrc<BM, BN>(a.partial, blockIdx.x);
+        if (tmap.fixup == 2) {
+            // Each slice finishes the rows of one wave row (slice s: wave row
+            // s); its other waves publish their partial sums for the other
+            // slice.  a + b = b + a in fp32, so every output is the same sum
+            // as in the one-way form.
+            static_assert(WM == 2, "the two slices split the tile by wave rows");
+            const int y = blockIdx.y;
+            const bool mine = wm == y;
+            uint64_t* line = tmap.flags + (size_t)blockIdx.x * 16;
+            const __amdgpu_buffer_rsrc_t rf_own = make_rsrc(line + 8 * y, 64), rf_other = make_rsrc(line + 8 * (1 - y), 64);
+            if (!mine) partial_store<MI, NI>(acc, rp, wid, lane);  // waits for its stores
+            __syncthreads();  // every wave is done with the stages and its stores are in L2
+            if (threadIdx.x == 0) {
+                const uint2 e = make_uint2((uint32_t)tmap.epoch, (uint32_t)(tmap.epoch >> 32));
+                __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((ext_vector_type(2))) int, e),
+                                                      rf_own, 0, 0, 1);
+            }
+            const bool ok = partial_wait(rf_other, tmap.expect, tmap.wait_ticks, reinterpret_cast<int*>(smem));
+            if (!mine) return;
+            if (ok) partial_add<MI, NI>(acc, rp, wid, lane);
+            else acc_fill_nan<MI, NI>(acc);
+            store_acc_tile<MI, NI, WTM, WTN, NW>(a, acc, smem, m0, n0, wm, wn, wid, lane, FIX);
+            return;
+        }
         const __amdgpu_buffer_rsrc_t rf = make_rsrc(tmap.flags + (size_t)blockIdx.x * 16, 128);
         if (blockIdx.y == 0) {
             partial_publish<MI, NI>(acc, rp, rf, tmap.epoch, wid, lane);

@@ -141,9 +141,12 @@ struct TileMapArgs {
     int tiles_m, tiles_n, group_m, xcd_remap;
     int64_t k_per_split;
     // Two K slices summed inside the kernel (256x256 direct-to-LDS kernel
-    // only): slice 0 leaves its accumulators in `partial` and raises
-    // flags[tile] (one 128-byte line per tile) to `epoch`; slice 1 adds them
-    // and writes C.
+    // only).  fixup = 1: slice 0 leaves its accumulators in `partial` and
+    // raises flags[tile] (one 128-byte line per tile) to `epoch`; slice 1 adds
+    // them and writes C.  fixup = 2 (every workgroup resident): slice s
+    // finishes the rows of wave row s; its other waves leave their
+    // accumulators in `partial` and it raises its own flag (word 8 s of the
+    // line), then waits for the other slice's.
     int fixup;
     uint64_t epoch;          // value slice 0 writes
     uint64_t expect;         // value slice 1 waits for (== epoch but in the timeout test)

@@ -51,6 +51,7 @@ struct GemmPlan {
     int dma;         // 1: direct-to-LDS kernel where it applies (bf16, A K-contiguous, vec)
     int dma_waves;   // 4 or 8 waves per workgroup for the direct-to-LDS kernel
     int fixup;       // 1: a two-slice split on 256x256 tiles may sum its slices inside the kernel
+                     // 2: the same, each slice finishing half of the tile (whole grid resident)
     int skinny;      // 1: streaming kernel for N <= 32 (k_splits = K slices of skinny_k_slice);
                      // 2: bf16 row-streaming kernel (16 rows per workgroup, whole K, no split);
                      // 4: narrow dot-product kernel (N < 8, not a multiple of the vector width)

@@ -182,11 +182,14 @@ def test_config_large_bf16_every_element(which):
 # 8 (the condition for the in-kernel sum), ragged M and N, both B layouts, both output
 # types, accumulate, repeated calls on one workspace; K with a ragged last tile takes the
 # reduction pass instead.  Every element against the oracle.
+# Both forms: each slice finishing half of the tile (every workgroup resident: the default
+# here) and the one-way form (fixup=1: slice 1 finishes the whole tile).
 @pytest.mark.parametrize("shape,in_kernel", [((512, 1024, 1280), True), ((500, 1000, 1280), True),
                                              ((512, 1024, 1200), False)])
 @pytest.mark.parametrize("tb", [0, 1])
-def test_split_sum_in_kernel_every_element(shape, in_kernel, tb, monkeypatch, capfd):
-    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,dmaw=8,splits=2")
+@pytest.mark.parametrize("form", ["halves", "one_way"])
+def test_split_sum_in_kernel_every_element(shape, in_kernel, tb, form, monkeypatch, capfd):
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,dmaw=8,splits=2" + (",fixup=1" if form == "one_way" else ""))
     monkeypatch.setenv("ISAM_LOG", "1")
     M, N, K = shape
     for rep in range(2):
@@ -195,13 +198,15 @@ def test_split_sum_in_kernel_every_element(shape, in_kernel, tb, monkeypatch, ca
     _run_case(M, N, K, "bf16", "f32", tb=tb, accumulate=True, seed=M + K + 7)
     log = capfd.readouterr().err
     assert ("two K slices summed in the kernel" in log) == in_kernel
+    assert ("each slice finishes half" in log) == (in_kernel and form == "halves")
 
 
-def test_split_sum_in_kernel_timeout_gives_nan(monkeypatch):
-    # The second slice's wait for the first is bounded; the host forces it to expire (the
-    # slice waits for a flag value that is never written, under a 1 ms bound): every output is
-    # NaN, and the next call on the same workspace is correct again.
-    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,dmaw=8,splits=2")
+@pytest.mark.parametrize("form", ["halves", "one_way"])
+def test_split_sum_in_kernel_timeout_gives_nan(form, monkeypatch):
+    # The slices' waits are bounded; the host forces them to expire (each waits for a flag
+    # value that is never written, under a 1 ms bound): every output is NaN, and the next
+    # call on the same workspace is correct again.
+    monkeypatch.setenv("ISAM_GEMM_CONFIG", "tile=0,dma=1,dmaw=8,splits=2" + (",fixup=1" if form == "one_way" else ""))
     M, N, K = 512, 1024, 1280
     A_h = bits(synth.uniform(3, 10, (M, K), -1, 1))
     B_h = bits(synth.uniform(3, 11, (K, N), -1, 1))
