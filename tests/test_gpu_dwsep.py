@@ -203,3 +203,28 @@ def test_fused_f32_row_ranges_cross_images():
     _case(40, 9, 16, 64, 48, dt="f32", ot="f32", seed=21)
     _case(20, 30, 8, 32, 16, dt="f32", ot="f32", seed=22)
     _case(6, 56, 56, 128, 256, dt="f32", ot="f32", seed=23)
+
+
+# Input and output just under the 2^31-byte limit of the 32-bit buffer offsets, on the fused
+# kernels (bf16: 2674 images of 56 x 56 x 128; fp32: 1337).  X is a 16-image random block
+# repeated along the batch; the oracle checks sampled images, the last ones among them.
+@pytest.mark.parametrize("dt,batch", [("bf16", 2674), ("f32", 1337)])
+def test_fused_at_the_extent_limit(dt, batch):
+    H = W = 56
+    C = Co = 128
+    es = 2 if dt == "bf16" else 4
+    assert batch * H * W * C * es < 2 ** 31 and batch * H * W * C * es > 2 ** 31 - 2 ** 22
+    blk = synth.normal(batch, 0, (16, H, W, C))
+    D = synth.uniform(batch, 1, (3, 3, C, 1), -1 / 3, 1 / 3)
+    P = synth.uniform(batch, 2, (C, Co), -1 / 11, 1 / 11)
+    if dt == "bf16":
+        blk, D, P = bits(blk), bits(D), bits(P)
+    X = to_gpu(blk).repeat(batch // 16 + 1, 1, 1, 1)[:batch].contiguous()
+    y = isam.dwsep_conv(X, to_gpu(D), to_gpu(P), out_dtype=torch.bfloat16 if dt == "bf16" else torch.float32)
+    torch.cuda.synchronize()
+    imgs = [0, 1, batch // 2, batch - 2, batch - 1]
+    Z, S = oracle.dwsep(np.ascontiguousarray(blk[[i % 16 for i in imgs]]), D, P)
+    got = to_host_f64(y[torch.as_tensor(imgs, device="cuda")])
+    assert norm_err(got, Z, S) <= (TOL_BF16 if dt == "bf16" else TOL_F32)
+    del X, y
+    torch.cuda.empty_cache()

@@ -625,3 +625,28 @@ def test_stream_kernel_planned(shape, monkeypatch):
     monkeypatch.setenv("ISAM_GEMM_CONFIG", "stream=0")
     e_tile = _run_case(M, N, K, "bf16", "f32", seed=M)
     assert e_stream <= TOL_BF16 and e_tile <= TOL_BF16
+
+
+# A operand just under the 2^31-byte limit of the 32-bit buffer offsets: bf16 65536 x 16376
+# (direct-to-LDS 256x256 kernel, ragged last K tile) and fp32 65536 x 8188 (fp32 tile kernel:
+# its split copies would pass the limit).  A is a 4096-row random block repeated down the
+# rows; the oracle checks sampled rows, the last ones (largest offsets) among them.
+@pytest.mark.parametrize("dt,K", [("bf16", 16376), ("f32", 8188)])
+def test_operand_at_the_extent_limit(dt, K):
+    M, N = 65536, 256
+    es = 2 if dt == "bf16" else 4
+    assert M * K * es < 2 ** 31 and M * K * es > 2 ** 31 - 2 ** 22
+    blk = synth.uniform(K, 70, (4096, K), -1, 1)
+    Bm = synth.uniform(K, 71, (K, N), -1, 1)
+    if dt == "bf16":
+        blk, Bm = bits(blk), bits(Bm)
+    A = to_gpu(blk).repeat(M // 4096, 1)
+    C = isam.gemm(A, to_gpu(Bm))
+    torch.cuda.synchronize()
+    rows = [0, 1, 4095, 4096, 32767, 40000, 65534, 65535]
+    A_rows = np.ascontiguousarray(blk[[r % 4096 for r in rows]])
+    ref, S = oracle.gemm(A_rows, Bm, len(rows), N, K)
+    got = to_host_f64(C[torch.as_tensor(rows, device="cuda")])
+    assert norm_err(got, ref, S) <= (TOL_BF16 if dt == "bf16" else TOL_F32)
+    del A, C
+    torch.cuda.empty_cache()
